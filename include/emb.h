@@ -1,0 +1,170 @@
+/*
+ * emb.h -- C ABI of one GPU's shard of a pooled sparse embedding layer
+ * (MI355X / gfx950, HIP).
+ *
+ * The layer: a recommendation model's large sparse embedding lookup layer,
+ * which turns massive high-dimensional sparse ids into dense features and is
+ * the part of the model with a high data-access cost (paper: Introduction;
+ * Section "Multi-mode Execution", heterogeneous pipeline paragraph, where it
+ * forms the embedding stage that pulls rows forward and pushes sparse
+ * updates back).  The paper states the layer only in words; the operations
+ * below are the plain definitions of a bag-pooled embedding lookup and its
+ * training step:
+ *
+ *   key(j)   = row_offset[t(j)] + indices[j]                 (global row)
+ *   out[m]   = scale_m * sum_{j in bag m} W[key(j)]           (forward)
+ *   grad W_r = sum_{j : key(j) = r} scale_{m(j)} * G[m(j)]    (backward)
+ *   W_r     <- opt(W_r, grad W_r) for every touched row r     (update)
+ *
+ * with scale_m = 1 (sum pooling) or 1/L_m (mean pooling), L_m the length of
+ * bag m, and an empty bag pooling to zero.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers are DEVICE pointers unless marked "host".  The caller
+ *    allocates and frees every buffer, including the workspace; the library
+ *    allocates no memory, keeps no pointer after returning and holds no state
+ *    between calls apart from its loaded code.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Every call only enqueues work on it; nothing synchronises.  Buffers must
+ *    stay alive until the stream has reached the enqueued work.
+ *  - Host-checkable problems return an error before anything is enqueued.
+ *    Device-content errors (an id >= rows of its table, decreasing offsets,
+ *    offsets[M] != num_indices) are undefined behaviour on the fast path:
+ *    emb_validate_batch detects them.
+ *  - For identical inputs every output is bitwise identical from run to run
+ *    (no floating-point atomics).
+ *  - Calls that share a workspace must be ordered (same stream or events);
+ *    calls with disjoint buffers may run concurrently on different streams.
+ */
+#ifndef EMB_H
+#define EMB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EMB_OK = 0,
+  EMB_EINVAL = 1,       /* null pointer, negative size, bad enum, bad table layout */
+  EMB_EWORKSPACE = 2,   /* ws_bytes < emb_workspace_size(...) or misaligned workspace */
+  EMB_EUNSUPPORTED = 3, /* dim*sizeof(dtype) not a multiple of 16, total rows >= 2^32,
+                           num_indices >= 2^30, more than EMB_MAX_TABLES tables */
+  EMB_EHIP = 4          /* a kernel launch failed (hipGetLastError) */
+} emb_status;
+
+typedef enum { EMB_FP32 = 0, EMB_BF16 = 1 } emb_dtype;
+typedef enum { EMB_POOL_SUM = 0, EMB_POOL_MEAN = 1 } emb_pool;
+typedef enum { EMB_OPT_SGD = 0, EMB_OPT_ADAGRAD_ROWWISE = 1 } emb_opt;
+
+#define EMB_MAX_TABLES 256
+
+/* All tables of one call share dim and dtype and are stacked row-wise in one
+ * buffer: the rows of table t are global rows row_offset[t] .. row_offset[t+1]-1. */
+typedef struct {
+  int32_t num_tables;        /* T, 1 <= T <= EMB_MAX_TABLES */
+  const int64_t* row_offset; /* host [T+1]; row_offset[0] = 0, nondecreasing, row_offset[T] = R < 2^32 */
+  int32_t dim;               /* D >= 1 with D * sizeof(dtype) a multiple of 16 bytes */
+  int32_t dtype;             /* emb_dtype */
+  void* weights;             /* device [R][D] row-major, 16-byte aligned */
+} emb_tables;
+
+/* One batch: M = T * bags_per_table bags, table-major (bag m belongs to table
+ * m / bags_per_table), given in CSR form. */
+typedef struct {
+  int32_t bags_per_table;    /* B >= 0 */
+  const int32_t* offsets;    /* device [M+1]; offsets[0] = 0, nondecreasing, offsets[M] = num_indices */
+  const int32_t* indices;    /* device [N]; table-local ids, 0 <= id < rows of the bag's table */
+  int64_t num_indices;       /* N, host value, 0 <= N < 2^30 */
+} emb_batch;
+
+/* Optimizer of one sparse step.
+ *   SGD:               W_r <- W_r - lr * g_r
+ *   row-wise Adagrad:  h_r <- h_r + (1/D) sum_d g_r[d]^2
+ *                      W_r <- W_r - lr * g_r / (sqrt(h_r) + eps)
+ * Arithmetic is fp32; bf16 tables store the fp32 result rounded to nearest even. */
+typedef struct {
+  int32_t opt;    /* emb_opt */
+  float lr;
+  float eps;      /* Adagrad only */
+  float* state;   /* device [R] fp32 accumulators h (Adagrad), NULL for SGD */
+} emb_update;
+
+/* Forward: out[m][d] = scale_m * sum over bag m of W[key(j)][d], fp32
+ * accumulation (bf16 rows are widened exactly).  out: device fp32 [M][D],
+ * fully overwritten (empty bags get zeros).  The layer's forward as defined
+ * above (paper: Introduction, the sparse-ids-to-dense-features layer). */
+emb_status emb_pool_fwd(const emb_tables* tables, const emb_batch* batch, int32_t pool, float* out,
+                        void* stream);
+
+/* Bytes of workspace that emb_unique_ids / emb_grad_reduce need for batches
+ * of up to num_indices ids and num_bags bags, rows of dim floats.  Returns 0
+ * for invalid sizes. */
+size_t emb_workspace_size(int64_t num_indices, int64_t num_bags, int32_t dim);
+
+/* Zero-fill a freshly allocated workspace (enqueued on stream).  Must run once
+ * before the workspace's first use; every later call leaves the workspace's
+ * internal counters back at their initial values when its work completes. */
+emb_status emb_workspace_init(void* ws, size_t ws_bytes, void* stream);
+
+/* Dedup of the batch's ids, the step that makes the sparse update race-free:
+ *   key[j]          = row_offset[t(j)] + indices[j]   (uint32)
+ *   sort_perm       = the stable ascending sort of positions 0..N-1 by key
+ *                     (equal keys keep position order), device int32 [N]
+ *   num_unique[0]   = U, the number of distinct keys, device int32 [1]
+ *   unique_keys[u]  = the u-th smallest distinct key, device uint32 [>= N]
+ *   seg_offsets[u]  = first sorted position of unique_keys[u];
+ *                     seg_offsets[U] = N, device int32 [>= N+1]
+ *   counts[u]       = seg_offsets[u+1] - seg_offsets[u], device int32 [>= N]
+ * Only the first U entries (U+1 of seg_offsets) are written.  ws (device,
+ * 256-byte aligned, ws_bytes >= emb_workspace_size(N, M, D)) also receives
+ * the per-position bag ids and sorted keys that emb_grad_reduce reads. */
+emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys, int32_t* counts,
+                          int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* Backward segment-reduce, optionally fused with the optimizer step:
+ *   g_u[d] = sum over sorted positions k in segment u of scale_{m(k)} * grad_out[m(k)][d],
+ * m(k) the bag holding position sort_perm[k], in a fixed order per segment
+ * (deterministic, no float atomics).  grad_out: device fp32 [M][D].
+ * grad_rows: device fp32 [>= N][D] receiving g_u for u < U, or NULL.
+ * fuse: NULL = reduce only (grad_rows required); otherwise the optimizer step
+ * is applied to tables->weights (and fuse->state) on rows unique_keys[u],
+ * each row by exactly one owner, so the update is race-free.
+ * sort_perm, seg_offsets, unique_keys, num_unique and ws must be those that
+ * emb_unique_ids produced for this same batch, unmodified. */
+emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* grad_out,
+                           const int32_t* sort_perm, const int32_t* seg_offsets, const uint32_t* unique_keys,
+                           const int32_t* num_unique, float* grad_rows, const emb_update* fuse, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* Unfused optimizer step: for u < num_unique[0], row r = unique_keys[u] gets
+ * opt(W_r, grad_rows[u]) as defined for emb_update.  max_unique (host) bounds
+ * num_unique[0] (the batch's N is a valid bound).  unique_keys must be
+ * distinct (one owner per row). */
+emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update, const uint32_t* unique_keys,
+                             const int32_t* num_unique, int64_t max_unique, const float* grad_rows, void* stream);
+
+/* Debug check of device contents (never on the timed path): flag[0] (device
+ * int32) is set to 0 if the batch is well formed, else to a bitwise OR of
+ * 1 (offsets[0] != 0), 2 (decreasing offsets), 4 (offsets[M] != N),
+ * 8 (an id out of range of its table). */
+emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, int32_t* flag, void* stream);
+
+/* Device-side error word of a workspace (host-readable after a copy): bit 0 is
+ * set if a bounded spin-wait inside a look-back scan ran out, bit 1 if a sort
+ * pass found digit totals inconsistent with its keys (a workspace that was not
+ * initialised); results of that call are then undefined and the word stays
+ * set until the workspace is initialised again.  Offset in bytes from the
+ * workspace base. */
+size_t emb_workspace_error_offset(void);
+
+const char* emb_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMB_H */

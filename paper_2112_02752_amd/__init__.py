@@ -1,0 +1,231 @@
+"""MI355X-native shard of a pooled sparse embedding layer.
+
+Thin ctypes binding over ``libemb.so`` (HIP kernels for gfx950, C ABI in
+``include/emb.h``).  This module only marshals arguments: every step of the
+layer runs in the library's kernels.  PyTorch provides device memory and
+streams; tensors are passed by ``data_ptr()`` and the current HIP stream.
+
+The layer is the one the paper's introduction names as the high data-access
+part of a recommendation model, turning sparse ids into dense features
+(Introduction; Section "Multi-mode Execution", heterogeneous pipeline).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libemb.so")
+
+EMB_OK, EMB_EINVAL, EMB_EWORKSPACE, EMB_EUNSUPPORTED, EMB_EHIP = range(5)
+FP32, BF16 = 0, 1
+POOL = {"sum": 0, "mean": 1}
+OPT = {"sgd": 0, "adagrad": 1}
+DTYPE = {"fp32": FP32, "bf16": BF16}
+
+EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_grad_reduce",
+            "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_status_string")
+
+
+class EmbError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {_status_string(status)} (status {status})")
+
+
+class CTables(ctypes.Structure):
+    _fields_ = [("num_tables", ctypes.c_int32), ("row_offset", ctypes.POINTER(ctypes.c_int64)),
+                ("dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("weights", ctypes.c_void_p)]
+
+
+class CBatch(ctypes.Structure):
+    _fields_ = [("bags_per_table", ctypes.c_int32), ("offsets", ctypes.c_void_p), ("indices", ctypes.c_void_p),
+                ("num_indices", ctypes.c_int64)]
+
+
+class CUpdate(ctypes.Structure):
+    _fields_ = [("opt", ctypes.c_int32), ("lr", ctypes.c_float), ("eps", ctypes.c_float),
+                ("state", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libemb.so; raises if it is not built (there is no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(the embedding layer has no non-HIP implementation)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        T, B, Up = ctypes.POINTER(CTables), ctypes.POINTER(CBatch), ctypes.POINTER(CUpdate)
+        L.emb_pool_fwd.restype = i32
+        L.emb_pool_fwd.argtypes = [T, B, i32, vp, vp]
+        L.emb_workspace_size.restype = sz
+        L.emb_workspace_size.argtypes = [i64, i64, i32]
+        L.emb_workspace_init.restype = i32
+        L.emb_workspace_init.argtypes = [vp, sz, vp]
+        L.emb_unique_ids.restype = i32
+        L.emb_unique_ids.argtypes = [T, B, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.emb_grad_reduce.restype = i32
+        L.emb_grad_reduce.argtypes = [T, B, i32, vp, vp, vp, vp, vp, vp, Up, vp, sz, vp]
+        L.emb_sparse_update.restype = i32
+        L.emb_sparse_update.argtypes = [T, Up, vp, vp, i64, vp, vp]
+        L.emb_validate_batch.restype = i32
+        L.emb_validate_batch.argtypes = [T, B, vp, vp]
+        L.emb_workspace_error_offset.restype = sz
+        L.emb_workspace_error_offset.argtypes = []
+        L.emb_status_string.restype = ctypes.c_char_p
+        L.emb_status_string.argtypes = [i32]
+        _lib = L
+    return _lib
+
+
+def _status_string(st: int) -> str:
+    try:
+        return lib().emb_status_string(st).decode()
+    except Exception:  # pragma: no cover - only while the library is unloadable
+        return "unknown"
+
+
+def _check(fn: str, st: int) -> None:
+    if st != EMB_OK:
+        raise EmbError(fn, st)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    return int(t.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+@dataclass
+class Tables:
+    """Stacked tables (device weights [R][D], host row offsets [T+1])."""
+    weights: object                  # torch tensor float32 [R][D] or bfloat16 [R][D]
+    row_offset: Sequence[int]
+
+    def c(self) -> CTables:
+        import torch
+        ro = (ctypes.c_int64 * len(self.row_offset))(*[int(x) for x in self.row_offset])
+        self._ro = ro  # keep alive for the call
+        dt = BF16 if self.weights.dtype == torch.bfloat16 else FP32
+        return CTables(len(self.row_offset) - 1, ro, int(self.weights.shape[1]), dt, _ptr(self.weights))
+
+
+@dataclass
+class Batch:
+    """A table-major batch in CSR form (device int32 offsets [M+1], indices [N])."""
+    offsets: object
+    indices: object
+    bags_per_table: int
+
+    def c(self) -> CBatch:
+        n = int(self.indices.numel())
+        return CBatch(self.bags_per_table, _ptr(self.offsets), _ptr(self.indices) if n else None, n)
+
+
+def workspace_size(num_indices: int, num_bags: int, dim: int) -> int:
+    return int(lib().emb_workspace_size(num_indices, num_bags, dim))
+
+
+def workspace_init(ws, stream=None) -> None:
+    _check("emb_workspace_init", lib().emb_workspace_init(_ptr(ws), ws.numel() * ws.element_size(),
+                                                          _stream(stream)))
+
+
+def pool_fwd(tables: Tables, batch: Batch, pool: str, out, stream=None) -> None:
+    _check("emb_pool_fwd", lib().emb_pool_fwd(ctypes.byref(tables.c()), ctypes.byref(batch.c()), POOL[pool],
+                                              _ptr(out), _stream(stream)))
+
+
+def unique_ids(tables: Tables, batch: Batch, unique_keys, counts, seg_offsets, sort_perm, num_unique, ws,
+               stream=None) -> None:
+    _check("emb_unique_ids", lib().emb_unique_ids(
+        ctypes.byref(tables.c()), ctypes.byref(batch.c()), _ptr(unique_keys), _ptr(counts), _ptr(seg_offsets),
+        _ptr(sort_perm), _ptr(num_unique), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def _update(opt: str, lr: float, eps: float, state) -> CUpdate:
+    return CUpdate(OPT[opt], lr, eps, _ptr(state))
+
+
+def grad_reduce(tables: Tables, batch: Batch, pool: str, grad_out, sort_perm, seg_offsets, unique_keys,
+                num_unique, ws, grad_rows=None, opt: Optional[str] = None, lr: float = 0.0, eps: float = 0.0,
+                state=None, stream=None) -> None:
+    """Segment-reduce the upstream gradient; with ``opt`` also apply the fused optimizer step."""
+    upd = ctypes.byref(_update(opt, lr, eps, state)) if opt is not None else None
+    _check("emb_grad_reduce", lib().emb_grad_reduce(
+        ctypes.byref(tables.c()), ctypes.byref(batch.c()), POOL[pool], _ptr(grad_out), _ptr(sort_perm),
+        _ptr(seg_offsets), _ptr(unique_keys), _ptr(num_unique), _ptr(grad_rows), upd, _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def sparse_update(tables: Tables, opt: str, lr: float, eps: float, state, unique_keys, num_unique,
+                  max_unique: int, grad_rows, stream=None) -> None:
+    _check("emb_sparse_update", lib().emb_sparse_update(
+        ctypes.byref(tables.c()), ctypes.byref(_update(opt, lr, eps, state)), _ptr(unique_keys),
+        _ptr(num_unique), max_unique, _ptr(grad_rows), _stream(stream)))
+
+
+def validate_batch(tables: Tables, batch: Batch, flag, stream=None) -> None:
+    _check("emb_validate_batch", lib().emb_validate_batch(ctypes.byref(tables.c()), ctypes.byref(batch.c()),
+                                                          _ptr(flag), _stream(stream)))
+
+
+def workspace_error_offset() -> int:
+    return int(lib().emb_workspace_error_offset())
+
+
+class Layer:
+    """One GPU's shard of the layer with its buffers: forward, then the
+    backward (dedup, segment-reduce, fused optimizer step) of the same batch."""
+
+    def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
+                 max_indices: int = 0, max_bags: int = 0):
+        import torch
+        self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
+        dev = tables.weights.device
+        n = max(1, max_indices)
+        D = int(tables.weights.shape[1])
+        wsb = workspace_size(n, max_bags, D)
+        if wsb == 0:
+            raise ValueError("batch too large for one call")
+        self.ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        workspace_init(self.ws)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.unique_keys = torch.empty(n, **i32)
+        self.counts = torch.empty(n, **i32)
+        self.seg_offsets = torch.empty(n + 1, **i32)
+        self.sort_perm = torch.empty(n, **i32)
+        self.num_unique = torch.zeros(1, **i32)
+        self.max_indices = n
+
+    def forward(self, batch: Batch, out, stream=None) -> None:
+        pool_fwd(self.tables, batch, self.pool, out, stream)
+
+    def backward(self, batch: Batch, grad_out, grad_rows=None, stream=None) -> None:
+        if int(batch.indices.numel()) > self.max_indices:
+            raise ValueError("batch larger than the layer's buffers")
+        unique_ids(self.tables, batch, self.unique_keys, self.counts, self.seg_offsets, self.sort_perm,
+                   self.num_unique, self.ws, stream)
+        grad_reduce(self.tables, batch, self.pool, grad_out, self.sort_perm, self.seg_offsets, self.unique_keys,
+                    self.num_unique, self.ws, grad_rows=grad_rows, opt=self.opt, lr=self.lr, eps=self.eps,
+                    state=self.state, stream=stream)
+
+    def step(self, batch: Batch, out, grad_out, stream=None) -> None:
+        self.forward(batch, out, stream)
+        self.backward(batch, grad_out, stream=stream)

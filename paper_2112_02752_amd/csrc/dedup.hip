@@ -1,0 +1,541 @@
+// ID dedup of a batch (gfx950): keys, stable LSD radix sort, unique runs.
+//
+//   key[j]   = row_offset[t(j)] + idx[j]
+//   perm     = stable ascending sort of positions by key
+//   unique_keys / seg_offsets / counts = the runs of equal sorted keys
+//
+// Kernels, in stream order:
+//  1. k_prepare: one wavefront per bag writes the bag id of every position
+//     (and the key, for several tables), and counts the digits of every
+//     radix pass into LDS histograms that are added to global totals.
+//  2. k_sort_pass (once per digit): a tile of kSortTile keys is ranked with
+//     wavefront ballots (the lanes sharing a digit are found with one ballot
+//     per digit bit, the rank is a masked popcount), the per-digit tile
+//     counts are published and each digit's offset among earlier tiles is
+//     found by a decoupled look-back over tile status words; the tile is
+//     reordered in LDS and written out in digit runs.  Ranks follow position
+//     order within a tile and tiles follow position order, so every pass is
+//     stable and so is the whole sort.
+//  3. k_unique: head flags key[k] != key[k-1], a block scan plus a look-back
+//     of (number of heads, last head position) gives every head its segment
+//     index and the length of the previous segment.
+#include "emb_common.h"
+#include "kernels.h"
+
+namespace emb {
+
+SortPlan make_sort_plan(int key_bits) {
+  SortPlan p{};
+  if (key_bits < 1) key_bits = 1;
+  const int passes = (key_bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  int shift = 0;
+  for (int i = 0; i < passes; ++i) {
+    const int left = key_bits - shift;
+    const int b = (left + (passes - i) - 1) / (passes - i);
+    p.shift[i] = shift;
+    p.bits[i] = b;
+    shift += b;
+  }
+  p.passes = passes;
+  return p;
+}
+
+namespace {
+
+constexpr uint64_t kFlagAgg = 1, kFlagInc = 2;
+
+// ------------------------------------------------------------------ prepare
+
+struct PrepArgs {
+  const int32_t* offsets;
+  const int32_t* idx;
+  TableOffsets ro;
+  int32_t B, M, bags_per_block, npass;
+  int32_t shift[kMaxPasses], bits[kMaxPasses];
+  uint32_t* keys_out;  // null for one table (the ids are the keys)
+  int32_t* bag_of;
+  uint32_t* totals;    // [kMaxPasses][kMaxDigits], zero on entry
+  WsHeader* hdr;
+  uint64_t* uniq_status;
+  int32_t uniq_tiles;
+  uint64_t* pass_status;  // the look-back words this call's passes use
+  int64_t pass_status_words;
+};
+
+__global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
+  __shared__ uint32_t hist[kMaxPasses * kMaxDigits];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < a.npass * kMaxDigits; i += kPrepThreads) hist[i] = 0;
+  if (blockIdx.x == 0 && tid == 0) a.hdr->gen = a.hdr->gen + 1u;
+  for (int i = blockIdx.x * kPrepThreads + tid; i < a.uniq_tiles; i += gridDim.x * kPrepThreads)
+    a.uniq_status[i] = 0;
+  for (int64_t i = (int64_t)blockIdx.x * kPrepThreads + tid; i < a.pass_status_words;
+       i += (int64_t)gridDim.x * kPrepThreads)
+    a.pass_status[i] = 0;
+  __syncthreads();
+  const int wave = tid >> 6, lane = tid & (kWave - 1);
+  const int m0 = blockIdx.x * a.bags_per_block;
+  const int m1 = min(a.M, m0 + a.bags_per_block);
+  for (int m = m0 + wave; m < m1; m += kPrepThreads / kWave) {
+    const uint32_t base = a.ro.off[m / a.B];
+    const int s = a.offsets[m], e = a.offsets[m + 1];
+    for (int j = s + lane; j < e; j += kWave) {
+      const uint32_t key = base + (uint32_t)a.idx[j];
+      a.bag_of[j] = m;
+      if (a.keys_out) a.keys_out[j] = key;
+      for (int p = 0; p < a.npass; ++p)
+        atomicAdd(&hist[p * kMaxDigits + ((key >> a.shift[p]) & ((1u << a.bits[p]) - 1u))], 1u);
+    }
+  }
+  __syncthreads();
+  for (int p = 0; p < a.npass; ++p) {
+    const int nd = 1 << a.bits[p];
+    for (int d = tid; d < nd; d += kPrepThreads) {
+      const uint32_t v = hist[p * kMaxDigits + d];
+      if (v) atomic_add_u32(&a.totals[p * kMaxDigits + d], v);
+    }
+  }
+}
+
+// ------------------------------------------------------------- sort pass
+
+struct PassArgs {
+  const uint32_t* keys_in;
+  const int32_t* vals_in;  // null: values are the positions
+  uint32_t* keys_out;
+  int32_t* vals_out;
+  uint32_t* totals;        // this pass's digit totals; cleared by the last tile
+  uint64_t* status;        // [tiles][status_stride], zeroed by k_prepare of the same call
+  WsHeader* hdr;
+  int32_t N, ntiles, shift, bits, pass, status_stride;
+};
+
+// Exclusive scan of n = 2^RB counters held in LDS, by kSortThreads threads.
+template <int RB>
+__device__ __forceinline__ void block_excl_scan(uint32_t* arr, uint32_t* s_wsum) {
+  constexpr int ND = 1 << RB;
+  constexpr int EPT = ND >= kSortThreads ? ND / kSortThreads : 1;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  uint32_t v[EPT];
+  uint32_t sum = 0;
+  const bool own = tid * EPT < ND;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    v[e] = own ? arr[tid * EPT + e] : 0u;
+    sum += v[e];
+  }
+  const uint32_t incl = wave_incl_sum(sum);
+  if (lane == kWave - 1) s_wsum[w] = incl;
+  __syncthreads();
+  uint32_t run = incl - sum;
+  for (int ww = 0; ww < w; ++ww) run += s_wsum[ww];
+  if (own) {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      arr[tid * EPT + e] = run;
+      run += v[e];
+    }
+  }
+  __syncthreads();
+}
+
+template <int RB>
+__global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
+  constexpr int ND = 1 << RB;
+  constexpr int NW = kSortThreads / kWave;
+  constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
+  __shared__ uint32_t s_cnt[NW][ND];
+  __shared__ uint32_t s_tstart[ND];
+  __shared__ uint32_t s_gbase[ND];
+  __shared__ uint32_t s_keys[kSortTile];
+  __shared__ int32_t s_vals[kSortTile];
+  __shared__ uint32_t s_wsum[NW];
+  __shared__ int s_tile, s_last;
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  if (tid == 0) s_tile = (int)atomic_add_u32(&a.hdr->ticket[a.pass], 1u);
+  for (int i = tid; i < NW * ND; i += kSortThreads) (&s_cnt[0][0])[i] = 0u;
+  __syncthreads();
+  const int tile = s_tile;
+  const uint32_t mask = (1u << a.bits) - 1u;
+  const uint32_t tag = 0x80000000u | (a.hdr->gen * 8u + (uint32_t)a.pass);
+  const int64_t wbase = (int64_t)tile * kSortTile + w * (kWave * kSortItems);
+
+  uint32_t key[kSortItems], dig[kSortItems], lrank[kSortItems];
+  int32_t val[kSortItems];
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int64_t pos = wbase + i * kWave + lane;
+    const bool valid = pos < a.N;
+    key[i] = valid ? a.keys_in[pos] : 0u;
+    val[i] = valid ? (a.vals_in ? a.vals_in[pos] : (int32_t)pos) : 0;
+    dig[i] = (key[i] >> a.shift) & mask;
+  }
+
+  // rank each element among the earlier elements of its wave with its digit
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const bool valid = wbase + i * kWave + lane < a.N;
+    uint64_t peers = __ballot(valid);
+    for (int b = 0; b < a.bits; ++b) {
+      const bool bit = (dig[i] >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      peers &= bit ? bb : ~bb;
+    }
+    lrank[i] = 0;
+    if (valid) {
+      const uint32_t r = lanes_below(peers);
+      const uint32_t c = s_cnt[w][dig[i]];
+      lrank[i] = c + r;
+      if (r == 0) s_cnt[w][dig[i]] = c + (uint32_t)__popcll(peers);
+    }
+  }
+  __syncthreads();
+
+  // per digit: exclusive prefix over the waves, and the tile's count
+  uint32_t my_cnt[DPT];
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int d = tid + k * kSortThreads;
+    my_cnt[k] = 0;
+    if (d < ND) {
+      uint32_t run = 0;
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) {
+        const uint32_t c = s_cnt[ww][d];
+        s_cnt[ww][d] = run;
+        run += c;
+      }
+      my_cnt[k] = run;
+      s_tstart[d] = run;
+      s_gbase[d] = a.totals[d];
+    }
+  }
+  __syncthreads();
+  block_excl_scan<RB>(s_tstart, s_wsum);
+  block_excl_scan<RB>(s_gbase, s_wsum);
+
+  // decoupled look-back: the digit's count in all earlier tiles
+  uint64_t* st = a.status + (size_t)tile * a.status_stride;
+  const uint64_t tag_hi = (uint64_t)tag << 32;
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int d = tid + k * kSortThreads;
+    if (d < ND) st_u64(st + d, tag_hi | ((tile == 0 ? kFlagInc : kFlagAgg) << 30) | my_cnt[k]);
+  }
+  if (tile > 0) {
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      if (d >= ND) continue;
+      uint32_t excl = 0;
+      int j = tile - 1;
+      uint32_t spins = 0;
+      while (j >= 0) {
+        const uint64_t sv = ld_acquire_u64(a.status + (size_t)j * a.status_stride + d);
+        const uint64_t flag = (sv >> 30) & 3u;
+        if ((uint32_t)(sv >> 32) == tag && flag != 0) {
+          excl += (uint32_t)(sv & 0x3fffffffu);
+          if (flag == kFlagInc) break;
+          --j;
+          continue;
+        }
+        if (++spins > kSpinLimit) {
+          atomicOr(&a.hdr->error, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      st_u64(st + d, tag_hi | (kFlagInc << 30) | (excl + my_cnt[k]));
+      s_gbase[d] += excl;
+    }
+  }
+  __syncthreads();
+
+  // reorder the tile in LDS by digit (stable), then write digit runs out
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const bool valid = wbase + i * kWave + lane < a.N;
+    if (valid) {
+      const uint32_t lp = s_tstart[dig[i]] + s_cnt[w][dig[i]] + lrank[i];
+      s_keys[lp] = key[i];
+      s_vals[lp] = val[i];
+    }
+  }
+  __syncthreads();
+  const int64_t tstart = (int64_t)tile * kSortTile;
+  const int nvalid = (int)min((int64_t)kSortTile, (int64_t)a.N - tstart);
+  for (int s = tid; s < nvalid; s += kSortThreads) {
+    const uint32_t k = s_keys[s];
+    const uint32_t d = (k >> a.shift) & mask;
+    const uint32_t dst = s_gbase[d] + (uint32_t)s - s_tstart[d];
+    if (dst < (uint32_t)a.N) {
+      a.keys_out[dst] = k;
+      a.vals_out[dst] = s_vals[s];
+    } else {
+      atomicOr(&a.hdr->error, 2u);  // digit totals inconsistent with the keys
+    }
+  }
+
+  // the last tile to finish clears this pass's totals and counters
+  __syncthreads();
+  if (tid == 0) s_last = atomic_add_u32(&a.hdr->done[a.pass], 1u) == (uint32_t)(a.ntiles - 1);
+  __syncthreads();
+  if (s_last) {
+    for (int d = tid; d < ND; d += kSortThreads) a.totals[d] = 0u;
+    if (tid == 0) {
+      a.hdr->ticket[a.pass] = 0u;
+      a.hdr->done[a.pass] = 0u;
+    }
+  }
+}
+
+// ----------------------------------------------------------------- unique
+
+struct UniqArgs {
+  const uint32_t* skeys;
+  int32_t N, ntiles, nchunks;
+  uint32_t* ukeys;
+  int32_t* counts;
+  int32_t* seg;
+  int32_t* num_unique;
+  int32_t* chunk_seg;  // [nchunks+1]: segment of position c*kChunk; [nchunks] = U
+  uint64_t* status;    // [tiles], zeroed by k_prepare of the same call
+  WsHeader* hdr;
+};
+
+// status word: flag [63:62], head count [61:31], last head position + 1 [30:0]
+__device__ __forceinline__ uint64_t pack_uniq(uint64_t flag, uint32_t c, uint32_t q) {
+  return (flag << 62) | ((uint64_t)c << 31) | (uint64_t)q;
+}
+
+__global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
+  constexpr int NW = kUniqThreads / kWave;
+  __shared__ uint32_t s_keys[kUniqTile];
+  __shared__ uint32_t s_wc[NW], s_wq[NW];
+  __shared__ uint32_t s_pc, s_pq, s_prev;
+  __shared__ int s_tile, s_last;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  if (tid == 0) s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
+  __syncthreads();
+  const int tile = s_tile;
+  const int64_t tbase = (int64_t)tile * kUniqTile;
+  for (int s = tid; s < kUniqTile; s += kUniqThreads) {
+    const int64_t pos = tbase + s;
+    s_keys[s] = pos < a.N ? a.skeys[pos] : 0u;
+  }
+  if (tid == 0) s_prev = tbase > 0 ? a.skeys[tbase - 1] : 0u;
+  __syncthreads();
+
+  uint32_t c = 0, q = 0, heads = 0;
+#pragma unroll
+  for (int i = 0; i < kUniqItems; ++i) {
+    const int s = tid * kUniqItems + i;
+    const int64_t pos = tbase + s;
+    if (pos < a.N) {
+      const uint32_t prev = s > 0 ? s_keys[s - 1] : s_prev;
+      if (pos == 0 || s_keys[s] != prev) {
+        ++c;
+        q = (uint32_t)pos + 1u;
+        heads |= 1u << i;
+      }
+    }
+  }
+  // block exclusive scan of (count sum, last-head max)
+  const uint32_t ci = wave_incl_sum(c);
+  const uint32_t qi = wave_incl_max(q);
+  if (lane == kWave - 1) {
+    s_wc[w] = ci;
+    s_wq[w] = qi;
+  }
+  const uint32_t q_before_lane = __shfl_up(qi, 1, kWave);
+  __syncthreads();
+  uint32_t c_ex = ci - c, q_ex = lane > 0 ? q_before_lane : 0u;
+  uint32_t tile_c = 0, tile_q = 0;
+  for (int ww = 0; ww < NW; ++ww) {
+    if (ww < w) {
+      c_ex += s_wc[ww];
+      q_ex = max(q_ex, s_wq[ww]);
+    }
+    tile_c += s_wc[ww];
+    tile_q = max(tile_q, s_wq[ww]);
+  }
+  if (tid == 0) {
+    uint32_t pc = 0, pq = 0;
+    if (tile == 0) {
+      st_u64(a.status, pack_uniq(kFlagInc, tile_c, tile_q));
+    } else {
+      st_u64(a.status + tile, pack_uniq(kFlagAgg, tile_c, tile_q));
+      int j = tile - 1;
+      uint32_t spins = 0;
+      while (j >= 0) {
+        const uint64_t sv = ld_acquire_u64(a.status + j);
+        const uint64_t flag = sv >> 62;
+        if (flag != 0) {
+          pc += (uint32_t)((sv >> 31) & 0x7fffffffu);
+          pq = max(pq, (uint32_t)(sv & 0x7fffffffu));
+          if (flag == kFlagInc) break;
+          --j;
+          continue;
+        }
+        if (++spins > kSpinLimit) {
+          atomicOr(&a.hdr->error, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      st_u64(a.status + tile, pack_uniq(kFlagInc, pc + tile_c, max(pq, tile_q)));
+    }
+    s_pc = pc;
+    s_pq = pq;
+  }
+  __syncthreads();
+  uint32_t u = s_pc + c_ex;
+  uint32_t lastq = max(s_pq, q_ex);
+#pragma unroll
+  for (int i = 0; i < kUniqItems; ++i) {
+    const int s = tid * kUniqItems + i;
+    const int64_t pos = tbase + s;
+    if (pos < a.N) {
+      if (heads & (1u << i)) {
+        a.ukeys[u] = s_keys[s];
+        a.seg[u] = (int32_t)pos;
+        if (u > 0) a.counts[u - 1] = (int32_t)pos - (int32_t)(lastq - 1u);
+        lastq = (uint32_t)pos + 1u;
+        ++u;
+      }
+      if (pos % kChunk == 0) a.chunk_seg[pos / kChunk] = (int32_t)u - 1;
+      if (pos == a.N - 1) {
+        a.num_unique[0] = (int32_t)u;
+        a.seg[u] = a.N;
+        a.counts[u - 1] = a.N - (int32_t)(lastq - 1u);
+        a.chunk_seg[a.nchunks] = (int32_t)u;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid == 0) s_last = atomic_add_u32(&a.hdr->done[kSlotUnique], 1u) == (uint32_t)(a.ntiles - 1);
+  __syncthreads();
+  if (s_last && tid == 0) {
+    a.hdr->ticket[kSlotUnique] = 0u;
+    a.hdr->done[kSlotUnique] = 0u;
+  }
+}
+
+__global__ void k_unique_empty(int32_t* num_unique, int32_t* seg) {
+  if (threadIdx.x == 0) {
+    num_unique[0] = 0;
+    seg[0] = 0;
+  }
+}
+
+template <int RB>
+hipError_t launch_pass(const PassArgs& pa, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(k_sort_pass<RB>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, pa);
+  return hipGetLastError();
+}
+
+hipError_t launch_pass_bits(const PassArgs& pa, int tiles, hipStream_t s) {
+  switch (pa.bits) {
+    case 1: return launch_pass<1>(pa, tiles, s);
+    case 2: return launch_pass<2>(pa, tiles, s);
+    case 3: return launch_pass<3>(pa, tiles, s);
+    case 4: return launch_pass<4>(pa, tiles, s);
+    case 5: return launch_pass<5>(pa, tiles, s);
+    case 6: return launch_pass<6>(pa, tiles, s);
+    case 7: return launch_pass<7>(pa, tiles, s);
+    case 8: return launch_pass<8>(pa, tiles, s);
+    case 9: return launch_pass<9>(pa, tiles, s);
+    case 10: return launch_pass<10>(pa, tiles, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
+  char* ws = static_cast<char*>(p.ws);
+  const WsLayout& L = p.lay;
+  WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+  if (p.N == 0) {
+    hipLaunchKernelGGL(k_unique_empty, dim3(1), dim3(64), 0, s, p.num_unique, p.seg_offsets);
+    return hipGetLastError();
+  }
+  const int N = (int)p.N;
+  const int sort_tiles = (N + kSortTile - 1) / kSortTile;
+  const int uniq_tiles = (N + kUniqTile - 1) / kUniqTile;
+  const int nchunks = (N + kChunk - 1) / kChunk;
+
+  PrepArgs pa{};
+  pa.offsets = p.offsets;
+  pa.idx = p.idx;
+  pa.ro = p.ro;
+  pa.B = p.B;
+  pa.M = p.M;
+  pa.bags_per_block = p.M / 256 > 4 ? (p.M + 255) / 256 : 4;
+  pa.npass = p.plan.passes;
+  for (int i = 0; i < kMaxPasses; ++i) {
+    pa.shift[i] = p.plan.shift[i];
+    pa.bits[i] = p.plan.bits[i];
+  }
+  uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
+  pa.keys_out = p.T > 1 ? keys_built : nullptr;
+  pa.bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
+  pa.totals = reinterpret_cast<uint32_t*>(ws + L.totals);
+  pa.hdr = hdr;
+  pa.uniq_status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
+  pa.uniq_tiles = uniq_tiles;
+  int max_bits = 1;
+  for (int i = 0; i < p.plan.passes; ++i) max_bits = p.plan.bits[i] > max_bits ? p.plan.bits[i] : max_bits;
+  const int status_stride = 1 << max_bits;
+  pa.pass_status = reinterpret_cast<uint64_t*>(ws + L.pass_status);
+  pa.pass_status_words = (int64_t)sort_tiles * status_stride;
+  const int prep_blocks = (p.M + pa.bags_per_block - 1) / pa.bags_per_block;
+  hipLaunchKernelGGL(k_prepare, dim3((unsigned)(prep_blocks > 0 ? prep_blocks : 1)), dim3(kPrepThreads), 0, s, pa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  const uint32_t* kin = p.T > 1 ? keys_built : reinterpret_cast<const uint32_t*>(p.idx);
+  const int32_t* vin = nullptr;
+  uint32_t* keys_a = reinterpret_cast<uint32_t*>(ws + L.keys_a);
+  uint32_t* keys_b = reinterpret_cast<uint32_t*>(ws + L.keys_b);
+  int32_t* vals_a = reinterpret_cast<int32_t*>(ws + L.vals_a);
+  int32_t* vals_b = reinterpret_cast<int32_t*>(ws + L.vals_b);
+  for (int ps = 0; ps < p.plan.passes; ++ps) {
+    PassArgs xa{};
+    xa.keys_in = kin;
+    xa.vals_in = vin;
+    xa.keys_out = (ps % 2 == 0) ? keys_a : keys_b;
+    xa.vals_out = (ps == p.plan.passes - 1) ? p.sort_perm : ((ps % 2 == 0) ? vals_a : vals_b);
+    xa.totals = reinterpret_cast<uint32_t*>(ws + L.totals) + ps * kMaxDigits;
+    xa.status = reinterpret_cast<uint64_t*>(ws + L.pass_status);
+    xa.hdr = hdr;
+    xa.N = N;
+    xa.ntiles = sort_tiles;
+    xa.shift = p.plan.shift[ps];
+    xa.bits = p.plan.bits[ps];
+    xa.pass = ps;
+    xa.status_stride = status_stride;
+    e = launch_pass_bits(xa, sort_tiles, s);
+    if (e != hipSuccess) return e;
+    kin = xa.keys_out;
+    vin = xa.vals_out;
+  }
+
+  UniqArgs ua{};
+  ua.skeys = kin;
+  ua.N = N;
+  ua.ntiles = uniq_tiles;
+  ua.nchunks = nchunks;
+  ua.ukeys = p.unique_keys;
+  ua.counts = p.counts;
+  ua.seg = p.seg_offsets;
+  ua.num_unique = p.num_unique;
+  ua.chunk_seg = reinterpret_cast<int32_t*>(ws + L.chunk_seg);
+  ua.status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
+  ua.hdr = hdr;
+  hipLaunchKernelGGL(k_unique, dim3((unsigned)uniq_tiles), dim3(kUniqThreads), 0, s, ua);
+  return hipGetLastError();
+}
+
+}  // namespace emb

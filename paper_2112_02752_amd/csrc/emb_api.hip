@@ -1,0 +1,251 @@
+// C ABI of the embedding layer: host-side argument checks, workspace
+// layout, kernel dispatch.  No allocation, no synchronisation.
+#include <string.h>
+
+#include "emb_common.h"
+#include "kernels.h"
+
+using namespace emb;
+
+namespace {
+
+constexpr int64_t kMaxIndices = (int64_t)1 << 30;
+
+int dtype_bytes(int32_t dtype) { return dtype == EMB_FP32 ? 4 : (dtype == EMB_BF16 ? 2 : 0); }
+
+emb_status check_tables(const emb_tables* t, TableOffsets* ro, int64_t* total_rows) {
+  if (t == nullptr || t->row_offset == nullptr || t->weights == nullptr) return EMB_EINVAL;
+  if (t->num_tables < 1 || t->num_tables > EMB_MAX_TABLES) return t->num_tables < 1 ? EMB_EINVAL : EMB_EUNSUPPORTED;
+  if (t->dim < 1) return EMB_EINVAL;
+  const int sb = dtype_bytes(t->dtype);
+  if (sb == 0) return EMB_EINVAL;
+  if (((int64_t)t->dim * sb) % 16 != 0) return EMB_EUNSUPPORTED;
+  if (((uintptr_t)t->weights & 15u) != 0) return EMB_EINVAL;
+  if (t->row_offset[0] != 0) return EMB_EINVAL;
+  memset(ro, 0, sizeof(*ro));
+  for (int i = 0; i < t->num_tables; ++i)
+    if (t->row_offset[i + 1] < t->row_offset[i]) return EMB_EINVAL;
+  const int64_t R = t->row_offset[t->num_tables];
+  if (R >= ((int64_t)1 << 32)) return EMB_EUNSUPPORTED;
+  for (int i = 0; i <= t->num_tables; ++i) ro->off[i] = (uint32_t)t->row_offset[i];
+  *total_rows = R;
+  return EMB_OK;
+}
+
+emb_status check_batch(const emb_batch* b, int32_t T, int32_t* M) {
+  if (b == nullptr || b->offsets == nullptr) return EMB_EINVAL;
+  if (b->bags_per_table < 0 || b->num_indices < 0) return EMB_EINVAL;
+  if (b->num_indices >= kMaxIndices) return EMB_EUNSUPPORTED;
+  if (b->num_indices > 0 && b->indices == nullptr) return EMB_EINVAL;
+  const int64_t m = (int64_t)T * b->bags_per_table;
+  if (m >= ((int64_t)1 << 31) - 1) return EMB_EUNSUPPORTED;
+  *M = (int32_t)m;
+  return EMB_OK;
+}
+
+int key_bits_for(int64_t R) {
+  int bits = 1;
+  while (bits < 32 && ((int64_t)1 << bits) < R) ++bits;
+  return bits;
+}
+
+emb_status check_ws(const void* ws, size_t ws_bytes, int64_t N, int64_t M, int32_t D, WsLayout* lay) {
+  if (ws == nullptr) return EMB_EINVAL;
+  if (((uintptr_t)ws & 255u) != 0) return EMB_EWORKSPACE;
+  *lay = ws_layout(N, M, D);
+  if (ws_bytes < lay->total) return EMB_EWORKSPACE;
+  return EMB_OK;
+}
+
+emb_status check_update(const emb_update* u) {
+  if (u == nullptr) return EMB_EINVAL;
+  if (u->opt != EMB_OPT_SGD && u->opt != EMB_OPT_ADAGRAD_ROWWISE) return EMB_EINVAL;
+  if (u->opt == EMB_OPT_ADAGRAD_ROWWISE && u->state == nullptr) return EMB_EINVAL;
+  return EMB_OK;
+}
+
+emb_status hip_status(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* emb_status_string(int32_t status) {
+  switch (status) {
+    case EMB_OK: return "ok";
+    case EMB_EINVAL: return "invalid argument";
+    case EMB_EWORKSPACE: return "workspace too small or misaligned";
+    case EMB_EUNSUPPORTED: return "unsupported size or layout";
+    case EMB_EHIP: return "HIP launch failure";
+    default: return "unknown status";
+  }
+}
+
+size_t emb_workspace_size(int64_t num_indices, int64_t num_bags, int32_t dim) {
+  if (num_indices < 0 || num_indices >= kMaxIndices || num_bags < 0 || dim < 1) return 0;
+  return ws_layout(num_indices, num_bags, dim).total;
+}
+
+size_t emb_workspace_error_offset(void) { return offsetof(WsHeader, error); }
+
+emb_status emb_workspace_init(void* ws, size_t ws_bytes, void* stream) {
+  if (ws == nullptr) return EMB_EINVAL;
+  if (((uintptr_t)ws & 255u) != 0) return EMB_EWORKSPACE;
+  return hip_status(launch_zero_bytes(ws, ws_bytes, (hipStream_t)stream));
+}
+
+emb_status emb_pool_fwd(const emb_tables* tables, const emb_batch* batch, int32_t pool, float* out, void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  st = check_batch(batch, tables->num_tables, &M);
+  if (st != EMB_OK) return st;
+  if (pool != EMB_POOL_SUM && pool != EMB_POOL_MEAN) return EMB_EINVAL;
+  if (M > 0 && out == nullptr) return EMB_EINVAL;
+  if ((int64_t)tables->dim * dtype_bytes(tables->dtype) / 16 > fwd_max_row_vectors()) return EMB_EUNSUPPORTED;
+  if (M == 0) return EMB_OK;
+  FwdLaunch p{};
+  p.W = tables->weights;
+  p.offsets = batch->offsets;
+  p.idx = batch->indices;
+  p.ro = ro;
+  p.B = batch->bags_per_table;
+  p.M = M;
+  p.D = tables->dim;
+  p.dtype = tables->dtype;
+  p.pool = pool;
+  p.out = out;
+  return hip_status(launch_pool_fwd(p, (hipStream_t)stream));
+}
+
+emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys, int32_t* counts,
+                          int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
+                          void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  st = check_batch(batch, tables->num_tables, &M);
+  if (st != EMB_OK) return st;
+  if (seg_offsets == nullptr || num_unique == nullptr) return EMB_EINVAL;
+  if (batch->num_indices > 0 && (unique_keys == nullptr || counts == nullptr || sort_perm == nullptr))
+    return EMB_EINVAL;
+  WsLayout lay;
+  st = check_ws(ws, ws_bytes, batch->num_indices, M, tables->dim, &lay);
+  if (st != EMB_OK) return st;
+  DedupLaunch p{};
+  p.offsets = batch->offsets;
+  p.idx = batch->indices;
+  p.ro = ro;
+  p.T = tables->num_tables;
+  p.B = batch->bags_per_table;
+  p.M = M;
+  p.N = batch->num_indices;
+  p.plan = make_sort_plan(key_bits_for(R));
+  p.ws = ws;
+  p.lay = lay;
+  p.unique_keys = unique_keys;
+  p.counts = counts;
+  p.seg_offsets = seg_offsets;
+  p.sort_perm = sort_perm;
+  p.num_unique = num_unique;
+  return hip_status(launch_dedup(p, (hipStream_t)stream));
+}
+
+emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* grad_out,
+                           const int32_t* sort_perm, const int32_t* seg_offsets, const uint32_t* unique_keys,
+                           const int32_t* num_unique, float* grad_rows, const emb_update* fuse, void* ws,
+                           size_t ws_bytes, void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  st = check_batch(batch, tables->num_tables, &M);
+  if (st != EMB_OK) return st;
+  if (pool != EMB_POOL_SUM && pool != EMB_POOL_MEAN) return EMB_EINVAL;
+  if (fuse == nullptr && grad_rows == nullptr) return EMB_EINVAL;
+  if (fuse != nullptr && (st = check_update(fuse)) != EMB_OK) return st;
+  if (tables->dim > reduce_max_dim()) return EMB_EUNSUPPORTED;
+  WsLayout lay;
+  st = check_ws(ws, ws_bytes, batch->num_indices, M, tables->dim, &lay);
+  if (st != EMB_OK) return st;
+  if (batch->num_indices == 0) return EMB_OK;
+  if (grad_out == nullptr || sort_perm == nullptr || seg_offsets == nullptr || unique_keys == nullptr ||
+      num_unique == nullptr)
+    return EMB_EINVAL;
+  ReduceLaunch p{};
+  p.grad_out = grad_out;
+  p.perm = sort_perm;
+  p.seg = seg_offsets;
+  p.ukeys = unique_keys;
+  p.num_unique = num_unique;
+  p.offsets = batch->offsets;
+  p.N = (int32_t)batch->num_indices;
+  p.M = M;
+  p.D = tables->dim;
+  p.pool = pool;
+  p.ws = ws;
+  p.lay = lay;
+  p.grad_rows = grad_rows;
+  p.fuse = fuse != nullptr;
+  p.opt = fuse ? fuse->opt : 0;
+  p.dtype = tables->dtype;
+  p.lr = fuse ? fuse->lr : 0.f;
+  p.eps = fuse ? fuse->eps : 0.f;
+  p.W = tables->weights;
+  p.state = fuse ? fuse->state : nullptr;
+  return hip_status(launch_grad_reduce(p, (hipStream_t)stream));
+}
+
+emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update, const uint32_t* unique_keys,
+                             const int32_t* num_unique, int64_t max_unique, const float* grad_rows, void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  if ((st = check_update(update)) != EMB_OK) return st;
+  if (max_unique < 0 || max_unique >= kMaxIndices) return max_unique < 0 ? EMB_EINVAL : EMB_EUNSUPPORTED;
+  if (tables->dim > reduce_max_dim()) return EMB_EUNSUPPORTED;
+  if (max_unique == 0) return EMB_OK;
+  if (unique_keys == nullptr || num_unique == nullptr || grad_rows == nullptr) return EMB_EINVAL;
+  UpdateLaunch p{};
+  p.grad_rows = grad_rows;
+  p.ukeys = unique_keys;
+  p.num_unique = num_unique;
+  p.max_unique = max_unique;
+  p.D = tables->dim;
+  p.opt = update->opt;
+  p.dtype = tables->dtype;
+  p.lr = update->lr;
+  p.eps = update->eps;
+  p.W = tables->weights;
+  p.state = update->state;
+  return hip_status(launch_sparse_update(p, (hipStream_t)stream));
+}
+
+emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, int32_t* flag, void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  st = check_batch(batch, tables->num_tables, &M);
+  if (st != EMB_OK) return st;
+  if (flag == nullptr) return EMB_EINVAL;
+  ValidateLaunch p{};
+  p.offsets = batch->offsets;
+  p.idx = batch->indices;
+  p.ro = ro;
+  p.T = tables->num_tables;
+  p.B = batch->bags_per_table;
+  p.M = M;
+  p.N = batch->num_indices;
+  p.flag = flag;
+  return hip_status(launch_validate(p, (hipStream_t)stream));
+}
+
+}  // extern "C"

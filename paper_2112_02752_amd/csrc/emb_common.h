@@ -1,0 +1,149 @@
+// Internal definitions shared by the gfx950 kernels of the embedding layer:
+// workspace layout, launch constants, wavefront helpers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "emb.h"
+
+namespace emb {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- dedup sort
+// LSD radix sort, one kernel per digit with a decoupled look-back over tiles.
+constexpr int kMaxPasses = 4;
+constexpr int kMaxDigitBits = 10;
+constexpr int kMaxDigits = 1 << kMaxDigitBits;
+constexpr int kSortThreads = 256;
+constexpr int kSortItems = 8;
+constexpr int kSortTile = kSortThreads * kSortItems;
+
+// unique / segment scan
+constexpr int kUniqThreads = 256;
+constexpr int kUniqItems = 8;
+constexpr int kUniqTile = kUniqThreads * kUniqItems;
+
+// prepare kernel (keys, bag ids, digit histograms)
+constexpr int kPrepThreads = 256;
+
+// gradient reduce: segments longer than kChunk positions are "heavy" and are
+// summed in aligned chunks of kChunk sorted positions, then combined.
+constexpr int kChunk = 64;
+
+// ticket / done counter slots in the workspace header
+constexpr int kSlotUnique = kMaxPasses;
+
+// Workspace header (device).  gen counts emb_unique_ids calls; it tags the
+// sort look-back words so they never need clearing.
+struct WsHeader {
+  uint32_t gen;
+  uint32_t error;
+  uint32_t ticket[8];
+  uint32_t done[8];
+  uint32_t pad[46];
+};
+static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
+
+struct WsLayout {
+  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bag_of, pass_status, uniq_status, chunk_seg,
+      partials, total;
+  int64_t sort_tiles, uniq_tiles, chunks;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
+  (void)M;
+  WsLayout L{};
+  int64_t n = N > 0 ? N : 1;
+  L.sort_tiles = (n + kSortTile - 1) / kSortTile;
+  L.uniq_tiles = (n + kUniqTile - 1) / kUniqTile;
+  L.chunks = (n + kChunk - 1) / kChunk;
+  size_t off = 0;
+  L.hdr = off;
+  off += sizeof(WsHeader);
+  L.totals = off;
+  off = align256(off + sizeof(uint32_t) * kMaxPasses * kMaxDigits);
+  L.keys_built = off;
+  off = align256(off + sizeof(uint32_t) * n);
+  L.keys_a = off;
+  off = align256(off + sizeof(uint32_t) * n);
+  L.keys_b = off;
+  off = align256(off + sizeof(uint32_t) * n);
+  L.vals_a = off;
+  off = align256(off + sizeof(int32_t) * n);
+  L.vals_b = off;
+  off = align256(off + sizeof(int32_t) * n);
+  L.bag_of = off;
+  off = align256(off + sizeof(int32_t) * n);
+  L.pass_status = off;
+  off = align256(off + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
+  L.uniq_status = off;
+  off = align256(off + sizeof(uint64_t) * L.uniq_tiles);
+  L.chunk_seg = off;
+  off = align256(off + sizeof(int32_t) * (L.chunks + 1));
+  L.partials = off;
+  off = align256(off + sizeof(float) * (size_t)L.chunks * 2 * (size_t)(D > 0 ? D : 1));
+  L.total = off;
+  return L;
+}
+
+// Global row offsets of the stacked tables, passed by value in kernel
+// arguments (R < 2^32, so 32 bits per entry).
+struct TableOffsets {
+  uint32_t off[EMB_MAX_TABLES + 1];
+};
+
+// ------------------------------------------------------------ device helpers
+
+// number of set bits of `mask` below this lane
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ uint64_t ld_acquire_u64(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_u64(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t atomic_add_u32(uint32_t* p, uint32_t v) {
+  return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bounded spin budget of a look-back wait; running out sets an error bit and
+// lets the wave continue, so every wave always exits.
+constexpr uint32_t kSpinLimit = 1u << 22;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// inclusive wave scan (sum) of a 32-bit value
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    uint32_t t = __shfl_up(v, o, kWave);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t v) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    uint32_t t = __shfl_up(v, o, kWave);
+    if (lane >= o) v = v > t ? v : t;
+  }
+  return v;
+}
+
+}  // namespace emb

@@ -1,0 +1,88 @@
+// Launch descriptors of the gfx950 kernels; the C-ABI layer fills them after
+// checking its arguments on the host.
+#pragma once
+
+#include "emb_common.h"
+
+namespace emb {
+
+struct FwdLaunch {
+  const void* W;
+  const int32_t* offsets;
+  const int32_t* idx;
+  TableOffsets ro;
+  int32_t B, M, D, dtype, pool;
+  float* out;
+};
+hipError_t launch_pool_fwd(const FwdLaunch& p, hipStream_t s);
+int fwd_max_row_vectors();
+
+// digit schedule of the LSD sort for keys of `key_bits` bits
+struct SortPlan {
+  int passes;
+  int shift[kMaxPasses];
+  int bits[kMaxPasses];
+};
+SortPlan make_sort_plan(int key_bits);
+
+struct DedupLaunch {
+  const int32_t* offsets;
+  const int32_t* idx;
+  TableOffsets ro;
+  int32_t T, B, M;
+  int64_t N;
+  SortPlan plan;
+  void* ws;
+  WsLayout lay;
+  uint32_t* unique_keys;
+  int32_t* counts;
+  int32_t* seg_offsets;
+  int32_t* sort_perm;
+  int32_t* num_unique;
+};
+hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s);
+
+struct ReduceLaunch {
+  const float* grad_out;
+  const int32_t* perm;
+  const int32_t* seg;
+  const uint32_t* ukeys;
+  const int32_t* num_unique;
+  const int32_t* offsets;
+  int32_t N, M, D, pool;
+  void* ws;
+  WsLayout lay;
+  float* grad_rows;  // may be null
+  // fused optimizer (fuse = 0: reduce only)
+  int32_t fuse, opt, dtype;
+  float lr, eps;
+  void* W;
+  float* state;
+};
+hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s);
+
+struct UpdateLaunch {
+  const float* grad_rows;
+  const uint32_t* ukeys;
+  const int32_t* num_unique;
+  int64_t max_unique;
+  int32_t D, opt, dtype;
+  float lr, eps;
+  void* W;
+  float* state;
+};
+hipError_t launch_sparse_update(const UpdateLaunch& p, hipStream_t s);
+int reduce_max_dim();
+
+struct ValidateLaunch {
+  const int32_t* offsets;
+  const int32_t* idx;
+  TableOffsets ro;
+  int32_t T, B, M;
+  int64_t N;
+  int32_t* flag;
+};
+hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s);
+hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace emb

@@ -1,0 +1,64 @@
+// Batch validation and workspace clearing (off the timed path).
+#include "emb_common.h"
+#include "kernels.h"
+
+namespace emb {
+
+namespace {
+
+__global__ void k_fill_zero_u32(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+// flag bits: 1 offsets[0] != 0, 2 decreasing offsets, 4 offsets[M] != N, 8 id out of range
+__global__ void k_validate(const int32_t* offsets, const int32_t* idx, TableOffsets ro, int32_t B, int32_t M,
+                           int64_t N, int32_t* flag) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  uint32_t bits = 0;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t0 == 0) {
+    if (offsets[0] != 0) bits |= 1u;
+    if ((int64_t)offsets[M] != N) bits |= 4u;
+  }
+  for (int64_t m = t0; m < M; m += stride) {
+    const int32_t s = offsets[m], e = offsets[m + 1];
+    if (e < s) {
+      bits |= 2u;
+      continue;
+    }
+    const int t = (int)(m / B);
+    const int64_t rows = (int64_t)ro.off[t + 1] - (int64_t)ro.off[t];
+    const int32_t lo = s < 0 ? 0 : s;
+    const int64_t hi = (int64_t)e < N ? (int64_t)e : N;
+    for (int64_t j = lo; j < hi; ++j) {
+      const int32_t id = idx[j];
+      if (id < 0 || (int64_t)id >= rows) bits |= 8u;
+    }
+  }
+  if (bits) atomicOr(reinterpret_cast<uint32_t*>(flag), bits);
+}
+
+}  // namespace
+
+hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill_zero_u32, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<uint32_t*>(p), n);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s) {
+  hipError_t e = launch_zero_bytes(p.flag, 4, s);
+  if (e != hipSuccess) return e;
+  int64_t blocks = ((int64_t)p.M + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_validate, dim3((unsigned)blocks), dim3(256), 0, s, p.offsets, p.idx, p.ro, p.B, p.M, p.N,
+                     p.flag);
+  return hipGetLastError();
+}
+
+}  // namespace emb

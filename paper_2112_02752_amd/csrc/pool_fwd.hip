@@ -1,0 +1,164 @@
+// Pooled embedding lookup, forward (gfx950).
+//
+//   out[m][d] = scale_m * sum_{j in bag m} W[row_offset[t(m)] + idx[j]][d]
+//
+// One wavefront per bag.  A row of D*sizeof(T) bytes is read as 16-byte
+// vectors by a group of G lanes (G a power of two), so one wave instruction
+// gathers 64/G rows; each group walks its share of the bag with UNROLL rows
+// in flight, accumulating in fp32.  The groups are summed with a butterfly at
+// the end and group 0 stores the pooled row.  Ids of the bag are read 64 at a
+// time with one coalesced load and handed to the groups by lane shuffles.
+#include "emb_common.h"
+#include "kernels.h"
+
+namespace emb {
+
+namespace {
+
+template <typename TW>
+struct Vec;  // 16 bytes of table row, widened to fp32
+
+template <>
+struct Vec<float> {
+  static constexpr int kElems = 4;
+  __device__ __forceinline__ static void load(const float* p, float (&o)[4]) {
+    float4 v = *reinterpret_cast<const float4*>(p);
+    o[0] = v.x;
+    o[1] = v.y;
+    o[2] = v.z;
+    o[3] = v.w;
+  }
+};
+
+template <>
+struct Vec<uint16_t> {
+  static constexpr int kElems = 8;
+  __device__ __forceinline__ static void load(const uint16_t* p, float (&o)[8]) {
+    uint4 v = *reinterpret_cast<const uint4*>(p);
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = __uint_as_float(w[i] << 16);
+      o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+};
+
+constexpr int unroll_for(int rpi) { return rpi == 1 ? 8 : (rpi == 2 ? 8 : (rpi == 4 ? 4 : 2)); }
+
+template <typename TW, int G, int NV>
+__global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, const int32_t* __restrict__ offsets,
+                                                  const int32_t* __restrict__ idx, TableOffsets ro, int32_t B,
+                                                  int32_t M, int32_t D, int32_t pool, float* __restrict__ out) {
+  constexpr int RPI = kWave / G;
+  constexpr int E = Vec<TW>::kElems;
+  constexpr int UN = unroll_for(RPI);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int m = blockIdx.x * (256 / kWave) + (threadIdx.x >> 6);
+  if (m >= M) return;
+  const int g = lane / G, sub = lane % G;
+  const uint32_t base = ro.off[m / B];
+  const int start = offsets[m], end = offsets[m + 1];
+
+  float acc[NV][E];
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[v][e] = 0.f;
+
+  for (int j0 = start; j0 < end; j0 += kWave) {
+    const int n = min(kWave, end - j0);
+    const int my_id = lane < n ? idx[j0 + lane] : 0;
+    for (int i0 = 0; i0 < n; i0 += RPI * UN) {
+      float row[UN][NV][E];
+#pragma unroll
+      for (int u = 0; u < UN; ++u) {
+        const int s = i0 + u * RPI + g;
+        const int id = __shfl(my_id, s & (kWave - 1), kWave);
+        if (s < n) {
+          const TW* rp = W + (size_t)(base + (uint32_t)id) * (size_t)D;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            const int c0 = (v * G + sub) * E;
+            if (c0 < D) Vec<TW>::load(rp + c0, row[u][v]);
+            else
+#pragma unroll
+              for (int e = 0; e < E; ++e) row[u][v][e] = 0.f;
+          }
+        } else {
+#pragma unroll
+          for (int v = 0; v < NV; ++v)
+#pragma unroll
+            for (int e = 0; e < E; ++e) row[u][v][e] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UN; ++u)
+#pragma unroll
+        for (int v = 0; v < NV; ++v)
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[v][e] += row[u][v][e];
+    }
+  }
+
+  // sum the RPI groups (butterfly over the group index bits)
+#pragma unroll
+  for (int o = G; o < kWave; o <<= 1)
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[v][e] += __shfl_xor(acc[v][e], o, kWave);
+
+  if (g == 0) {
+    const int L = end - start;
+    const float scale = (pool == EMB_POOL_MEAN && L > 0) ? 1.0f / (float)L : 1.0f;
+    float* op = out + (size_t)m * (size_t)D;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c0 = (v * G + sub) * E;
+      if (c0 < D) {
+#pragma unroll
+        for (int e = 0; e < E; e += 4) {
+          float4 w = make_float4(acc[v][e] * scale, acc[v][e + 1] * scale, acc[v][e + 2] * scale,
+                                 acc[v][e + 3] * scale);
+          *reinterpret_cast<float4*>(op + c0 + e) = w;
+        }
+      }
+    }
+  }
+}
+
+template <typename TW, int G, int NV>
+hipError_t launch_t(const FwdLaunch& p, hipStream_t s) {
+  dim3 grid((unsigned)((p.M + 3) / 4)), block(256);
+  hipLaunchKernelGGL((k_pool_fwd<TW, G, NV>), grid, block, 0, s, reinterpret_cast<const TW*>(p.W), p.offsets,
+                     p.idx, p.ro, p.B, p.M, p.D, p.pool, p.out);
+  return hipGetLastError();
+}
+
+template <typename TW>
+hipError_t launch_dtype(const FwdLaunch& p, hipStream_t s) {
+  const int vecs = p.D * (int)sizeof(TW) / 16;  // 16-byte vectors per row
+  if (vecs <= 1) return launch_t<TW, 1, 1>(p, s);
+  if (vecs <= 2) return launch_t<TW, 2, 1>(p, s);
+  if (vecs <= 4) return launch_t<TW, 4, 1>(p, s);
+  if (vecs <= 8) return launch_t<TW, 8, 1>(p, s);
+  if (vecs <= 16) return launch_t<TW, 16, 1>(p, s);
+  if (vecs <= 32) return launch_t<TW, 32, 1>(p, s);
+  if (vecs <= 64) return launch_t<TW, 64, 1>(p, s);
+  if (vecs <= 128) return launch_t<TW, 64, 2>(p, s);
+  if (vecs <= 256) return launch_t<TW, 64, 4>(p, s);
+  if (vecs <= 512) return launch_t<TW, 64, 8>(p, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+int fwd_max_row_vectors() { return 512; }
+
+hipError_t launch_pool_fwd(const FwdLaunch& p, hipStream_t s) {
+  if (p.M == 0) return hipSuccess;
+  return p.dtype == EMB_FP32 ? launch_dtype<float>(p, s) : launch_dtype<uint16_t>(p, s);
+}
+
+}  // namespace emb

@@ -1,0 +1,150 @@
+"""The C ABI library without a GPU: it loads, exports every entry point the
+header declares, sizes workspaces, and rejects bad arguments synchronously
+(host checks run before anything touches the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2112_02752_amd as emb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "emb.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(emb_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for fn in ("emb_pool_fwd", "emb_unique_ids", "emb_grad_reduce", "emb_sparse_update"):
+        assert fn in names
+    assert set(names) == set(emb.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    L = emb.lib()
+    for fn in declared_functions():
+        assert hasattr(L, fn), fn
+        assert getattr(L, fn) is not None
+
+
+def test_status_strings():
+    for st in range(5):
+        assert emb.lib().emb_status_string(st).decode()
+    assert emb.lib().emb_status_string(99).decode() == "unknown status"
+
+
+def test_workspace_size_monotone_and_invalid():
+    a = emb.workspace_size(1000, 100, 64)
+    b = emb.workspace_size(100_000, 100, 64)
+    c = emb.workspace_size(100_000, 100, 128)
+    assert 0 < a < b < c
+    assert a % 256 == 0
+    assert emb.workspace_size(-1, 1, 64) == 0
+    assert emb.workspace_size(1 << 30, 1, 64) == 0
+    assert emb.workspace_size(10, 1, 0) == 0
+    assert emb.workspace_size(0, 0, 16) > 0
+
+
+def _tables(row_offset=(0, 100), dim=16, dtype=0, weights=0x1000):
+    ro = (ctypes.c_int64 * len(row_offset))(*row_offset)
+    t = emb.CTables(len(row_offset) - 1, ro, dim, dtype, weights)
+    t._keep = ro
+    return t
+
+
+def _batch(B=4, offsets=0x2000, indices=0x3000, n=10):
+    return emb.CBatch(B, offsets, indices, n)
+
+
+def call_fwd(t, b, pool=0, out=0x4000):
+    return emb.lib().emb_pool_fwd(ctypes.byref(t), ctypes.byref(b), pool, out, None)
+
+
+def test_fwd_argument_errors():
+    assert call_fwd(_tables(weights=None), _batch()) == emb.EMB_EINVAL
+    assert call_fwd(_tables(dim=3), _batch()) == emb.EMB_EUNSUPPORTED        # 12-byte rows
+    assert call_fwd(_tables(dim=4, dtype=1), _batch()) == emb.EMB_EUNSUPPORTED  # 8-byte bf16 rows
+    assert call_fwd(_tables(dtype=7), _batch()) == emb.EMB_EINVAL
+    assert call_fwd(_tables(row_offset=(0, 1 << 32)), _batch()) == emb.EMB_EUNSUPPORTED
+    assert call_fwd(_tables(row_offset=(1, 10)), _batch()) == emb.EMB_EINVAL
+    assert call_fwd(_tables(row_offset=(0, 10, 5)), _batch()) == emb.EMB_EINVAL
+    assert call_fwd(_tables(weights=0x1008), _batch()) == emb.EMB_EINVAL      # not 16-byte aligned
+    assert call_fwd(_tables(), _batch(offsets=None)) == emb.EMB_EINVAL
+    assert call_fwd(_tables(), _batch(B=-1)) == emb.EMB_EINVAL
+    assert call_fwd(_tables(), _batch(n=1 << 30)) == emb.EMB_EUNSUPPORTED
+    assert call_fwd(_tables(), _batch(indices=None)) == emb.EMB_EINVAL
+    assert call_fwd(_tables(), _batch(), pool=2) == emb.EMB_EINVAL
+    assert call_fwd(_tables(), _batch(), out=None) == emb.EMB_EINVAL
+    t = _tables()
+    t.num_tables = 0
+    assert call_fwd(t, _batch()) == emb.EMB_EINVAL
+    many = _tables(row_offset=tuple(range(300)))
+    assert call_fwd(many, _batch()) == emb.EMB_EUNSUPPORTED
+    # an empty batch is valid and enqueues nothing
+    assert call_fwd(_tables(), _batch(B=0, n=0, indices=None), out=None) == emb.EMB_OK
+
+
+def test_unique_ids_workspace_errors():
+    L = emb.lib()
+    t, b = _tables(), _batch(n=1000)
+    need = emb.workspace_size(1000, 4, 16)
+
+    def call(ws=0x100000, nbytes=need, **kw):
+        args = dict(uk=0x5000, cnt=0x6000, seg=0x7000, perm=0x8000, nu=0x9000)
+        args.update(kw)
+        return L.emb_unique_ids(ctypes.byref(t), ctypes.byref(b), args["uk"], args["cnt"], args["seg"],
+                                args["perm"], args["nu"], ws, nbytes, None)
+
+    assert call(nbytes=need - 1) == emb.EMB_EWORKSPACE
+    assert call(ws=0x100010) == emb.EMB_EWORKSPACE  # not 256-byte aligned
+    assert call(ws=None) == emb.EMB_EINVAL
+    assert call(seg=None) == emb.EMB_EINVAL
+    assert call(perm=None) == emb.EMB_EINVAL
+
+
+def test_grad_reduce_argument_errors():
+    L = emb.lib()
+    t, b = _tables(), _batch(n=1000)
+    need = emb.workspace_size(1000, 4, 16)
+    bad_opt = emb.CUpdate(5, 0.1, 0.0, None)
+    adagrad_no_state = emb.CUpdate(1, 0.1, 1e-8, None)
+
+    def call(grad_rows=0xa000, fuse=None, pool=0, nbytes=need):
+        f = ctypes.byref(fuse) if fuse is not None else None
+        return L.emb_grad_reduce(ctypes.byref(t), ctypes.byref(b), pool, 0xb000, 0xc000, 0xd000, 0xe000, 0xf000,
+                                 grad_rows, f, 0x100000, nbytes, None)
+
+    assert call(grad_rows=None) == emb.EMB_EINVAL
+    assert call(fuse=bad_opt) == emb.EMB_EINVAL
+    assert call(fuse=adagrad_no_state) == emb.EMB_EINVAL
+    assert call(pool=3) == emb.EMB_EINVAL
+    assert call(nbytes=16) == emb.EMB_EWORKSPACE
+
+
+def test_sparse_update_argument_errors():
+    L = emb.lib()
+    t = _tables()
+    ok = emb.CUpdate(0, 0.1, 0.0, None)
+    assert L.emb_sparse_update(ctypes.byref(t), ctypes.byref(ok), None, 0x1, 10, 0x2, None) == emb.EMB_EINVAL
+    assert L.emb_sparse_update(ctypes.byref(t), ctypes.byref(ok), 0x1, 0x1, -1, 0x2, None) == emb.EMB_EINVAL
+    assert L.emb_sparse_update(ctypes.byref(t), ctypes.byref(ok), None, None, 0, None, None) == emb.EMB_OK
+    big = _tables(dim=2048)
+    assert L.emb_sparse_update(ctypes.byref(big), ctypes.byref(ok), 0x1, 0x1, 5, 0x2, None) == \
+        emb.EMB_EUNSUPPORTED
+
+
+def test_error_word_offset():
+    assert emb.workspace_error_offset() == 4
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(emb, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(emb, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        emb.lib()

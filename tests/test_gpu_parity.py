@@ -1,0 +1,286 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Integer outputs (unique keys, counts, segment offsets, sort permutation,
+number of unique ids) must be bit-exact; floating outputs must meet the
+row-norm relative tolerance (1e-5 fp32, 1e-2 for bf16 table rows); dyadic
+inputs must agree bit-exactly in any summation order.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _rand_batch(rng, rows, B, lmax, empty_frac=0.0, zipf=None):
+    T = len(rows)
+    M = T * B
+    lens = rng.integers(1, lmax + 1, size=M).astype(np.int32)
+    if empty_frac:
+        lens[rng.random(M) < empty_frac] = 0
+    offsets = np.zeros(M + 1, np.int32)
+    offsets[1:] = np.cumsum(lens)
+    idx = np.zeros(int(offsets[-1]), np.int32)
+    for m in range(M):
+        t = m // B
+        n = int(lens[m])
+        if zipf:
+            ids = (rng.zipf(zipf, size=n) - 1) % rows[t]
+        else:
+            ids = rng.integers(0, rows[t], size=n)
+        idx[offsets[m]:offsets[m + 1]] = ids
+    return offsets, idx
+
+
+def _row_offset(rows):
+    ro = np.zeros(len(rows) + 1, np.int64)
+    ro[1:] = np.cumsum(rows)
+    return ro
+
+
+# ------------------------------------------------------------- small cases
+
+@pytest.mark.parametrize("pool", ["sum", "mean"])
+@pytest.mark.parametrize("opt", ["sgd", "adagrad"])
+def test_small_random_multi_table(pool, opt):
+    _say(f"case small_random pool={pool} opt={opt}")
+    rng = np.random.default_rng(1)
+    rows = [1000, 37, 5000]
+    B, D = 300, 64
+    off, idx = _rand_batch(rng, rows, B, 40, empty_frac=0.05, zipf=1.3)
+    W = rng.uniform(-0.5, 0.5, size=(sum(rows), D)).astype(np.float32)
+    G = rng.standard_normal(size=(len(off) - 1, D)).astype(np.float32)
+    parity.run_case(_row_offset(rows), W, off, idx, G, B, pool, opt, 0.01, 1e-8)
+
+
+@pytest.mark.parametrize("pool", ["sum", "mean"])
+def test_dyadic_inputs_bit_exact(pool):
+    """Dyadic W and G: every fp32 sum is exact, so GPU == oracle bit for bit."""
+    _say(f"case dyadic pool={pool}")
+    rng = np.random.default_rng(2)
+    rows = [3000, 700]
+    B, D = 500, 32
+    lmax = 8
+    off, idx = _rand_batch(rng, rows, B, lmax, empty_frac=0.1, zipf=1.5)
+    if pool == "mean":  # bag lengths in {0, 1, 2, 4, 8} keep 1/L dyadic
+        lens = np.diff(off)
+        lens = np.where(lens == 0, 0, 2 ** np.floor(np.log2(np.maximum(lens, 1)))).astype(np.int32)
+        off = np.zeros_like(off)
+        off[1:] = np.cumsum(lens)
+        idx = np.concatenate([idx[:0]] + [rng.integers(0, rows[m // B], size=lens[m]) for m in range(len(lens))])
+    W = (rng.integers(-512, 512, size=(sum(rows), D)) / 1024.0).astype(np.float32)
+    G = (rng.integers(-64, 64, size=(len(off) - 1, D)) / 64.0).astype(np.float32)
+    parity.run_case(_row_offset(rows), W, off, idx.astype(np.int32), G, B, pool, "sgd", 0.5, 0.0, exact=True)
+
+
+def test_empty_bags_and_empty_batch():
+    _say("case empty bags")
+    rng = np.random.default_rng(3)
+    rows = [100]
+    B, D = 64, 16
+    lens = np.zeros(B, np.int32)
+    lens[[1, 5, 6, 63]] = [3, 1, 70, 2]
+    off = np.zeros(B + 1, np.int32)
+    off[1:] = np.cumsum(lens)
+    idx = rng.integers(0, 100, size=int(off[-1])).astype(np.int32)
+    W = rng.standard_normal((100, D)).astype(np.float32)
+    G = rng.standard_normal((B, D)).astype(np.float32)
+    g, _, _ = parity.run_case(_row_offset(rows), W, off, idx, G, B, "mean", "adagrad", 0.05, 1e-8)
+    assert np.all(g.out[lens == 0] == 0)
+    # the whole batch empty
+    off0 = np.zeros(B + 1, np.int32)
+    g0, _, _ = parity.run_case(_row_offset(rows), W, off0, np.zeros(0, np.int32), G, B, "sum", "sgd", 0.1, 0.0)
+    assert g0.num_unique == 0 and np.all(g0.out == 0)
+
+
+def test_single_id():
+    _say("case N=1")
+    W = np.arange(64, dtype=np.float32).reshape(4, 16)
+    off = np.array([0, 0, 1], np.int32)
+    g, _, _ = parity.run_case([0, 4], W, off, np.array([3], np.int32), np.ones((2, 16), np.float32), 2, "sum",
+                              "sgd", 0.25, 0.0, exact=True)
+    assert g.num_unique == 1 and list(g.perm) == [0]
+
+
+def test_all_same_id_one_heavy_segment():
+    """100k lookups of one row: a single segment spanning ~1600 reduce chunks."""
+    _say("case all same id")
+    rng = np.random.default_rng(4)
+    B, D = 2000, 64
+    off, _ = _rand_batch(rng, [10], B, 100)
+    idx = np.full(int(off[-1]), 7, np.int32)
+    W = rng.uniform(-1, 1, size=(10, D)).astype(np.float32)
+    G = rng.standard_normal((B, D)).astype(np.float32)
+    g, _, _ = parity.run_case([0, 10], W, off, idx, G, B, "sum", "adagrad", 0.01, 1e-8)
+    assert g.num_unique == 1 and g.counts[0] == len(idx)
+
+
+@pytest.mark.parametrize("n", [63, 64, 65, 2047, 2048, 2049, 4097, 10_000])
+def test_tile_and_chunk_boundaries(n):
+    _say(f"case N={n}")
+    rng = np.random.default_rng(n)
+    rows = 5000
+    B = max(1, n // 7)
+    # exactly n ids over B bags
+    cuts = np.sort(rng.integers(0, n + 1, size=B - 1))
+    off = np.concatenate([[0], cuts, [n]]).astype(np.int32)
+    idx = ((rng.zipf(1.2, size=n) - 1) % rows).astype(np.int32)
+    W = rng.uniform(-1, 1, size=(rows, 16)).astype(np.float32)
+    G = rng.standard_normal((B, 16)).astype(np.float32)
+    parity.run_case([0, rows], W, off, idx, G, B, "sum", "adagrad", 0.01, 1e-8)
+
+
+@pytest.mark.parametrize("rows", [2, 1024, 1025, 1 << 20, (1 << 20) + 1])
+def test_key_bit_boundaries(rows):
+    """Key widths that change the number of radix passes; ids 0 and rows-1 present."""
+    _say(f"case rows={rows}")
+    rng = np.random.default_rng(rows)
+    B, D = 700, 8
+    off, idx = _rand_batch(rng, [rows], B, 30)
+    idx[:5] = 0
+    idx[-5:] = rows - 1
+    W = rng.uniform(-1, 1, size=(rows, D)).astype(np.float32)
+    G = rng.standard_normal((B, D)).astype(np.float32)
+    parity.run_case([0, rows], W, off, idx, G, B, "sum", "sgd", 0.01, 0.0)
+
+
+@pytest.mark.parametrize("dtype,D", [("fp32", 4), ("fp32", 16), ("fp32", 48), ("fp32", 128), ("fp32", 256),
+                                     ("fp32", 512), ("fp32", 1024), ("bf16", 8), ("bf16", 64), ("bf16", 128),
+                                     ("bf16", 200), ("bf16", 1024)])
+def test_row_widths(dtype, D):
+    _say(f"case dtype={dtype} D={D}")
+    rng = np.random.default_rng(D)
+    rows = [3000, 2000]
+    B = 200
+    off, idx = _rand_batch(rng, rows, B, 60, zipf=1.2)
+    Wf = rng.uniform(-0.5, 0.5, size=(sum(rows), D)).astype(np.float32)
+    if dtype == "bf16":
+        u = Wf.view(np.uint32).astype(np.uint64)
+        W = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    else:
+        W = Wf
+    G = rng.standard_normal((len(off) - 1, D)).astype(np.float32)
+    parity.run_case(_row_offset(rows), W, off, idx, G, B, "mean", "adagrad", 0.01, 1e-8)
+
+
+def test_unfused_equals_fused():
+    _say("case unfused vs fused")
+    rng = np.random.default_rng(5)
+    rows = [20000]
+    B, D = 1000, 64
+    off, idx = _rand_batch(rng, rows, B, 50, zipf=1.1)
+    W = rng.uniform(-0.1, 0.1, size=(rows[0], D)).astype(np.float32)
+    G = rng.standard_normal((B, D)).astype(np.float32)
+    g1, s1, d1 = parity.run_case([0, rows[0]], W, off, idx, G, B, "sum", "adagrad", 0.01, 1e-8, fused=True)
+    g2, s2, d2 = parity.run_case([0, rows[0]], W, off, idx, G, B, "sum", "adagrad", 0.01, 1e-8, fused=False)
+    np.testing.assert_array_equal(g1.grad_rows, g2.grad_rows)
+    keys = g1.unique_keys
+    np.testing.assert_array_equal(d1.rows(keys), d2.rows(keys))
+    np.testing.assert_array_equal(d1.state_rows(keys), d2.state_rows(keys))
+
+
+def test_run_to_run_bitwise_identical():
+    _say("case determinism")
+    import torch
+    rng = np.random.default_rng(6)
+    rows = [200000]
+    B, D = 4000, 64
+    off, idx = _rand_batch(rng, rows, B, 60, zipf=1.2)
+    W = rng.uniform(-0.1, 0.1, size=(rows[0], D)).astype(np.float32)
+    G = rng.standard_normal((B, D)).astype(np.float32)
+    outs = []
+    for rep in range(3):
+        dl = parity.device_layer_from_host([0, rows[0]], W, np.zeros(rows[0], np.float32))
+        g = parity.gpu_step(dl, off, idx, G, B, "sum", "adagrad", 0.01, 1e-8)
+        outs.append((g, dl.rows(g.unique_keys), dl.state_rows(g.unique_keys)))
+        torch.cuda.synchronize()
+    for g, r, h in outs[1:]:
+        np.testing.assert_array_equal(g.out, outs[0][0].out)
+        np.testing.assert_array_equal(g.grad_rows, outs[0][0].grad_rows)
+        np.testing.assert_array_equal(g.perm, outs[0][0].perm)
+        np.testing.assert_array_equal(r, outs[0][1])
+        np.testing.assert_array_equal(h, outs[0][2])
+
+
+def test_workspace_reuse_with_varying_batch_sizes():
+    """One workspace, batches of very different N in a row (big, small, big)."""
+    _say("case workspace reuse")
+    import oracle
+    import paper_2112_02752_amd as emb
+    rng = np.random.default_rng(7)
+    rows = 100000
+    D = 16
+    W = rng.uniform(-1, 1, size=(rows, D)).astype(np.float32)
+    dl = parity.device_layer_from_host([0, rows], W, None)
+    layer = emb.Layer(dl.tables, "sum", "sgd", 0.01, 0.0, None, max_indices=200_000, max_bags=5000)
+    store = oracle.RowStore(W.copy())
+    for B, lmax in [(4000, 80), (3, 2), (1, 1), (5000, 60), (50, 10)]:
+        off, idx = _rand_batch(rng, [rows], B, lmax, zipf=1.3)
+        G = rng.standard_normal((B, D)).astype(np.float32)
+        g = parity.gpu_step(dl, off, idx, G, B, "sum", "sgd", 0.01, 0.0, layer=layer)
+        o_out, o_dd, o_gr = oracle.step(1, np.array([0, rows], np.int64), B, off, idx, G, store, "sum", "sgd",
+                                        0.01, 0.0)
+        parity.check_against_oracle(g, o_out, o_dd, o_gr)
+        parity.check_rows(dl, store, o_dd.unique_keys, "sgd")
+
+
+def test_validate_batch_flags():
+    _say("case validate")
+    import torch
+    import paper_2112_02752_amd as emb
+    W = torch.zeros((10, 16), dtype=torch.float32, device="cuda")
+    t = emb.Tables(W, [0, 4, 10])
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def check(offsets, idx, B):
+        b = emb.Batch(torch.tensor(offsets, dtype=torch.int32, device="cuda"),
+                      torch.tensor(idx, dtype=torch.int32, device="cuda"), B)
+        emb.validate_batch(t, b, flag)
+        torch.cuda.synchronize()
+        return int(flag.item())
+
+    assert check([0, 2, 3], [3, 0, 5], 1) == 0
+    assert check([0, 2, 3], [4, 0, 5], 1) == 8          # id 4 >= rows of table 0
+    assert check([0, 2, 3], [3, 0, 6], 1) == 8          # id 6 >= rows of table 1
+    assert check([0, 3, 2], [3, 0, 1], 1) & 2           # decreasing offsets
+    assert check([1, 2, 3], [3, 0, 1], 1) & 1           # offsets[0] != 0
+
+
+# --------------------------------------------------------- full workloads
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_workload_full_size_one_step(name):
+    w = synth.workload(name)
+    _say(f"case workload {name} rows={w.total_rows} D={w.dim} {w.dtype}")
+    parity.run_workload(w, steps=1)
+
+
+def test_c5_three_consecutive_steps():
+    w = synth.workload("c5")
+    _say("case c5 x3 steps")
+    parity.run_workload(w, steps=3)
+
+
+def test_c2_unfused_path():
+    w = synth.workload("c2")
+    _say("case c2 unfused")
+    parity.run_workload(w, steps=1, fused=False)

@@ -24,11 +24,13 @@ TOL_BF16_ROWS = 1e-2
 
 
 def rel_rownorm(x: np.ndarray, y: np.ndarray) -> float:
-    x = np.asarray(x, dtype=np.float64).reshape(len(x), -1)
-    y = np.asarray(y, dtype=np.float64).reshape(len(y), -1)
+    x = np.asarray(x, dtype=np.float64)
+    y = np.asarray(y, dtype=np.float64)
     assert x.shape == y.shape, (x.shape, y.shape)
     if x.size == 0:
         return 0.0
+    x = x.reshape(len(x), -1)
+    y = y.reshape(len(y), -1)
     den = np.maximum(np.abs(y).max(axis=1), 1e-30)
     return float((np.abs(x - y).max(axis=1) / den).max())
 

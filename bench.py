@@ -1,0 +1,243 @@
+"""Benchmark: one training step of one GPU's shard of the pooled embedding layer.
+
+A step is the whole hot path over one fresh seeded batch: pooled forward,
+id dedup (sort + unique), gradient segment-reduce fused with the row-wise
+Adagrad / SGD update.  Inputs (tables, optimizer state, all batches and
+upstream gradients) are resident in HBM before the timed region starts.
+
+Prints ONE JSON line.  `value` is pooled lookups per second of whole steps;
+`roofline` prices the dominant kernel (the pooled forward) against HBM
+bandwidth; `cpu_baseline` is the CPU oracle timed on this host's cores on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "pooled lookups/sec (fwd+bwd+update) and achieved HBM GB/s vs peak, 1 GPU"
+COUNTERS = os.path.join(ROOT, "profiles", "pool_fwd_c3_counters.txt")
+FWD_SOURCE = os.path.join(ROOT, "paper_2112_02752_amd", "csrc", "pool_fwd.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (for counter calibration)")
+    return ap.parse_args()
+
+
+def byte_models(w, N: float, U: float):
+    """Algorithmic bytes per step of each phase, logical (every lookup's row)
+    and compulsory (every distinct row once per phase)."""
+    M, D = w.num_bags, w.dim
+    sw = 4 if w.dtype == "fp32" else 2
+    s_state = 4 if w.opt == "adagrad" else 0
+    fwd_fixed = 4 * (M + 1) + 4 * N + 4 * M * D
+    fwd_log = fwd_fixed + N * D * sw
+    fwd_comp = fwd_fixed + U * D * sw
+    dedup = 8 * N + 12 * U + 4
+    bwd_fixed = 4 * N + 4 * (U + 1) + 4 * (M + 1) + 4 * U + 2 * U * D * sw + 2 * U * s_state
+    bwd_log = bwd_fixed + N * D * 4
+    bwd_comp = bwd_fixed + M * D * 4
+    return {"fwd": (fwd_log, fwd_comp), "dedup": (dedup, dedup), "bwd_update": (bwd_log, bwd_comp)}
+
+
+def global_keys(row_offset, B, offsets, indices):
+    bag = np.repeat(np.arange(len(offsets) - 1), np.diff(offsets))
+    return (np.asarray(row_offset, dtype=np.int64)[bag // B] + indices).astype(np.uint32)
+
+
+def file_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def counter_traffic():
+    """HBM bytes per forward launch from the committed rocprofv3 counter
+    summary, scaled by the copy-kernel calibration; None if the kernel source
+    changed since the counters were taken."""
+    if not os.path.exists(COUNTERS):
+        return None
+    kv = {}
+    for line in open(COUNTERS):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    try:
+        if kv.get("source_sha") != file_sha(FWD_SOURCE):
+            return None
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 28  # 1 GiB of fp32
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 3}), flush=True)
+
+
+def cpu_baseline(w, batches, budget_s: float):
+    """The oracle, untuned, single-threaded, on whole steps of the same workload."""
+    import oracle
+    import synth
+    done_n, elapsed, steps = 0, 0.0, 0
+    for b in batches:
+        keys = np.unique(global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices))
+        store = oracle.RowStore(synth.weight_rows(w, keys), keys=keys,
+                                state=np.zeros(len(keys), np.float32) if w.opt == "adagrad" else None)
+        t0 = time.perf_counter()
+        oracle.step(w.num_tables, w.row_offset, w.bags_per_table, b.offsets, b.indices, b.grad, store, w.pool,
+                    w.opt, w.lr, w.eps)
+        elapsed += time.perf_counter() - t0
+        done_n += len(b.indices)
+        steps += 1
+        if elapsed >= budget_s:
+            break
+    return {"value": done_n / elapsed, "unit": "lookups/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} whole steps of {w.name} (fwd+dedup+reduce+update), {done_n} lookups, "
+                      f"{elapsed:.1f} s, single thread"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build measures one GPU's shard of the embedding layer; "
+              "multi-GPU runs are not part of it", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    import paper_2112_02752_amd as emb
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    w = synth.workload(args.workload)
+    dev = "cuda"
+    total = args.warmup + args.steps
+    print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
+    t0 = time.time()
+    batches = [synth.make_batch(w, s) for s in range(total)]
+    print(f"[bench] generated {total} batches in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    W = torch.empty((w.total_rows, w.dim), dtype=torch.float32 if w.dtype == "fp32" else torch.bfloat16,
+                    device=dev)
+    synth.fill_device_weights(w, W.data_ptr(), int(torch.cuda.current_stream().cuda_stream))
+    state = torch.zeros(w.total_rows, dtype=torch.float32, device=dev) if w.opt == "adagrad" else None
+    tables = emb.Tables(W, [int(x) for x in w.row_offset])
+    nmax = max(len(b.indices) for b in batches)
+    layer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags)
+    dev_batches = []
+    for b in batches:
+        off = torch.from_numpy(b.offsets).to(dev)
+        idx = torch.from_numpy(b.indices).to(dev)
+        g = torch.from_numpy(b.grad).to(dev)
+        dev_batches.append((emb.Batch(off, idx, w.bags_per_table), g, len(b.indices)))
+    out = torch.empty((w.num_bags, w.dim), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    sp = int(stream.cuda_stream)
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        b, g, _ = dev_batches[i]
+        if ev:
+            ev[0].record(stream)
+        emb.pool_fwd(tables, b, w.pool, out, sp)
+        if ev:
+            ev[1].record(stream)
+        emb.unique_ids(tables, b, layer.unique_keys, layer.counts, layer.seg_offsets, layer.sort_perm,
+                       layer.num_unique, layer.ws, sp)
+        if ev:
+            ev[2].record(stream)
+        emb.grad_reduce(tables, b, w.pool, g, layer.sort_perm, layer.seg_offsets, layer.unique_keys,
+                        layer.num_unique, layer.ws, opt=w.opt, lr=w.lr, eps=w.eps, state=state, stream=sp)
+        if ev:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region: K whole steps, one fresh batch each; HIP events on the
+    # launch stream bracket each phase of every step
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k, i in enumerate(range(args.warmup, total)):
+        step(i, evs[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
+    ph = {"fwd": [], "dedup": [], "bwd_update": []}
+    for e in evs:
+        ph["fwd"].append(e[0].elapsed_time(e[1]) * 1e-3)
+        ph["dedup"].append(e[1].elapsed_time(e[2]) * 1e-3)
+        ph["bwd_update"].append(e[2].elapsed_time(e[3]) * 1e-3)
+    gpu_step_s = float(np.mean([e[0].elapsed_time(e[3]) * 1e-3 for e in evs]))
+
+    # unique counts of the timed batches (for the byte models)
+    us = []
+    for i in range(args.warmup, total):
+        b = batches[i]
+        us.append(len(np.unique(global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices))))
+    N_avg = n_lookups / args.steps
+    U_avg = float(np.mean(us))
+    models = byte_models(w, N_avg, U_avg)
+    t_phase = {k: float(np.mean(v)) for k, v in ph.items()}
+    fwd_log, fwd_comp = models["fwd"]
+    achieved = fwd_log / t_phase["fwd"] / 1e9
+    traffic = counter_traffic()
+    step_log = sum(v[0] for v in models.values())
+    step_comp = sum(v[1] for v in models.values())
+    ms = elapsed / args.steps * 1e3
+    line = {
+        "metric": METRIC, "value": n_lookups / elapsed, "unit": "lookups/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if w.dtype == "fp32" else "bf16 tables, f32 accumulate",
+        "data": "synthetic (seeded Zipf ids, N(0,1) upstream gradients, U(-0.01,0.01) tables)",
+        "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
+                   "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
+                   "table_bytes": w.weight_bytes},
+        "roofline": {"bound": "hbm", "kernel": "k_pool_fwd (emb_pool_fwd)", "model": "logical",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "bytes_per_launch": fwd_log,
+                     "compulsory_bytes_per_launch": fwd_comp,
+                     "compulsory_frac": fwd_comp / t_phase["fwd"] / 1e9 / HBM_PEAK_GBS,
+                     "avg_launch_us": t_phase["fwd"] * 1e6},
+        "step_bytes": {"logical": step_log, "compulsory": step_comp,
+                       "logical_GBs": step_log / (ms * 1e-3) / 1e9,
+                       "compulsory_GBs": step_comp / (ms * 1e-3) / 1e9},
+        "phase_us": {k: v * 1e6 for k, v in t_phase.items()},
+        "gpu_us_per_step": gpu_step_s * 1e6,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(w, batches, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -119,11 +119,15 @@ class Tables:
     row_offset: Sequence[int]
 
     def c(self) -> CTables:
-        import torch
-        ro = (ctypes.c_int64 * len(self.row_offset))(*[int(x) for x in self.row_offset])
-        self._ro = ro  # keep alive for the call
-        dt = BF16 if self.weights.dtype == torch.bfloat16 else FP32
-        return CTables(len(self.row_offset) - 1, ro, int(self.weights.shape[1]), dt, _ptr(self.weights))
+        key = (_ptr(self.weights), tuple(self.weights.shape), self.weights.dtype)
+        if getattr(self, "_ckey", None) != key:
+            import torch
+            ro = (ctypes.c_int64 * len(self.row_offset))(*[int(x) for x in self.row_offset])
+            dt = BF16 if self.weights.dtype == torch.bfloat16 else FP32
+            self._ro = ro  # kept alive with the struct
+            self._c = CTables(len(self.row_offset) - 1, ro, int(self.weights.shape[1]), dt, _ptr(self.weights))
+            self._ckey = key
+        return self._c
 
 
 @dataclass
@@ -134,8 +138,12 @@ class Batch:
     bags_per_table: int
 
     def c(self) -> CBatch:
-        n = int(self.indices.numel())
-        return CBatch(self.bags_per_table, _ptr(self.offsets), _ptr(self.indices) if n else None, n)
+        key = (_ptr(self.offsets), _ptr(self.indices), int(self.indices.numel()), self.bags_per_table)
+        if getattr(self, "_ckey", None) != key:
+            n = key[2]
+            self._c = CBatch(self.bags_per_table, key[0], key[1] if n else None, n)
+            self._ckey = key
+        return self._c
 
 
 def workspace_size(num_indices: int, num_bags: int, dim: int) -> int:

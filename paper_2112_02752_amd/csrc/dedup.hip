@@ -50,11 +50,12 @@ struct PrepArgs {
   const int32_t* offsets;
   const int32_t* idx;
   TableOffsets ro;
-  int32_t B, M, bags_per_block, npass;
+  int32_t B, M, bags_per_block, npass, histograms;
   int32_t shift[kMaxPasses], bits[kMaxPasses];
   uint32_t* keys_out;  // null for one table (the ids are the keys)
   int32_t* bag_of;
-  uint32_t* totals;    // [kMaxPasses][kMaxDigits], zero on entry
+  float* inv_len;      // [M]: 1 / bag length (0 for an empty bag)
+  uint32_t* totals;    // [kMaxPasses][kMaxDigits], zero on entry (only with histograms)
   WsHeader* hdr;
   uint64_t* uniq_status;
   int32_t uniq_tiles;
@@ -62,31 +63,64 @@ struct PrepArgs {
   int64_t pass_status_words;
 };
 
+// A block owns a contiguous range of bags and therefore of positions.  The
+// bags' offsets are staged in LDS; every thread takes positions of the range
+// in strides, finds each one's bag by a binary search in LDS, and writes the
+// bag id (and the key for several tables).  With `histograms`, the digits of
+// every radix pass are counted in LDS and added to the global totals.
 __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
+  constexpr int UN = 8;
   __shared__ uint32_t hist[kMaxPasses * kMaxDigits];
+  __shared__ int32_t s_off[kPrepMaxBags + 1];
   const int tid = threadIdx.x;
-  for (int i = tid; i < a.npass * kMaxDigits; i += kPrepThreads) hist[i] = 0;
-  if (blockIdx.x == 0 && tid == 0) a.hdr->gen = a.hdr->gen + 1u;
+  if (a.histograms)
+    for (int i = tid; i < a.npass * kMaxDigits; i += kPrepThreads) hist[i] = 0;
+  if (blockIdx.x == 0 && tid == 0) {
+    a.hdr->gen = a.hdr->gen + 1u;
+    a.hdr->ticket[kSlotUnique] = 0u;  // the previous call's unique scan is complete
+  }
   for (int i = blockIdx.x * kPrepThreads + tid; i < a.uniq_tiles; i += gridDim.x * kPrepThreads)
     a.uniq_status[i] = 0;
   for (int64_t i = (int64_t)blockIdx.x * kPrepThreads + tid; i < a.pass_status_words;
        i += (int64_t)gridDim.x * kPrepThreads)
     a.pass_status[i] = 0;
-  __syncthreads();
-  const int wave = tid >> 6, lane = tid & (kWave - 1);
   const int m0 = blockIdx.x * a.bags_per_block;
-  const int m1 = min(a.M, m0 + a.bags_per_block);
-  for (int m = m0 + wave; m < m1; m += kPrepThreads / kWave) {
-    const uint32_t base = a.ro.off[m / a.B];
-    const int s = a.offsets[m], e = a.offsets[m + 1];
-    for (int j = s + lane; j < e; j += kWave) {
-      const uint32_t key = base + (uint32_t)a.idx[j];
-      a.bag_of[j] = m;
-      if (a.keys_out) a.keys_out[j] = key;
-      for (int p = 0; p < a.npass; ++p)
-        atomicAdd(&hist[p * kMaxDigits + ((key >> a.shift[p]) & ((1u << a.bits[p]) - 1u))], 1u);
+  const int nb = min(a.M - m0, a.bags_per_block);
+  for (int i = tid; i <= nb; i += kPrepThreads) s_off[i] = a.offsets[m0 + i];
+  __syncthreads();
+  for (int i = tid; i < nb; i += kPrepThreads) {
+    const int L = s_off[i + 1] - s_off[i];
+    a.inv_len[m0 + i] = L > 0 ? 1.0f / (float)L : 0.0f;
+  }
+  const int j0 = s_off[0], j1 = s_off[nb];
+  for (int jb = j0; jb < j1; jb += kPrepThreads * UN) {
+    int32_t id[UN];
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int j = jb + u * kPrepThreads + tid;
+      id[u] = j < j1 ? a.idx[j] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int j = jb + u * kPrepThreads + tid;
+      if (j < j1) {
+        // last bag i with s_off[i] <= j (empty bags share an offset with the next one)
+        int lo = 0, hi = nb - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (s_off[mid] <= j) lo = mid; else hi = mid - 1;
+        }
+        const int m = m0 + lo;
+        const uint32_t key = a.ro.off[m / a.B] + (uint32_t)id[u];
+        a.bag_of[j] = m;
+        if (a.keys_out) a.keys_out[j] = key;
+        if (a.histograms)
+          for (int p = 0; p < a.npass; ++p)
+            atomicAdd(&hist[p * kMaxDigits + ((key >> a.shift[p]) & ((1u << a.bits[p]) - 1u))], 1u);
+      }
     }
   }
+  if (!a.histograms) return;
   __syncthreads();
   for (int p = 0; p < a.npass; ++p) {
     const int nd = 1 << a.bits[p];
@@ -102,12 +136,19 @@ __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
 struct PassArgs {
   const uint32_t* keys_in;
   const int32_t* vals_in;  // null: values are the positions
+  const int32_t* bags_in;  // bag of each element (travels with it through the passes)
   uint32_t* keys_out;
   int32_t* vals_out;
-  uint32_t* totals;        // this pass's digit totals; cleared by the last tile
-  uint64_t* status;        // [tiles][status_stride], zeroed by k_prepare of the same call
+  int32_t* bags_out;
+  uint32_t* totals;        // this pass's digit totals (global histogram)
+  uint32_t* prev_totals;   // the previous pass's totals, cleared here (null for the first pass)
+  uint64_t* status;        // look-back: [tiles][status_stride], zeroed by k_prepare of the same call
+  uint64_t* rows;          // published tile counts (tag << 32 | count): [tiles][status_stride]
+  uint64_t* grp;           // published group sums, same form: [groups][status_stride]
   WsHeader* hdr;
   int32_t N, ntiles, shift, bits, pass, status_stride;
+  int32_t coresident;      // 1: every tile is resident at once (tile = block index, two-level prefix;
+                           //    digit totals come from the published counts, not from `totals`)
 };
 
 // Exclusive scan of n = 2^RB counters held in LDS, by kSortThreads threads.
@@ -139,6 +180,77 @@ __device__ __forceinline__ void block_excl_scan(uint32_t* arr, uint32_t* s_wsum)
   __syncthreads();
 }
 
+// Count of digit d in all tiles before `tile`: walks back over the tiles'
+// status words, kLookbackWindow of them per round (loaded together), adding
+// aggregates until it reaches an inclusive prefix.  A word that is not yet
+// published (wrong tag or no flag) ends the round; the next round starts
+// there.  The wait is bounded: running out of spins flags an error.
+__device__ __forceinline__ uint32_t lookback_digit(const uint64_t* status, int stride, int tile, int d,
+                                                   uint32_t tag, uint32_t* err) {
+  uint32_t excl = 0;
+  int j = tile - 1;
+  uint32_t spins = 0;
+  while (j >= 0) {
+    uint64_t sv[kLookbackWindow];
+#pragma unroll
+    for (int k = 0; k < kLookbackWindow; ++k)
+      sv[k] = (j - k >= 0) ? ld_acquire_u64(status + (size_t)(j - k) * stride + d) : 0;
+    int consumed = 0;
+    bool stop = false, inc = false;
+#pragma unroll
+    for (int k = 0; k < kLookbackWindow; ++k) {
+      if (!stop) {
+        const uint64_t flag = (sv[k] >> 30) & 3u;
+        if (j - k >= 0 && (uint32_t)(sv[k] >> 32) == tag && flag != 0) {
+          excl += (uint32_t)(sv[k] & 0x3fffffffu);
+          consumed = k + 1;
+          if (flag == kFlagInc) inc = stop = true;
+        } else {
+          stop = true;
+        }
+      }
+    }
+    if (inc) break;
+    j -= consumed;
+    if (consumed == 0) {
+      if (++spins > kSpinLimit) {
+        atomicOr(err, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  return excl;
+}
+
+// Sum over rows r in [lo, hi) of the counts published in m[r][d] as
+// (tag << 32 | count) words: kPrefixGroup words are loaded together; a word
+// that does not carry this pass's tag yet is polled again (bounded).
+__device__ __forceinline__ uint32_t sum_column(const uint64_t* m, int stride, int lo, int hi, int d, uint32_t tag,
+                                               uint32_t* err) {
+  uint32_t sum = 0;
+  for (int base = lo; base < hi; base += kPrefixGroup) {
+    uint64_t v[kPrefixGroup];
+#pragma unroll
+    for (int i = 0; i < kPrefixGroup; ++i)
+      v[i] = base + i < hi ? ld_acquire_u64(m + (size_t)(base + i) * stride + d) : ((uint64_t)tag << 32);
+#pragma unroll
+    for (int i = 0; i < kPrefixGroup; ++i) {
+      uint32_t spins = 0;
+      while ((uint32_t)(v[i] >> 32) != tag) {
+        if (++spins > kSpinLimit) {
+          atomicOr(err, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        v[i] = ld_acquire_u64(m + (size_t)(base + i) * stride + d);
+      }
+      sum += (uint32_t)v[i];
+    }
+  }
+  return sum;
+}
+
 template <int RB>
 __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   constexpr int ND = 1 << RB;
@@ -149,12 +261,22 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   __shared__ uint32_t s_gbase[ND];
   __shared__ uint32_t s_keys[kSortTile];
   __shared__ int32_t s_vals[kSortTile];
+  __shared__ int32_t s_bags[kSortTile];
   __shared__ uint32_t s_wsum[NW];
-  __shared__ int s_tile, s_last;
+  __shared__ int s_tile;
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  if (tid == 0) s_tile = (int)atomic_add_u32(&a.hdr->ticket[a.pass], 1u);
+  if (a.coresident) {
+    if (tid == 0) s_tile = blockIdx.x;
+  } else if (tid == 0) {
+    s_tile = (int)atomic_add_u32(&a.hdr->ticket[a.pass], 1u);
+  }
   for (int i = tid; i < NW * ND; i += kSortThreads) (&s_cnt[0][0])[i] = 0u;
+  // the previous pass is complete: clear its totals and ticket for the next call
+  if (blockIdx.x == 0 && a.prev_totals) {
+    for (int d = tid; d < kMaxDigits; d += kSortThreads) a.prev_totals[d] = 0u;
+    if (tid == 0) a.hdr->ticket[a.pass - 1] = 0u;
+  }
   __syncthreads();
   const int tile = s_tile;
   const uint32_t mask = (1u << a.bits) - 1u;
@@ -162,13 +284,14 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   const int64_t wbase = (int64_t)tile * kSortTile + w * (kWave * kSortItems);
 
   uint32_t key[kSortItems], dig[kSortItems], lrank[kSortItems];
-  int32_t val[kSortItems];
+  int32_t val[kSortItems], bag[kSortItems];
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
     const int64_t pos = wbase + i * kWave + lane;
     const bool valid = pos < a.N;
     key[i] = valid ? a.keys_in[pos] : 0u;
     val[i] = valid ? (a.vals_in ? a.vals_in[pos] : (int32_t)pos) : 0;
+    bag[i] = valid ? a.bags_in[pos] : 0;
     dig[i] = (key[i] >> a.shift) & mask;
   }
 
@@ -208,47 +331,76 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
       }
       my_cnt[k] = run;
       s_tstart[d] = run;
-      s_gbase[d] = a.totals[d];
+      if (!a.coresident) s_gbase[d] = a.totals[d];
+    }
+  }
+
+  const uint64_t tag_hi = (uint64_t)tag << 32;
+  uint32_t excl[DPT];
+  if (a.coresident) {
+    // publish this tile's counts as tagged words
+    uint64_t* row = a.rows + (size_t)tile * a.status_stride;
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      if (d < ND) st_u64(row + d, tag_hi | my_cnt[k]);
+    }
+  } else {
+    uint64_t* st = a.status + (size_t)tile * a.status_stride;
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      if (d < ND) st_u64(st + d, tag_hi | ((tile == 0 ? kFlagInc : kFlagAgg) << 30) | my_cnt[k]);
     }
   }
   __syncthreads();
   block_excl_scan<RB>(s_tstart, s_wsum);
-  block_excl_scan<RB>(s_gbase, s_wsum);
+  if (!a.coresident) block_excl_scan<RB>(s_gbase, s_wsum);
 
-  // decoupled look-back: the digit's count in all earlier tiles
-  uint64_t* st = a.status + (size_t)tile * a.status_stride;
-  const uint64_t tag_hi = (uint64_t)tag << 32;
+  if (a.coresident) {
+    // two-level prefix: groups of kPrefixGroup tiles; the last tile of a group
+    // publishes the group's sum, every tile adds the sums of the earlier
+    // groups and the counts of the earlier tiles of its own group; the digit
+    // totals are the sum of all groups
+    const int g = tile / kPrefixGroup, g0 = g * kPrefixGroup;
+    const int g1 = min(a.ntiles, g0 + kPrefixGroup);
+    const int ngroups = (a.ntiles + kPrefixGroup - 1) / kPrefixGroup;
+    if (tile == g1 - 1) {
+      uint64_t* gs = a.grp + (size_t)g * a.status_stride;
 #pragma unroll
-  for (int k = 0; k < DPT; ++k) {
-    const int d = tid + k * kSortThreads;
-    if (d < ND) st_u64(st + d, tag_hi | ((tile == 0 ? kFlagInc : kFlagAgg) << 30) | my_cnt[k]);
-  }
-  if (tile > 0) {
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        if (d < ND) st_u64(gs + d, tag_hi | sum_column(a.rows, a.status_stride, g0, g1, d, tag, &a.hdr->error));
+      }
+    }
 #pragma unroll
     for (int k = 0; k < DPT; ++k) {
       const int d = tid + k * kSortThreads;
-      if (d >= ND) continue;
-      uint32_t excl = 0;
-      int j = tile - 1;
-      uint32_t spins = 0;
-      while (j >= 0) {
-        const uint64_t sv = ld_acquire_u64(a.status + (size_t)j * a.status_stride + d);
-        const uint64_t flag = (sv >> 30) & 3u;
-        if ((uint32_t)(sv >> 32) == tag && flag != 0) {
-          excl += (uint32_t)(sv & 0x3fffffffu);
-          if (flag == kFlagInc) break;
-          --j;
-          continue;
-        }
-        if (++spins > kSpinLimit) {
-          atomicOr(&a.hdr->error, 1u);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
+      excl[k] = 0;
+      if (d < ND) {
+        const uint32_t before = sum_column(a.grp, a.status_stride, 0, g, d, tag, &a.hdr->error);
+        s_gbase[d] = before + sum_column(a.grp, a.status_stride, g, ngroups, d, tag, &a.hdr->error);
+        excl[k] = before + sum_column(a.rows, a.status_stride, g0, tile, d, tag, &a.hdr->error);
       }
-      st_u64(st + d, tag_hi | (kFlagInc << 30) | (excl + my_cnt[k]));
-      s_gbase[d] += excl;
     }
+    __syncthreads();
+    block_excl_scan<RB>(s_gbase, s_wsum);
+  } else {
+    uint64_t* st = a.status + (size_t)tile * a.status_stride;
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      excl[k] = 0;
+      if (d < ND && tile > 0) {
+        excl[k] = lookback_digit(a.status, a.status_stride, tile, d, tag, &a.hdr->error);
+        st_u64(st + d, tag_hi | (kFlagInc << 30) | (excl[k] + my_cnt[k]));
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int d = tid + k * kSortThreads;
+    if (d < ND) s_gbase[d] += excl[k];
   }
   __syncthreads();
 
@@ -260,6 +412,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
       const uint32_t lp = s_tstart[dig[i]] + s_cnt[w][dig[i]] + lrank[i];
       s_keys[lp] = key[i];
       s_vals[lp] = val[i];
+      s_bags[lp] = bag[i];
     }
   }
   __syncthreads();
@@ -272,20 +425,9 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
     if (dst < (uint32_t)a.N) {
       a.keys_out[dst] = k;
       a.vals_out[dst] = s_vals[s];
+      a.bags_out[dst] = s_bags[s];
     } else {
       atomicOr(&a.hdr->error, 2u);  // digit totals inconsistent with the keys
-    }
-  }
-
-  // the last tile to finish clears this pass's totals and counters
-  __syncthreads();
-  if (tid == 0) s_last = atomic_add_u32(&a.hdr->done[a.pass], 1u) == (uint32_t)(a.ntiles - 1);
-  __syncthreads();
-  if (s_last) {
-    for (int d = tid; d < ND; d += kSortThreads) a.totals[d] = 0u;
-    if (tid == 0) {
-      a.hdr->ticket[a.pass] = 0u;
-      a.hdr->done[a.pass] = 0u;
     }
   }
 }
@@ -301,6 +443,9 @@ struct UniqArgs {
   int32_t* num_unique;
   int32_t* chunk_seg;  // [nchunks+1]: segment of position c*kChunk; [nchunks] = U
   uint64_t* status;    // [tiles], zeroed by k_prepare of the same call
+  uint32_t* prev_totals;  // the last sort pass's totals, cleared here
+  int32_t last_pass;
+  int32_t coresident;  // 1: tile = block index
   WsHeader* hdr;
 };
 
@@ -314,9 +459,18 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   __shared__ uint32_t s_keys[kUniqTile];
   __shared__ uint32_t s_wc[NW], s_wq[NW];
   __shared__ uint32_t s_pc, s_pq, s_prev;
-  __shared__ int s_tile, s_last;
+  __shared__ int s_tile;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  if (tid == 0) s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
+  if (a.coresident) {
+    if (tid == 0) s_tile = blockIdx.x;
+  } else if (tid == 0) {
+    s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
+  }
+  // the sort is complete: clear the last pass's totals and ticket for the next call
+  if (blockIdx.x == 0) {
+    for (int d = tid; d < kMaxDigits; d += kUniqThreads) a.prev_totals[d] = 0u;
+    if (tid == 0) a.hdr->ticket[a.last_pass] = 0u;
+  }
   __syncthreads();
   const int tile = s_tile;
   const int64_t tbase = (int64_t)tile * kUniqTile;
@@ -360,34 +514,54 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     tile_c += s_wc[ww];
     tile_q = max(tile_q, s_wq[ww]);
   }
-  if (tid == 0) {
+  if (w == 0) {
+    // wave-parallel look-back: lane k reads the status of tile (j - k)
     uint32_t pc = 0, pq = 0;
     if (tile == 0) {
-      st_u64(a.status, pack_uniq(kFlagInc, tile_c, tile_q));
+      if (lane == 0) st_u64(a.status, pack_uniq(kFlagInc, tile_c, tile_q));
     } else {
-      st_u64(a.status + tile, pack_uniq(kFlagAgg, tile_c, tile_q));
+      if (lane == 0) st_u64(a.status + tile, pack_uniq(kFlagAgg, tile_c, tile_q));
       int j = tile - 1;
       uint32_t spins = 0;
-      while (j >= 0) {
-        const uint64_t sv = ld_acquire_u64(a.status + j);
+      while (true) {
+        const int jj = j - lane;
+        const uint64_t sv = jj >= 0 ? ld_acquire_u64(a.status + jj) : 0;
         const uint64_t flag = sv >> 62;
-        if (flag != 0) {
-          pc += (uint32_t)((sv >> 31) & 0x7fffffffu);
-          pq = max(pq, (uint32_t)(sv & 0x7fffffffu));
-          if (flag == kFlagInc) break;
-          --j;
-          continue;
+        const uint64_t not_ready = __ballot(!(jj >= 0 && flag != 0));
+        const uint64_t inc = __ballot(jj >= 0 && flag == kFlagInc);
+        const int first_nr = not_ready ? __builtin_ctzll(not_ready) : kWave;
+        const int first_inc = inc ? __builtin_ctzll(inc) : kWave;
+        const bool done = first_inc < first_nr;
+        const int take = done ? first_inc + 1 : first_nr;
+        uint32_t c = 0, q = 0;
+        if (lane < take) {
+          c = (uint32_t)((sv >> 31) & 0x7fffffffu);
+          q = (uint32_t)(sv & 0x7fffffffu);
         }
-        if (++spins > kSpinLimit) {
-          atomicOr(&a.hdr->error, 1u);
-          break;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+          c += __shfl_xor(c, o, kWave);
+          const uint32_t qo = __shfl_xor(q, o, kWave);
+          q = q > qo ? q : qo;
         }
-        __builtin_amdgcn_s_sleep(1);
+        pc += c;
+        pq = max(pq, q);
+        if (done) break;
+        j -= take;
+        if (take == 0) {
+          if (++spins > kSpinLimit) {
+            if (lane == 0) atomicOr(&a.hdr->error, 1u);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
       }
-      st_u64(a.status + tile, pack_uniq(kFlagInc, pc + tile_c, max(pq, tile_q)));
+      if (lane == 0) st_u64(a.status + tile, pack_uniq(kFlagInc, pc + tile_c, max(pq, tile_q)));
     }
-    s_pc = pc;
-    s_pq = pq;
+    if (lane == 0) {
+      s_pc = pc;
+      s_pq = pq;
+    }
   }
   __syncthreads();
   uint32_t u = s_pc + c_ex;
@@ -413,13 +587,6 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
       }
     }
   }
-  __syncthreads();
-  if (tid == 0) s_last = atomic_add_u32(&a.hdr->done[kSlotUnique], 1u) == (uint32_t)(a.ntiles - 1);
-  __syncthreads();
-  if (s_last && tid == 0) {
-    a.hdr->ticket[kSlotUnique] = 0u;
-    a.hdr->done[kSlotUnique] = 0u;
-  }
 }
 
 __global__ void k_unique_empty(int32_t* num_unique, int32_t* seg) {
@@ -433,6 +600,26 @@ template <int RB>
 hipError_t launch_pass(const PassArgs& pa, int tiles, hipStream_t s) {
   hipLaunchKernelGGL(k_sort_pass<RB>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, pa);
   return hipGetLastError();
+}
+
+template <int RB>
+const void* pass_kernel() {
+  return reinterpret_cast<const void*>(&k_sort_pass<RB>);
+}
+
+const void* pass_kernel_bits(int bits) {
+  switch (bits) {
+    case 1: return pass_kernel<1>();
+    case 2: return pass_kernel<2>();
+    case 3: return pass_kernel<3>();
+    case 4: return pass_kernel<4>();
+    case 5: return pass_kernel<5>();
+    case 6: return pass_kernel<6>();
+    case 7: return pass_kernel<7>();
+    case 8: return pass_kernel<8>();
+    case 9: return pass_kernel<9>();
+    default: return pass_kernel<10>();
+  }
 }
 
 hipError_t launch_pass_bits(const PassArgs& pa, int tiles, hipStream_t s) {
@@ -466,14 +653,27 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   const int uniq_tiles = (N + kUniqTile - 1) / kUniqTile;
   const int nchunks = (N + kChunk - 1) / kChunk;
 
+  int max_bits = 1;
+  for (int i = 0; i < p.plan.passes; ++i) max_bits = p.plan.bits[i] > max_bits ? p.plan.bits[i] : max_bits;
+  const int status_stride = 1 << max_bits;
+  // every tile of a pass resident at once: tile = block index and a
+  // two-level published-count prefix; otherwise tickets and a look-back
+  int sort_cores = 1;
+  for (int i = 0; i < p.plan.passes; ++i)
+    if (sort_tiles > resident_blocks(pass_kernel_bits(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
+  const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
+
   PrepArgs pa{};
   pa.offsets = p.offsets;
   pa.idx = p.idx;
   pa.ro = p.ro;
   pa.B = p.B;
   pa.M = p.M;
-  pa.bags_per_block = p.M / 256 > 4 ? (p.M + 255) / 256 : 4;
+  // about kPrepPositions positions per block (more with global histograms, fewer atomics)
+  const int64_t want = (int64_t)(sort_cores ? kPrepPositions : 4 * kPrepPositions) * p.M / (p.N > 0 ? p.N : 1);
+  pa.bags_per_block = (int)(want < 1 ? 1 : (want > kPrepMaxBags ? kPrepMaxBags : want));
   pa.npass = p.plan.passes;
+  pa.histograms = !sort_cores;
   for (int i = 0; i < kMaxPasses; ++i) {
     pa.shift[i] = p.plan.shift[i];
     pa.bits[i] = p.plan.bits[i];
@@ -481,34 +681,42 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
   pa.keys_out = p.T > 1 ? keys_built : nullptr;
   pa.bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
+  pa.inv_len = reinterpret_cast<float*>(ws + L.inv_len);
   pa.totals = reinterpret_cast<uint32_t*>(ws + L.totals);
   pa.hdr = hdr;
   pa.uniq_status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
   pa.uniq_tiles = uniq_tiles;
-  int max_bits = 1;
-  for (int i = 0; i < p.plan.passes; ++i) max_bits = p.plan.bits[i] > max_bits ? p.plan.bits[i] : max_bits;
-  const int status_stride = 1 << max_bits;
   pa.pass_status = reinterpret_cast<uint64_t*>(ws + L.pass_status);
-  pa.pass_status_words = (int64_t)sort_tiles * status_stride;
-  const int prep_blocks = (p.M + pa.bags_per_block - 1) / pa.bags_per_block;
-  hipLaunchKernelGGL(k_prepare, dim3((unsigned)(prep_blocks > 0 ? prep_blocks : 1)), dim3(kPrepThreads), 0, s, pa);
+  pa.pass_status_words = sort_cores ? 0 : (int64_t)sort_tiles * status_stride;
+  const int prep_blocks = p.M > 0 ? (p.M + pa.bags_per_block - 1) / pa.bags_per_block : 1;
+  hipLaunchKernelGGL(k_prepare, dim3((unsigned)prep_blocks), dim3(kPrepThreads), 0, s, pa);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
 
   const uint32_t* kin = p.T > 1 ? keys_built : reinterpret_cast<const uint32_t*>(p.idx);
   const int32_t* vin = nullptr;
+  const int32_t* bin = reinterpret_cast<const int32_t*>(ws + L.bag_of);
   uint32_t* keys_a = reinterpret_cast<uint32_t*>(ws + L.keys_a);
   uint32_t* keys_b = reinterpret_cast<uint32_t*>(ws + L.keys_b);
   int32_t* vals_a = reinterpret_cast<int32_t*>(ws + L.vals_a);
   int32_t* vals_b = reinterpret_cast<int32_t*>(ws + L.vals_b);
+  int32_t* bags_a = reinterpret_cast<int32_t*>(ws + L.bags_a);
+  int32_t* bags_b = reinterpret_cast<int32_t*>(ws + L.bags_b);
   for (int ps = 0; ps < p.plan.passes; ++ps) {
+    const bool last = ps == p.plan.passes - 1;
     PassArgs xa{};
     xa.keys_in = kin;
     xa.vals_in = vin;
+    xa.bags_in = bin;
     xa.keys_out = (ps % 2 == 0) ? keys_a : keys_b;
-    xa.vals_out = (ps == p.plan.passes - 1) ? p.sort_perm : ((ps % 2 == 0) ? vals_a : vals_b);
+    xa.vals_out = last ? p.sort_perm : ((ps % 2 == 0) ? vals_a : vals_b);
+    xa.bags_out = last ? reinterpret_cast<int32_t*>(ws + L.sorted_bag) : ((ps % 2 == 0) ? bags_a : bags_b);
     xa.totals = reinterpret_cast<uint32_t*>(ws + L.totals) + ps * kMaxDigits;
+    xa.prev_totals = ps > 0 ? reinterpret_cast<uint32_t*>(ws + L.totals) + (ps - 1) * kMaxDigits : nullptr;
     xa.status = reinterpret_cast<uint64_t*>(ws + L.pass_status);
+    xa.rows = reinterpret_cast<uint64_t*>(ws + L.rows);
+    xa.grp = reinterpret_cast<uint64_t*>(ws + L.grp);
+    xa.coresident = sort_cores;
     xa.hdr = hdr;
     xa.N = N;
     xa.ntiles = sort_tiles;
@@ -520,6 +728,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     if (e != hipSuccess) return e;
     kin = xa.keys_out;
     vin = xa.vals_out;
+    bin = xa.bags_out;
   }
 
   UniqArgs ua{};
@@ -533,6 +742,9 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   ua.num_unique = p.num_unique;
   ua.chunk_seg = reinterpret_cast<int32_t*>(ws + L.chunk_seg);
   ua.status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
+  ua.prev_totals = reinterpret_cast<uint32_t*>(ws + L.totals) + (p.plan.passes - 1) * kMaxDigits;
+  ua.last_pass = p.plan.passes - 1;
+  ua.coresident = uniq_cores;
   ua.hdr = hdr;
   hipLaunchKernelGGL(k_unique, dim3((unsigned)uniq_tiles), dim3(kUniqThreads), 0, s, ua);
   return hipGetLastError();

@@ -17,7 +17,7 @@ constexpr int kWave = 64;
 constexpr int kMaxPasses = 4;
 constexpr int kMaxDigitBits = 10;
 constexpr int kMaxDigits = 1 << kMaxDigitBits;
-constexpr int kSortThreads = 256;
+constexpr int kSortThreads = 512;
 constexpr int kSortItems = 8;
 constexpr int kSortTile = kSortThreads * kSortItems;
 
@@ -26,42 +26,57 @@ constexpr int kUniqThreads = 256;
 constexpr int kUniqItems = 8;
 constexpr int kUniqTile = kUniqThreads * kUniqItems;
 
+// tile status words a look-back round loads together
+constexpr int kLookbackWindow = 8;
+// tiles per group of the two-level prefix used when all tiles are resident
+constexpr int kPrefixGroup = 16;
+
 // prepare kernel (keys, bag ids, digit histograms)
 constexpr int kPrepThreads = 256;
+constexpr int kPrepMaxBags = 1024;     // bags of one block (offsets staged in LDS)
+constexpr int kPrepPositions = 2048;   // positions a block aims at
 
 // gradient reduce: segments longer than kChunk positions are "heavy" and are
 // summed in aligned chunks of kChunk sorted positions, then combined.
 constexpr int kChunk = 64;
+// light segments each lane group carries at once, and the longest such
+// segment (longer light ones are summed by a whole wavefront)
+constexpr int kSlots = 2;
+constexpr int kTinySeg = 16;
+// heavy-segment combine: threads per block, chunks a block checks
+constexpr int kCombineThreads = 1024;
+constexpr int kCombineChunks = 16;
 
 // ticket / done counter slots in the workspace header
 constexpr int kSlotUnique = kMaxPasses;
 
 // Workspace header (device).  gen counts emb_unique_ids calls; it tags the
-// sort look-back words so they never need clearing.
+// sort's published counts so they never need clearing.  A tile ticket is
+// cleared by the kernel that runs after the one that used it.
 struct WsHeader {
   uint32_t gen;
   uint32_t error;
   uint32_t ticket[8];
-  uint32_t done[8];
-  uint32_t pad[46];
+  uint32_t pad[54];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 
 struct WsLayout {
-  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bag_of, pass_status, uniq_status, chunk_seg,
-      partials, total;
-  int64_t sort_tiles, uniq_tiles, chunks;
+  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_bag, inv_len,
+      pass_status, rows,
+      grp, uniq_status, chunk_seg, partials, total;
+  int64_t sort_tiles, uniq_tiles, chunks, groups;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
-  (void)M;
   WsLayout L{};
   int64_t n = N > 0 ? N : 1;
   L.sort_tiles = (n + kSortTile - 1) / kSortTile;
   L.uniq_tiles = (n + kUniqTile - 1) / kUniqTile;
   L.chunks = (n + kChunk - 1) / kChunk;
+  L.groups = (L.sort_tiles + kPrefixGroup - 1) / kPrefixGroup;
   size_t off = 0;
   L.hdr = off;
   off += sizeof(WsHeader);
@@ -77,10 +92,22 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   off = align256(off + sizeof(int32_t) * n);
   L.vals_b = off;
   off = align256(off + sizeof(int32_t) * n);
+  L.bags_a = off;
+  off = align256(off + sizeof(int32_t) * n);
+  L.bags_b = off;
+  off = align256(off + sizeof(int32_t) * n);
   L.bag_of = off;
   off = align256(off + sizeof(int32_t) * n);
+  L.sorted_bag = off;
+  off = align256(off + sizeof(int32_t) * n);
+  L.inv_len = off;
+  off = align256(off + sizeof(float) * (M > 0 ? M : 1));
   L.pass_status = off;
   off = align256(off + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
+  L.rows = off;
+  off = align256(off + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
+  L.grp = off;
+  off = align256(off + sizeof(uint64_t) * L.groups * kMaxDigits);
   L.uniq_status = off;
   off = align256(off + sizeof(uint64_t) * L.uniq_tiles);
   L.chunk_seg = off;
@@ -113,6 +140,10 @@ __device__ __forceinline__ void st_u64(uint64_t* p, uint64_t v) {
 __device__ __forceinline__ uint32_t atomic_add_u32(uint32_t* p, uint32_t v) {
   return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+
+// Workgroups of `kernel` (with `threads` per block) that the current device
+// holds at once, all compute units together (cached per device and kernel).
+int resident_blocks(const void* kernel, int threads);
 
 // Bounded spin budget of a look-back wait; running out sets an error bit and
 // lets the wave continue, so every wave always exits.

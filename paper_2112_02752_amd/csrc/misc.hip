@@ -1,4 +1,9 @@
-// Batch validation and workspace clearing (off the timed path).
+// Batch validation, workspace clearing (off the timed path) and the
+// residency query used to pick the sort's prefix scheme.
+#include <map>
+#include <mutex>
+#include <utility>
+
 #include "emb_common.h"
 #include "kernels.h"
 
@@ -59,6 +64,23 @@ hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s) {
   hipLaunchKernelGGL(k_validate, dim3((unsigned)blocks), dim3(256), 0, s, p.offsets, p.idx, p.ro, p.B, p.M, p.N,
                      p.flag);
   return hipGetLastError();
+}
+
+int resident_blocks(const void* kernel, int threads) {
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  auto key = std::make_pair(dev, kernel);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) per_cu = 0;
+  const int n = cus * per_cu;
+  cache[key] = n;
+  return n;
 }
 
 }  // namespace emb

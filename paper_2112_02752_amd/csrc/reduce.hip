@@ -30,12 +30,11 @@ struct Upd {
 
 struct RArgs {
   const float* G;
-  const int32_t* perm;
   const int32_t* seg;
   const uint32_t* ukeys;
   const int32_t* num_unique;
-  const int32_t* bag_of;
-  const int32_t* offsets;
+  const int32_t* sorted_bag;  // bag of every sorted position
+  const float* inv_len;       // 1 / bag length (mean pooling)
   const int32_t* chunk_seg;
   float* grad_rows;
   float* partials;
@@ -100,11 +99,31 @@ __device__ __forceinline__ void add_row(const float* src, float sc, int D, int s
   }
 }
 
-// Write g_u (if grad_rows) and apply the optimizer to row r (if fused).
-// Called by the G lanes of one group, all active.
+// The table row and optimizer state an update reads, loaded ahead of time.
+template <int NV>
+struct RowPre {
+  float w[NV][4];
+  float h;
+};
+
 template <typename TW, int G, int NV>
-__device__ __forceinline__ void finalize(const Upd& up, float* grad_rows, int64_t u, uint32_t r,
-                                         const float (&acc)[NV][4], int sub) {
+__device__ __forceinline__ void prefetch_row(const Upd& up, uint32_t r, int sub, RowPre<NV>& pre) {
+  pre.h = 0.f;
+  if (!up.fuse) return;
+  if (up.opt == EMB_OPT_ADAGRAD_ROWWISE) pre.h = up.state[r];
+  const TW* wp = reinterpret_cast<const TW*>(up.W) + (size_t)r * (size_t)up.D;
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int c0 = (v * G + sub) * 4;
+    if (c0 < up.D) Row4<TW>::load(wp + c0, pre.w[v]);
+  }
+}
+
+// Write g_u (if grad_rows) and apply the optimizer to row r (if fused) from
+// the prefetched row.  Called by the G lanes of one group, all active.
+template <typename TW, int G, int NV>
+__device__ __forceinline__ void apply_row(const Upd& up, float* grad_rows, int64_t u, uint32_t r,
+                                          const float (&acc)[NV][4], const RowPre<NV>& pre, int sub) {
   const int D = up.D;
   if (grad_rows) {
     float* gp = grad_rows + u * D;
@@ -124,7 +143,7 @@ __device__ __forceinline__ void finalize(const Upd& up, float* grad_rows, int64_
       for (int e = 0; e < 4; ++e) sq += acc[v][e] * acc[v][e];
 #pragma unroll
     for (int o = 1; o < G; o <<= 1) sq += __shfl_xor(sq, o, kWave);
-    const float h = up.state[r] + sq / (float)D;
+    const float h = pre.h + sq / (float)D;
     if (sub == 0) up.state[r] = h;
     step = up.lr / (sqrtf(h) + up.eps);
   }
@@ -134,44 +153,87 @@ __device__ __forceinline__ void finalize(const Upd& up, float* grad_rows, int64_
     const int c0 = (v * G + sub) * 4;
     if (c0 < D) {
       float w[4];
-      Row4<TW>::load(wp + c0, w);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = w[e] - step * acc[v][e];
+      for (int e = 0; e < 4; ++e) w[e] = pre.w[v][e] - step * acc[v][e];
       Row4<TW>::store(wp + c0, w);
     }
   }
 }
 
-__device__ __forceinline__ float bag_scale(const RArgs& a, int bag) {
-  return a.pool == EMB_POOL_MEAN ? 1.0f / (float)(a.offsets[bag + 1] - a.offsets[bag]) : 1.0f;
+template <typename TW, int G, int NV>
+__device__ __forceinline__ void finalize(const Upd& up, float* grad_rows, int64_t u, uint32_t r,
+                                         const float (&acc)[NV][4], int sub) {
+  RowPre<NV> pre;
+  prefetch_row<TW, G, NV>(up, r, sub, pre);
+  apply_row<TW, G, NV>(up, grad_rows, u, r, acc, pre, sub);
 }
 
-// Sum the gradient rows of sorted positions [lo, hi) (hi - lo <= 64) with all
-// groups of the wavefront, then reduce the groups.  Result valid in group 0.
+// Metadata of one heavy-segment check: the pieces of heavy segments that
+// lie in chunk c.  Slot 0: the segment holding the chunk's first position
+// (if heavy); slot 1: a different heavy segment holding its last position.
+struct ChunkPieces {
+  int lo[2], hi[2];
+  int u1, s1, e1;  // the segment holding the chunk's last position
+};
+
+__device__ __forceinline__ ChunkPieces chunk_pieces(const RArgs& a, int c, int U) {
+  ChunkPieces r;
+  const int p0 = c * kChunk, p1 = min(a.N, p0 + kChunk);
+  const int u0 = a.chunk_seg[c], cs1 = a.chunk_seg[c + 1];
+  // all needed offsets in one round of independent loads
+  const int s0 = a.seg[u0], e0 = a.seg[u0 + 1];
+  const int sc = a.seg[cs1];
+  const int scm = cs1 > 0 ? a.seg[cs1 - 1] : 0;
+  const int scp = cs1 < U ? a.seg[cs1 + 1] : a.N;
+  if (sc == p1) {  // position p1 starts segment cs1: the chunk ends with segment cs1 - 1
+    r.u1 = cs1 - 1;
+    r.s1 = scm;
+    r.e1 = sc;
+  } else {
+    r.u1 = cs1;
+    r.s1 = sc;
+    r.e1 = scp;
+  }
+  r.lo[0] = r.hi[0] = r.lo[1] = r.hi[1] = 0;
+  if (e0 - s0 > kChunk) {
+    r.lo[0] = p0;
+    r.hi[0] = min(p1, e0);
+  }
+  if (r.u1 != u0 && r.e1 - r.s1 > kChunk) {
+    r.lo[1] = r.s1;
+    r.hi[1] = p1;
+  }
+  return r;
+}
+
+// Sum of the scaled gradient rows of sorted positions [lo, hi) (at most 64)
+// by all groups of the wavefront, every row load issued up front; the groups
+// are reduced with a butterfly, the result is valid in every group.
 template <int G, int NV>
 __device__ __forceinline__ void wave_piece_sum(const RArgs& a, int lo, int hi, int g, int sub, int lane,
                                                float (&acc)[NV][4]) {
   constexpr int RPI = kWave / G;
+  constexpr int UN = 8;
   const int n = hi - lo;
   int mbag = 0;
   float msc = 0.f;
   if (lane < n) {
-    mbag = a.bag_of[a.perm[lo + lane]];
-    msc = bag_scale(a, mbag);
+    mbag = a.sorted_bag[lo + lane];
+    msc = a.pool == EMB_POOL_MEAN ? a.inv_len[mbag] : 1.0f;
   }
   zero<G, NV>(acc);
-  for (int i0 = 0; i0 < n; i0 += RPI * 4) {
-    int bag[4];
-    float sc[4];
+  for (int i0 = 0; i0 < n; i0 += RPI * UN) {
+    int bag[UN];
+    float sc[UN];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < UN; ++q) {
       const int k = i0 + q * RPI + g;
       bag[q] = __shfl(mbag, k & (kWave - 1), kWave);
       sc[q] = __shfl(msc, k & (kWave - 1), kWave);
-      if (k >= n) sc[q] = 0.f, bag[q] = -1;
+      if (k >= n) bag[q] = -1;
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+    for (int q = 0; q < UN; ++q)
       if (bag[q] >= 0) add_row<G, NV>(a.G + (size_t)bag[q] * a.D, sc[q], a.D, sub, acc);
   }
 #pragma unroll
@@ -182,8 +244,111 @@ __device__ __forceinline__ void wave_piece_sum(const RArgs& a, int lo, int hi, i
       for (int e = 0; e < 4; ++e) acc[v][e] += __shfl_xor(acc[v][e], o, kWave);
 }
 
+template <int G, int NV>
+__device__ __forceinline__ void store_row(float* dst, int D, int sub, const float (&acc)[NV][4]) {
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int c0 = (v * G + sub) * 4;
+    if (c0 < D) Row4<float>::store(dst + c0, acc[v]);
+  }
+}
+
+// slots per lane group: one lane of the wavefront reads each segment's offsets
+constexpr int slots_for(int rpi) { return rpi * kSlots <= kWave ? kSlots : kWave / rpi; }
+// register budget of the main kernel: 7 waves per SIMD for rows of up to 256 floats
+constexpr int reduce_waves(int nv) { return nv == 1 ? 7 : 4; }
+
+// Light segments, kSlots per lane group: the segments of a batch are
+// consecutive; their offsets and keys are read by one lane each, the bags of
+// their positions by the group's lanes, then every slot's rows are summed
+// with the loads of all slots in flight together.
 template <typename TW, int G, int NV>
-__global__ __launch_bounds__(256) void k_reduce_main(RArgs a) {
+__device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, int g, int sub, int lane) {
+  constexpr int RPI = kWave / G;
+  constexpr int S = slots_for(RPI);
+  int ms = 0, me = 0;
+  uint32_t mk = 0;
+  if (lane < RPI * S && ubase + lane < U) {
+    ms = a.seg[ubase + lane];
+    me = a.seg[ubase + lane + 1];
+    mk = a.ukeys[ubase + lane];
+  }
+  int s[S], c[S];
+  uint32_t r[S];
+  int cmax = 0;
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int src = j * RPI + g;
+    s[j] = __shfl(ms, src, kWave);
+    c[j] = __shfl(me, src, kWave) - s[j];
+    r[j] = (uint32_t)__shfl((int)mk, src, kWave);
+    if (ubase + src >= U || c[j] > kTinySeg) c[j] = 0;  // absent, medium or heavy
+    cmax = max(cmax, c[j]);
+  }
+  RowPre<NV> pre[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j)
+    if (c[j] > 0) prefetch_row<TW, G, NV>(a.up, r[j], sub, pre[j]);
+  float acc[S][NV][4];
+#pragma unroll
+  for (int j = 0; j < S; ++j) zero<G, NV>(acc[j]);
+  for (int i0 = 0; i0 < cmax; i0 += G) {
+    int mb[S];
+    float msc[S];
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      mb[j] = 0;
+      msc[j] = 0.f;
+      if (i0 + sub < c[j]) {
+        mb[j] = a.sorted_bag[s[j] + i0 + sub];
+        msc[j] = a.pool == EMB_POOL_MEAN ? a.inv_len[mb[j]] : 1.0f;
+      }
+    }
+    const int n = min(G, cmax - i0);
+    for (int i = 0; i < n; i += 2) {
+      // two positions of every slot per round: their loads are issued together
+      int bag[2][S];
+      float sc[2][S];
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int j = 0; j < S; ++j) {
+          const int src = g * G + ((i + q) & (G - 1));
+          bag[q][j] = __shfl(mb[j], src, kWave);
+          sc[q][j] = __shfl(msc[j], src, kWave);
+          if (i + q >= n || i0 + i + q >= c[j]) bag[q][j] = -1;
+        }
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int j = 0; j < S; ++j)
+          if (bag[q][j] >= 0) add_row<G, NV>(a.G + (size_t)bag[q][j] * a.D, sc[q][j], a.D, sub, acc[j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < S; ++j)
+    if (c[j] > 0) apply_row<TW, G, NV>(a.up, a.grad_rows, ubase + j * RPI + g, r[j], acc[j], pre[j], sub);
+
+  // medium segments of the batch (kTinySeg < count <= kChunk): the whole
+  // wavefront sums each one with all its rows in flight, group 0 applies it
+  const int cnt = me - ms;
+  uint64_t medium = __ballot(lane < RPI * S && ubase + lane < U && cnt > kTinySeg && cnt <= kChunk);
+  while (medium) {
+    const int l = __builtin_ctzll(medium);
+    medium &= medium - 1;
+    const int lo = __shfl(ms, l, kWave), hi = __shfl(me, l, kWave);
+    const uint32_t key = (uint32_t)__shfl((int)mk, l, kWave);
+    RowPre<NV> pm;
+    if (g == 0) prefetch_row<TW, G, NV>(a.up, key, sub, pm);
+    float am[NV][4];
+    wave_piece_sum<G, NV>(a, lo, hi, g, sub, lane, am);
+    if (g == 0) apply_row<TW, G, NV>(a.up, a.grad_rows, ubase + l, key, am, pm, sub);
+  }
+}
+
+template <typename TW, int G, int NV>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_waves(NV), reduce_waves(NV)))) void k_reduce_main(
+    RArgs a) {
   constexpr int RPI = kWave / G;
   const int lane = threadIdx.x & (kWave - 1), g = lane / G, sub = lane % G;
   const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -192,87 +357,54 @@ __global__ __launch_bounds__(256) void k_reduce_main(RArgs a) {
 
   // heavy pieces: one wavefront per aligned chunk of sorted positions
   for (int c = wave_id; c < a.nchunks; c += nwaves) {
-    const int p0 = c * kChunk, p1 = min(a.N, p0 + kChunk);
-    const int u0 = a.chunk_seg[c];
-    const int s0 = a.seg[u0], e0 = a.seg[u0 + 1];
-    const int cs1 = a.chunk_seg[c + 1];
-    const int u1 = (a.seg[cs1] == p1) ? cs1 - 1 : cs1;
-    float acc[NV][4];
-    if (e0 - s0 > kChunk) {
-      wave_piece_sum<G, NV>(a, p0, min(p1, e0), g, sub, lane, acc);
-      if (g == 0) {
-        float* pp = a.partials + ((size_t)c * 2 + 0) * a.D;
+    const ChunkPieces cp = chunk_pieces(a, c, U);
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int c0 = (v * G + sub) * 4;
-          if (c0 < a.D) Row4<float>::store(pp + c0, acc[v]);
-        }
-      }
-    }
-    if (u1 != u0) {
-      const int s1 = a.seg[u1], e1 = a.seg[u1 + 1];
-      if (e1 - s1 > kChunk) {
-        wave_piece_sum<G, NV>(a, s1, p1, g, sub, lane, acc);
-        if (g == 0) {
-          float* pp = a.partials + ((size_t)c * 2 + 1) * a.D;
-#pragma unroll
-          for (int v = 0; v < NV; ++v) {
-            const int c0 = (v * G + sub) * 4;
-            if (c0 < a.D) Row4<float>::store(pp + c0, acc[v]);
-          }
-        }
+    for (int slot = 0; slot < 2; ++slot) {
+      if (cp.hi[slot] > cp.lo[slot]) {
+        float acc[NV][4];
+        wave_piece_sum<G, NV>(a, cp.lo[slot], cp.hi[slot], g, sub, lane, acc);
+        if (g == 0) store_row<G, NV>(a.partials + ((size_t)c * 2 + slot) * a.D, a.D, sub, acc);
       }
     }
   }
 
-  // light segments: one lane group per segment
-  for (int u = wave_id * RPI + g; u < U; u += nwaves * RPI) {
-    const int s = a.seg[u], e = a.seg[u + 1];
-    if (e - s > kChunk) continue;
-    float acc[NV][4];
-    zero<G, NV>(acc);
-    for (int k0 = s; k0 < e; k0 += G) {
-      const int my = k0 + sub;
-      int mbag = 0;
-      float msc = 0.f;
-      if (my < e) {
-        mbag = a.bag_of[a.perm[my]];
-        msc = bag_scale(a, mbag);
-      }
-      const int n = min(G, e - k0);
-      for (int i = 0; i < n; i += 4) {
-        int bag[4];
-        float sc[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int src = g * G + ((i + q) % G);
-          bag[q] = __shfl(mbag, src, kWave);
-          sc[q] = __shfl(msc, src, kWave);
-          if (i + q >= n) bag[q] = -1;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (bag[q] >= 0) add_row<G, NV>(a.G + (size_t)bag[q] * a.D, sc[q], a.D, sub, acc);
-      }
-    }
-    finalize<TW, G, NV>(a.up, a.grad_rows, u, a.ukeys[u], acc, sub);
-  }
+  // light segments: batches of RPI * slots consecutive segments per wavefront
+  const int per_batch = RPI * slots_for(RPI);
+  for (int ub = wave_id * per_batch; ub < U; ub += nwaves * per_batch) light_batch<TW, G, NV>(a, ub, U, g, sub, lane);
 }
 
-// Combine the partials of each heavy segment, in chunk order, by the block
-// of the segment's first chunk.
+// Heavy segments: the block of a range of kCombineChunks chunks finds (one
+// lane per chunk) the heavy segments whose first position lies in its
+// range, then sums each one's partials in chunk order with all its lane
+// groups and applies the optimizer.
 template <typename TW, int G, int NV>
-__global__ __launch_bounds__(256) void k_reduce_combine(RArgs a) {
+__global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   constexpr int RPI = kWave / G;
-  constexpr int NG = 4 * RPI;
-  __shared__ float s_red[4][G * NV * 4];
-  const int lane = threadIdx.x & (kWave - 1), g = lane / G, sub = lane % G, w = threadIdx.x >> 6;
-  for (int c = blockIdx.x; c < a.nchunks; c += gridDim.x) {
+  constexpr int NWv = kCombineThreads / kWave;
+  constexpr int NG = NWv * RPI;
+  __shared__ float s_red[NWv][G * NV * 4];
+  __shared__ int s_list[kCombineChunks];
+  __shared__ int s_n;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G, w = tid >> 6;
+  const int U = *a.num_unique;
+  const int c0 = blockIdx.x * kCombineChunks;
+  if (tid == 0) s_n = 0;
+  __syncthreads();
+  if (tid < kCombineChunks && c0 + tid < a.nchunks) {
+    const int c = c0 + tid;
+    const ChunkPieces cp = chunk_pieces(a, c, U);
+    // a heavy segment starts in chunk c when the chunk's last segment is
+    // heavy and begins inside the chunk
+    if (cp.e1 - cp.s1 > kChunk && cp.s1 >= c * kChunk) s_list[atomicAdd(&s_n, 1)] = c;
+  }
+  __syncthreads();
+  const int n = s_n;
+  for (int it = 0; it < n; ++it) {
+    const int c = s_list[it];
     const int p0 = c * kChunk, p1 = min(a.N, p0 + kChunk);
     const int cs1 = a.chunk_seg[c + 1];
     const int u1 = (a.seg[cs1] == p1) ? cs1 - 1 : cs1;
     const int s1 = a.seg[u1], e1 = a.seg[u1 + 1];
-    if (s1 < p0 || e1 - s1 <= kChunk) continue;
     const int np = (e1 - 1) / kChunk - c + 1;
     float acc[NV][4];
     zero<G, NV>(acc);
@@ -306,7 +438,7 @@ __global__ __launch_bounds__(256) void k_reduce_combine(RArgs a) {
         for (int e = 0; e < 4; ++e) {
           float t = s_red[0][(v * G + sub) * 4 + e];
 #pragma unroll
-          for (int ww = 1; ww < 4; ++ww) t += s_red[ww][(v * G + sub) * 4 + e];
+          for (int ww = 1; ww < NWv; ++ww) t += s_red[ww][(v * G + sub) * 4 + e];
           acc[v][e] = t;
         }
       finalize<TW, G, NV>(a.up, a.grad_rows, u1, a.ukeys[u1], acc, sub);
@@ -343,7 +475,7 @@ hipError_t launch_reduce_t(const RArgs& ra, int blocks_main, int blocks_comb, hi
   hipLaunchKernelGGL((k_reduce_main<TW, G, NV>), dim3((unsigned)blocks_main), dim3(256), 0, s, ra);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((k_reduce_combine<TW, G, NV>), dim3((unsigned)blocks_comb), dim3(256), 0, s, ra);
+  hipLaunchKernelGGL((k_reduce_combine<TW, G, NV>), dim3((unsigned)blocks_comb), dim3(kCombineThreads), 0, s, ra);
   return hipGetLastError();
 }
 
@@ -398,12 +530,11 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   char* ws = static_cast<char*>(p.ws);
   RArgs ra{};
   ra.G = p.grad_out;
-  ra.perm = p.perm;
   ra.seg = p.seg;
   ra.ukeys = p.ukeys;
   ra.num_unique = p.num_unique;
-  ra.bag_of = reinterpret_cast<const int32_t*>(ws + p.lay.bag_of);
-  ra.offsets = p.offsets;
+  ra.sorted_bag = reinterpret_cast<const int32_t*>(ws + p.lay.sorted_bag);
+  ra.inv_len = reinterpret_cast<const float*>(ws + p.lay.inv_len);
   ra.chunk_seg = reinterpret_cast<const int32_t*>(ws + p.lay.chunk_seg);
   ra.grad_rows = p.grad_rows;
   ra.partials = reinterpret_cast<float*>(ws + p.lay.partials);
@@ -418,11 +549,9 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.up.fuse = p.fuse;
   ra.up.lr = p.lr;
   ra.up.eps = p.eps;
-  // main: enough wavefronts to give every lane group a few segments
-  const int groups_per_block = 4 * (64 / (((p.D + 3) / 4) >= 64 ? 64 : 1));
-  (void)groups_per_block;
-  const int bm = clamp_blocks(((int64_t)p.N + 63) / 64, 1, 2048);
-  const int bc = clamp_blocks(ra.nchunks, 1, 1024);
+  // main: a wavefront per chunk of sorted positions (up to a full device)
+  const int bm = clamp_blocks(((int64_t)ra.nchunks + 3) / 4, 1, 2048);
+  const int bc = clamp_blocks(((int64_t)ra.nchunks + kCombineChunks - 1) / kCombineChunks, 1, 1 << 20);
   return p.dtype == EMB_FP32 ? launch_reduce_dt<float>(ra, bm, bc, s) : launch_reduce_dt<uint16_t>(ra, bm, bc, s);
 }
 

@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3")
+    ap.add_argument("--schedule", choices=("pipelined", "serial"), default="pipelined",
+                    help="pipelined: the id dedup of batch k+1 runs on a second stream alongside the forward and "
+                         "update of batch k (same results as serial)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -181,22 +184,41 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    # timed region: K whole steps, one fresh batch each; HIP events on the
-    # launch stream bracket each phase of every step
+    # serial steps with HIP events on the launch stream around each phase:
+    # per-phase and per-kernel times for the roofline
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k, i in enumerate(range(args.warmup, total)):
         step(i, evs[k])
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
+    serial_elapsed = time.perf_counter() - t_start
     ph = {"fwd": [], "dedup": [], "bwd_update": []}
     for e in evs:
         ph["fwd"].append(e[0].elapsed_time(e[1]) * 1e-3)
         ph["dedup"].append(e[1].elapsed_time(e[2]) * 1e-3)
         ph["bwd_update"].append(e[2].elapsed_time(e[3]) * 1e-3)
     gpu_step_s = float(np.mean([e[0].elapsed_time(e[3]) * 1e-3 for e in evs]))
+
+    if args.schedule == "pipelined":
+        pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags)
+
+        def pstep(i):
+            nxt = dev_batches[i + 1][0] if i + 1 < total else None
+            pipe.step(dev_batches[i][0], out, dev_batches[i][1], next_batch=nxt)
+
+        for i in range(args.warmup):
+            pstep(i)
+        torch.cuda.synchronize()
+        # timed region: K whole steps, one fresh batch each
+        t_start = time.perf_counter()
+        for i in range(args.warmup, total):
+            pstep(i)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+    else:
+        elapsed = serial_elapsed
+    n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
 
     # unique counts of the timed batches (for the byte models)
     us = []
@@ -232,6 +254,8 @@ def main():
                        "compulsory_GBs": step_comp / (ms * 1e-3) / 1e9},
         "phase_us": {k: v * 1e6 for k, v in t_phase.items()},
         "gpu_us_per_step": gpu_step_s * 1e6,
+        "schedule": args.schedule,
+        "serial_ms_per_step": serial_elapsed / args.steps * 1e3,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

@@ -237,3 +237,80 @@ class Layer:
     def step(self, batch: Batch, out, grad_out, stream=None) -> None:
         self.forward(batch, out, stream)
         self.backward(batch, grad_out, stream=stream)
+
+
+class DedupBuffers:
+    """Outputs and workspace of one emb_unique_ids call."""
+
+    def __init__(self, device, max_indices: int, max_bags: int, dim: int):
+        import torch
+        n = max(1, max_indices)
+        wsb = workspace_size(n, max_bags, dim)
+        if wsb == 0:
+            raise ValueError("batch too large for one call")
+        self.ws = torch.empty(wsb, dtype=torch.uint8, device=device)
+        workspace_init(self.ws)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.unique_keys = torch.empty(n, **i32)
+        self.counts = torch.empty(n, **i32)
+        self.seg_offsets = torch.empty(n + 1, **i32)
+        self.sort_perm = torch.empty(n, **i32)
+        self.num_unique = torch.zeros(1, **i32)
+
+
+class Pipeline:
+    """Training steps of the layer with the id dedup of the next batch
+    overlapped with the forward and update of the current one.
+
+    The dedup of a batch reads only its ids, never the table, so it can run
+    ahead on a second stream; the forward of batch k+1 still runs after the
+    update of batch k on the main stream, so every step sees exactly the
+    weights a serial execution would.  Two dedup buffer sets alternate; a set
+    is reused only after the update that read it has completed (events)."""
+
+    def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
+                 max_indices: int = 0, max_bags: int = 0):
+        import torch
+        self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
+        dev = tables.weights.device
+        D = int(tables.weights.shape[1])
+        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(2)]
+        self.main = torch.cuda.current_stream(dev)
+        self.side = torch.cuda.Stream(device=dev)
+        self.dedup_done = [torch.cuda.Event(), torch.cuda.Event()]
+        self.update_done = [torch.cuda.Event(), torch.cuda.Event()]
+        for e in self.update_done:
+            e.record(self.main)
+        self.max_indices = max(1, max_indices)
+        self._pending = None  # (batch, set index) whose dedup is enqueued
+
+    def _dedup(self, batch: Batch, k: int) -> None:
+        import torch
+        if int(batch.indices.numel()) > self.max_indices:
+            raise ValueError("batch larger than the pipeline's buffers")
+        b = self.sets[k]
+        self.side.wait_event(self.update_done[k])
+        with torch.cuda.stream(self.side):
+            unique_ids(self.tables, batch, b.unique_keys, b.counts, b.seg_offsets, b.sort_perm, b.num_unique, b.ws,
+                       int(self.side.cuda_stream))
+        self.dedup_done[k].record(self.side)
+
+    def step(self, batch: Batch, out, grad_out, next_batch: Optional[Batch] = None, grad_rows=None) -> None:
+        """Forward of `batch` into `out`, then its backward with `grad_out`;
+        the dedup of `next_batch` (if given) is started alongside."""
+        if self._pending is None or self._pending[0] is not batch:
+            k = 0 if self._pending is None else 1 - self._pending[1]
+            self._dedup(batch, k)
+            self._pending = (batch, k)
+        k = self._pending[1]
+        if next_batch is not None:
+            self._dedup(next_batch, 1 - k)
+        sm = int(self.main.cuda_stream)
+        pool_fwd(self.tables, batch, self.pool, out, sm)
+        self.main.wait_event(self.dedup_done[k])
+        b = self.sets[k]
+        grad_reduce(self.tables, batch, self.pool, grad_out, b.sort_perm, b.seg_offsets, b.unique_keys,
+                    b.num_unique, b.ws, grad_rows=grad_rows, opt=self.opt, lr=self.lr, eps=self.eps,
+                    state=self.state, stream=sm)
+        self.update_done[k].record(self.main)
+        self._pending = (next_batch, 1 - k) if next_batch is not None else None

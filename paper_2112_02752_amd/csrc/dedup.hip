@@ -54,20 +54,16 @@ struct PrepArgs {
   int32_t shift[kMaxPasses], bits[kMaxPasses];
   uint32_t* keys_out;  // null for one table (the ids are the keys)
   int32_t* bag_of;
-  float* inv_len;      // [M]: 1 / bag length (0 for an empty bag)
   uint32_t* totals;    // [kMaxPasses][kMaxDigits], zero on entry (only with histograms)
-  WsHeader* hdr;
-  uint64_t* uniq_status;
-  int32_t uniq_tiles;
-  uint64_t* pass_status;  // the look-back words this call's passes use
-  int64_t pass_status_words;
 };
 
-// A block owns a contiguous range of bags and therefore of positions.  The
-// bags' offsets are staged in LDS; every thread takes positions of the range
-// in strides, finds each one's bag by a binary search in LDS, and writes the
-// bag id (and the key for several tables).  With `histograms`, the digits of
-// every radix pass are counted in LDS and added to the global totals.
+// Used when the tiles of a pass are not all resident at once (the look-back
+// needs every pass's digit totals up front).  A block owns a contiguous range
+// of bags and therefore of positions.  The bags' offsets are staged in LDS;
+// every thread takes positions of the range in strides, finds each one's bag
+// by a binary search in LDS, and writes the bag id (and the key for several
+// tables); the digits of every radix pass are counted in LDS and added to the
+// global totals.
 __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
   constexpr int UN = 8;
   __shared__ uint32_t hist[kMaxPasses * kMaxDigits];
@@ -75,23 +71,10 @@ __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
   const int tid = threadIdx.x;
   if (a.histograms)
     for (int i = tid; i < a.npass * kMaxDigits; i += kPrepThreads) hist[i] = 0;
-  if (blockIdx.x == 0 && tid == 0) {
-    a.hdr->gen = a.hdr->gen + 1u;
-    a.hdr->ticket[kSlotUnique] = 0u;  // the previous call's unique scan is complete
-  }
-  for (int i = blockIdx.x * kPrepThreads + tid; i < a.uniq_tiles; i += gridDim.x * kPrepThreads)
-    a.uniq_status[i] = 0;
-  for (int64_t i = (int64_t)blockIdx.x * kPrepThreads + tid; i < a.pass_status_words;
-       i += (int64_t)gridDim.x * kPrepThreads)
-    a.pass_status[i] = 0;
   const int m0 = blockIdx.x * a.bags_per_block;
   const int nb = min(a.M - m0, a.bags_per_block);
   for (int i = tid; i <= nb; i += kPrepThreads) s_off[i] = a.offsets[m0 + i];
   __syncthreads();
-  for (int i = tid; i < nb; i += kPrepThreads) {
-    const int L = s_off[i + 1] - s_off[i];
-    a.inv_len[m0 + i] = L > 0 ? 1.0f / (float)L : 0.0f;
-  }
   const int j0 = s_off[0], j1 = s_off[nb];
   for (int jb = j0; jb < j1; jb += kPrepThreads * UN) {
     int32_t id[UN];
@@ -146,6 +129,16 @@ struct PassArgs {
   uint64_t* rows;          // published tile counts (tag << 32 | count): [tiles][status_stride]
   uint64_t* grp;           // published group sums, same form: [groups][status_stride]
   WsHeader* hdr;
+  // first pass with co-resident tiles: the bag of every position is found here
+  // (offsets, idx, ro, B, M); the first pass also clears the unique scan's
+  // look-back words
+  int32_t search_bags;
+  const int32_t* offsets;
+  const int32_t* idx;
+  TableOffsets ro;
+  int32_t B, M, T;
+  uint64_t* uniq_status;
+  int32_t uniq_tiles;
   int32_t N, ntiles, shift, bits, pass, status_stride;
   int32_t coresident;      // 1: every tile is resident at once (tile = block index, two-level prefix;
                            //    digit totals come from the published counts, not from `totals`)
@@ -251,6 +244,54 @@ __device__ __forceinline__ uint32_t sum_column(const uint64_t* m, int stride, in
   return sum;
 }
 
+// Bag of each of this thread's positions of a tile: the bag holding position
+// j is the last m with offsets[m] <= j.  One offset in every S (S chosen so
+// the samples fit one per thread) narrows the tile's bags to a few sample
+// intervals; their offsets are staged in LDS and searched per position.
+// Intervals that do not fit the stage are searched in global memory.
+__device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int32_t* s_boff, int* s_lohi,
+                                               int32_t (&bag)[kSortItems]) {
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  const int64_t p0 = (int64_t)tile * kSortTile;
+  const int64_t p1 = min(p0 + kSortTile, (int64_t)a.N);
+  const int S = (a.M + kSortThreads) / kSortThreads;  // samples offsets[0], offsets[S], ... up to offsets[M]
+  const int nsamp = a.M / S + 1;
+  int samp = 0;
+  if (tid < nsamp) samp = a.offsets[min(tid * S, a.M)];
+  if (tid == 0) s_lohi[0] = s_lohi[1] = 0;
+  __syncthreads();
+  // samples are nondecreasing: count those <= p0 and <= p1 - 1
+  const uint64_t le0 = __ballot(tid < nsamp && samp <= p0);
+  const uint64_t le1 = __ballot(tid < nsamp && samp <= p1 - 1);
+  if (lane == 0) {
+    atomicAdd(&s_lohi[0], (int)__popcll(le0));
+    atomicAdd(&s_lohi[1], (int)__popcll(le1));
+  }
+  __syncthreads();
+  const int m_lo = (s_lohi[0] - 1) * S;                    // a bag at or before the tile's first bag
+  const int m_hi = min((s_lohi[1] - 1) * S + S, a.M);      // an offset index at or after its last bag's end
+  const int nst = m_hi - m_lo + 1;
+  const bool staged = nst <= kBagStage + 1;
+  if (staged)
+    for (int i = tid; i < nst; i += kSortThreads) s_boff[i] = a.offsets[m_lo + i];
+  __syncthreads();
+  (void)w;
+#pragma unroll
+  for (int i = 0; i < kSortItems; ++i) {
+    const int64_t j = p0 + (int64_t)(threadIdx.x >> 6) * (kWave * kSortItems) + i * kWave + lane;
+    bag[i] = 0;
+    if (j < p1) {
+      int lo = 0, hi = nst - 2;  // last idx in [0, nst-2] with offset <= j
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        const int32_t v = staged ? s_boff[mid] : a.offsets[m_lo + mid];
+        if (v <= j) lo = mid; else hi = mid - 1;
+      }
+      bag[i] = m_lo + lo;
+    }
+  }
+}
+
 template <int RB>
 __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   constexpr int ND = 1 << RB;
@@ -264,6 +305,8 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   __shared__ int32_t s_bags[kSortTile];
   __shared__ uint32_t s_wsum[NW];
   __shared__ int s_tile;
+  __shared__ int32_t s_boff[kBagStage + 1];
+  __shared__ int s_lohi[2];
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
   if (a.coresident) {
@@ -280,19 +323,39 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   __syncthreads();
   const int tile = s_tile;
   const uint32_t mask = (1u << a.bits) - 1u;
-  const uint32_t tag = 0x80000000u | (a.hdr->gen * 8u + (uint32_t)a.pass);
+  // the call's tag: the header's generation advances once per call, at its end
+  const uint32_t tag = 0x80000000u | ((a.hdr->gen + 1u) * 8u + (uint32_t)a.pass);
   const int64_t wbase = (int64_t)tile * kSortTile + w * (kWave * kSortItems);
 
   uint32_t key[kSortItems], dig[kSortItems], lrank[kSortItems];
   int32_t val[kSortItems], bag[kSortItems];
+  if (a.pass == 0) {
+    // the unique scan of this call starts from cleared look-back words
+    for (int i = blockIdx.x * kSortThreads + tid; i < a.uniq_tiles; i += gridDim.x * kSortThreads)
+      a.uniq_status[i] = 0;
+    if (blockIdx.x == 0 && tid == 0) a.hdr->ticket[kSlotUnique] = 0u;
+  }
+  if (a.search_bags) {
+    find_tile_bags(a, tile, s_boff, s_lohi, bag);
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const int64_t pos = wbase + i * kWave + lane;
-    const bool valid = pos < a.N;
-    key[i] = valid ? a.keys_in[pos] : 0u;
-    val[i] = valid ? (a.vals_in ? a.vals_in[pos] : (int32_t)pos) : 0;
-    bag[i] = valid ? a.bags_in[pos] : 0;
-    dig[i] = (key[i] >> a.shift) & mask;
+    for (int i = 0; i < kSortItems; ++i) {
+      const int64_t pos = wbase + i * kWave + lane;
+      const bool valid = pos < a.N;
+      const uint32_t id = valid ? (uint32_t)a.idx[pos] : 0u;
+      key[i] = valid ? (a.T > 1 ? a.ro.off[bag[i] / a.B] + id : id) : 0u;
+      val[i] = valid ? (int32_t)pos : 0;
+      dig[i] = (key[i] >> a.shift) & mask;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+      const int64_t pos = wbase + i * kWave + lane;
+      const bool valid = pos < a.N;
+      key[i] = valid ? a.keys_in[pos] : 0u;
+      val[i] = valid ? (a.vals_in ? a.vals_in[pos] : (int32_t)pos) : 0;
+      bag[i] = valid ? a.bags_in[pos] : 0;
+      dig[i] = (key[i] >> a.shift) & mask;
+    }
   }
 
   // rank each element among the earlier elements of its wave with its digit
@@ -466,10 +529,14 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   } else if (tid == 0) {
     s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
   }
-  // the sort is complete: clear the last pass's totals and ticket for the next call
+  // the sort is complete: clear the last pass's totals and ticket and advance
+  // the generation that tags the next call's coordination words
   if (blockIdx.x == 0) {
     for (int d = tid; d < kMaxDigits; d += kUniqThreads) a.prev_totals[d] = 0u;
-    if (tid == 0) a.hdr->ticket[a.last_pass] = 0u;
+    if (tid == 0) {
+      a.hdr->ticket[a.last_pass] = 0u;
+      a.hdr->gen = a.hdr->gen + 1u;
+    }
   }
   __syncthreads();
   const int tile = s_tile;
@@ -643,6 +710,7 @@ hipError_t launch_pass_bits(const PassArgs& pa, int tiles, hipStream_t s) {
 hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   char* ws = static_cast<char*>(p.ws);
   const WsLayout& L = p.lay;
+  char* back = ws_back(p.ws, p.ws_bytes, L);
   WsHeader* hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   if (p.N == 0) {
     hipLaunchKernelGGL(k_unique_empty, dim3(1), dim3(64), 0, s, p.num_unique, p.seg_offsets);
@@ -652,46 +720,43 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   const int sort_tiles = (N + kSortTile - 1) / kSortTile;
   const int uniq_tiles = (N + kUniqTile - 1) / kUniqTile;
   const int nchunks = (N + kChunk - 1) / kChunk;
-
   int max_bits = 1;
   for (int i = 0; i < p.plan.passes; ++i) max_bits = p.plan.bits[i] > max_bits ? p.plan.bits[i] : max_bits;
   const int status_stride = 1 << max_bits;
-  // every tile of a pass resident at once: tile = block index and a
-  // two-level published-count prefix; otherwise tickets and a look-back
+  // every tile of a pass resident at once: tile = block index, bags found by
+  // the first pass, two-level published-count prefix; otherwise a prepare
+  // kernel (bags, keys, digit totals), tickets and a look-back
   int sort_cores = 1;
   for (int i = 0; i < p.plan.passes; ++i)
     if (sort_tiles > resident_blocks(pass_kernel_bits(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
   const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
-
-  PrepArgs pa{};
-  pa.offsets = p.offsets;
-  pa.idx = p.idx;
-  pa.ro = p.ro;
-  pa.B = p.B;
-  pa.M = p.M;
-  // about kPrepPositions positions per block (more with global histograms, fewer atomics)
-  const int64_t want = (int64_t)(sort_cores ? kPrepPositions : 4 * kPrepPositions) * p.M / (p.N > 0 ? p.N : 1);
-  pa.bags_per_block = (int)(want < 1 ? 1 : (want > kPrepMaxBags ? kPrepMaxBags : want));
-  pa.npass = p.plan.passes;
-  pa.histograms = !sort_cores;
-  for (int i = 0; i < kMaxPasses; ++i) {
-    pa.shift[i] = p.plan.shift[i];
-    pa.bits[i] = p.plan.bits[i];
-  }
   uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
-  pa.keys_out = p.T > 1 ? keys_built : nullptr;
-  pa.bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
-  pa.inv_len = reinterpret_cast<float*>(ws + L.inv_len);
-  pa.totals = reinterpret_cast<uint32_t*>(ws + L.totals);
-  pa.hdr = hdr;
-  pa.uniq_status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
-  pa.uniq_tiles = uniq_tiles;
-  pa.pass_status = reinterpret_cast<uint64_t*>(ws + L.pass_status);
-  pa.pass_status_words = sort_cores ? 0 : (int64_t)sort_tiles * status_stride;
-  const int prep_blocks = p.M > 0 ? (p.M + pa.bags_per_block - 1) / pa.bags_per_block : 1;
-  hipLaunchKernelGGL(k_prepare, dim3((unsigned)prep_blocks), dim3(kPrepThreads), 0, s, pa);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+
+  if (!sort_cores) {
+    PrepArgs pa{};
+    pa.offsets = p.offsets;
+    pa.idx = p.idx;
+    pa.ro = p.ro;
+    pa.B = p.B;
+    pa.M = p.M;
+    // about 4 * kPrepPositions positions per block: fewer global histogram atomics
+    const int64_t want = (int64_t)4 * kPrepPositions * p.M / N;
+    pa.bags_per_block = (int)(want < 1 ? 1 : (want > kPrepMaxBags ? kPrepMaxBags : want));
+    pa.npass = p.plan.passes;
+    pa.histograms = 1;
+    for (int i = 0; i < kMaxPasses; ++i) {
+      pa.shift[i] = p.plan.shift[i];
+      pa.bits[i] = p.plan.bits[i];
+    }
+    pa.keys_out = p.T > 1 ? keys_built : nullptr;
+    pa.bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
+    pa.totals = reinterpret_cast<uint32_t*>(ws + L.totals);
+    const int prep_blocks = p.M > 0 ? (p.M + pa.bags_per_block - 1) / pa.bags_per_block : 1;
+    hipLaunchKernelGGL(k_prepare, dim3((unsigned)prep_blocks), dim3(kPrepThreads), 0, s, pa);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
 
   const uint32_t* kin = p.T > 1 ? keys_built : reinterpret_cast<const uint32_t*>(p.idx);
   const int32_t* vin = nullptr;
@@ -713,10 +778,19 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.bags_out = last ? reinterpret_cast<int32_t*>(ws + L.sorted_bag) : ((ps % 2 == 0) ? bags_a : bags_b);
     xa.totals = reinterpret_cast<uint32_t*>(ws + L.totals) + ps * kMaxDigits;
     xa.prev_totals = ps > 0 ? reinterpret_cast<uint32_t*>(ws + L.totals) + (ps - 1) * kMaxDigits : nullptr;
-    xa.status = reinterpret_cast<uint64_t*>(ws + L.pass_status);
-    xa.rows = reinterpret_cast<uint64_t*>(ws + L.rows);
-    xa.grp = reinterpret_cast<uint64_t*>(ws + L.grp);
+    xa.status = reinterpret_cast<uint64_t*>(back + L.pass_status);
+    xa.rows = reinterpret_cast<uint64_t*>(back + L.rows);
+    xa.grp = reinterpret_cast<uint64_t*>(back + L.grp);
     xa.coresident = sort_cores;
+    xa.search_bags = sort_cores && ps == 0;
+    xa.offsets = p.offsets;
+    xa.idx = p.idx;
+    xa.ro = p.ro;
+    xa.B = p.B;
+    xa.M = p.M;
+    xa.T = p.T;
+    xa.uniq_status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
+    xa.uniq_tiles = uniq_tiles;
     xa.hdr = hdr;
     xa.N = N;
     xa.ntiles = sort_tiles;

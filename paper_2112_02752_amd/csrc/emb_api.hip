@@ -146,6 +146,7 @@ emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint
   p.N = batch->num_indices;
   p.plan = make_sort_plan(key_bits_for(R));
   p.ws = ws;
+  p.ws_bytes = ws_bytes;
   p.lay = lay;
   p.unique_keys = unique_keys;
   p.counts = counts;
@@ -189,6 +190,7 @@ emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int
   p.D = tables->dim;
   p.pool = pool;
   p.ws = ws;
+  p.ws_bytes = ws_bytes;
   p.lay = lay;
   p.grad_rows = grad_rows;
   p.fuse = fuse != nullptr;

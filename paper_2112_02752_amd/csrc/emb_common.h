@@ -30,6 +30,8 @@ constexpr int kUniqTile = kUniqThreads * kUniqItems;
 constexpr int kLookbackWindow = 8;
 // tiles per group of the two-level prefix used when all tiles are resident
 constexpr int kPrefixGroup = 16;
+// bag offsets a first-pass tile stages in LDS to find the bag of each position
+constexpr int kBagStage = 2048;
 
 // prepare kernel (keys, bag ids, digit histograms)
 constexpr int kPrepThreads = 256;
@@ -61,16 +63,27 @@ struct WsHeader {
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 
+// Workspace layout.  The front holds the batch's data arrays; the back (the
+// last bytes of the caller's workspace, wherever it ends) holds the
+// tag-checked coordination words of the sort.  Data of a call never lands on
+// bytes another call used for coordination words: a smaller batch has a
+// smaller front and its back lies inside the back of a larger one, so stale
+// words in the back are always coordination words of another call, whose
+// tags differ.
 struct WsLayout {
-  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_bag, inv_len,
-      pass_status, rows,
-      grp, uniq_status, chunk_seg, partials, total;
+  // front (offsets from the workspace base)
+  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_bag, uniq_status,
+      chunk_seg, partials, front;
+  // back (offsets from the back base)
+  size_t pass_status, rows, grp, back;
+  size_t total;
   int64_t sort_tiles, uniq_tiles, chunks, groups;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
+  (void)M;
   WsLayout L{};
   int64_t n = N > 0 ? N : 1;
   L.sort_tiles = (n + kSortTile - 1) / kSortTile;
@@ -82,40 +95,47 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   off += sizeof(WsHeader);
   L.totals = off;
   off = align256(off + sizeof(uint32_t) * kMaxPasses * kMaxDigits);
+  const size_t n4 = sizeof(uint32_t) * (size_t)n;
   L.keys_built = off;
-  off = align256(off + sizeof(uint32_t) * n);
+  off = align256(off + n4);
   L.keys_a = off;
-  off = align256(off + sizeof(uint32_t) * n);
+  off = align256(off + n4);
   L.keys_b = off;
-  off = align256(off + sizeof(uint32_t) * n);
+  off = align256(off + n4);
   L.vals_a = off;
-  off = align256(off + sizeof(int32_t) * n);
+  off = align256(off + n4);
   L.vals_b = off;
-  off = align256(off + sizeof(int32_t) * n);
+  off = align256(off + n4);
   L.bags_a = off;
-  off = align256(off + sizeof(int32_t) * n);
+  off = align256(off + n4);
   L.bags_b = off;
-  off = align256(off + sizeof(int32_t) * n);
+  off = align256(off + n4);
   L.bag_of = off;
-  off = align256(off + sizeof(int32_t) * n);
+  off = align256(off + n4);
   L.sorted_bag = off;
-  off = align256(off + sizeof(int32_t) * n);
-  L.inv_len = off;
-  off = align256(off + sizeof(float) * (M > 0 ? M : 1));
-  L.pass_status = off;
-  off = align256(off + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
-  L.rows = off;
-  off = align256(off + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
-  L.grp = off;
-  off = align256(off + sizeof(uint64_t) * L.groups * kMaxDigits);
+  off = align256(off + n4);
   L.uniq_status = off;
   off = align256(off + sizeof(uint64_t) * L.uniq_tiles);
   L.chunk_seg = off;
   off = align256(off + sizeof(int32_t) * (L.chunks + 1));
   L.partials = off;
   off = align256(off + sizeof(float) * (size_t)L.chunks * 2 * (size_t)(D > 0 ? D : 1));
-  L.total = off;
+  L.front = off;
+  size_t b = 0;
+  L.pass_status = b;
+  b = align256(b + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
+  L.rows = b;
+  b = align256(b + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
+  L.grp = b;
+  b = align256(b + sizeof(uint64_t) * L.groups * kMaxDigits);
+  L.back = b;
+  L.total = L.front + L.back;
   return L;
+}
+
+// base of the back region of a workspace of ws_bytes bytes (256-aligned)
+inline char* ws_back(void* ws, size_t ws_bytes, const WsLayout& L) {
+  return static_cast<char*>(ws) + ((ws_bytes - L.back) & ~(size_t)255);
 }
 
 // Global row offsets of the stacked tables, passed by value in kernel

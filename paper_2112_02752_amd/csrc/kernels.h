@@ -33,6 +33,7 @@ struct DedupLaunch {
   int64_t N;
   SortPlan plan;
   void* ws;
+  size_t ws_bytes;
   WsLayout lay;
   uint32_t* unique_keys;
   int32_t* counts;
@@ -51,6 +52,7 @@ struct ReduceLaunch {
   const int32_t* offsets;
   int32_t N, M, D, pool;
   void* ws;
+  size_t ws_bytes;
   WsLayout lay;
   float* grad_rows;  // may be null
   // fused optimizer (fuse = 0: reduce only)

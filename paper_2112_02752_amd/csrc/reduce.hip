@@ -34,7 +34,7 @@ struct RArgs {
   const uint32_t* ukeys;
   const int32_t* num_unique;
   const int32_t* sorted_bag;  // bag of every sorted position
-  const float* inv_len;       // 1 / bag length (mean pooling)
+  const int32_t* offsets;     // bag offsets (mean pooling scales by 1 / bag length)
   const int32_t* chunk_seg;
   float* grad_rows;
   float* partials;
@@ -168,6 +168,11 @@ __device__ __forceinline__ void finalize(const Upd& up, float* grad_rows, int64_
   apply_row<TW, G, NV>(up, grad_rows, u, r, acc, pre, sub);
 }
 
+// 1 / bag length for mean pooling (a position's bag is never empty), else 1
+__device__ __forceinline__ float bag_scale(const RArgs& a, int bag) {
+  return a.pool == EMB_POOL_MEAN ? 1.0f / (float)(a.offsets[bag + 1] - a.offsets[bag]) : 1.0f;
+}
+
 // Metadata of one heavy-segment check: the pieces of heavy segments that
 // lie in chunk c.  Slot 0: the segment holding the chunk's first position
 // (if heavy); slot 1: a different heavy segment holding its last position.
@@ -219,7 +224,7 @@ __device__ __forceinline__ void wave_piece_sum(const RArgs& a, int lo, int hi, i
   float msc = 0.f;
   if (lane < n) {
     mbag = a.sorted_bag[lo + lane];
-    msc = a.pool == EMB_POOL_MEAN ? a.inv_len[mbag] : 1.0f;
+    msc = bag_scale(a, mbag);
   }
   zero<G, NV>(acc);
   for (int i0 = 0; i0 < n; i0 += RPI * UN) {
@@ -301,7 +306,7 @@ __device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, in
       msc[j] = 0.f;
       if (i0 + sub < c[j]) {
         mb[j] = a.sorted_bag[s[j] + i0 + sub];
-        msc[j] = a.pool == EMB_POOL_MEAN ? a.inv_len[mb[j]] : 1.0f;
+        msc[j] = bag_scale(a, mb[j]);
       }
     }
     const int n = min(G, cmax - i0);
@@ -534,7 +539,7 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.ukeys = p.ukeys;
   ra.num_unique = p.num_unique;
   ra.sorted_bag = reinterpret_cast<const int32_t*>(ws + p.lay.sorted_bag);
-  ra.inv_len = reinterpret_cast<const float*>(ws + p.lay.inv_len);
+  ra.offsets = p.offsets;
   ra.chunk_seg = reinterpret_cast<const int32_t*>(ws + p.lay.chunk_seg);
   ra.grad_rows = p.grad_rows;
   ra.partials = reinterpret_cast<float*>(ws + p.lay.partials);

@@ -6,8 +6,8 @@ Adagrad / SGD update.  Inputs (tables, optimizer state, all batches and
 upstream gradients) are resident in HBM before the timed region starts.
 
 Prints ONE JSON line.  `value` is pooled lookups per second of whole steps;
-`roofline` prices the dominant kernel (the pooled forward) against HBM
-bandwidth; `cpu_baseline` is the CPU oracle timed on this host's cores on a
+`roofline` prices the phase that takes the most time (measured live with HIP
+events on the launch stream) against HBM bandwidth, `phases` lists all three; `cpu_baseline` is the CPU oracle timed on this host's cores on a
 bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -27,8 +27,11 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "pooled lookups/sec (fwd+bwd+update) and achieved HBM GB/s vs peak, 1 GPU"
-COUNTERS = os.path.join(ROOT, "profiles", "pool_fwd_c3_counters.txt")
-FWD_SOURCE = os.path.join(ROOT, "paper_2112_02752_amd", "csrc", "pool_fwd.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "c3_step_hbm_counters.txt")
+_CSRC = os.path.join(ROOT, "paper_2112_02752_amd", "csrc")
+PHASE_SOURCES = {"fwd": [os.path.join(_CSRC, "pool_fwd.hip")],
+                 "dedup": [os.path.join(_CSRC, "dedup.hip"), os.path.join(_CSRC, "emb_common.h")],
+                 "bwd_update": [os.path.join(_CSRC, "reduce.hip"), os.path.join(_CSRC, "emb_common.h")]}
 
 
 def parse():
@@ -74,9 +77,9 @@ def file_sha(path):
 
 
 def counter_traffic():
-    """HBM bytes per forward launch from the committed rocprofv3 counter
-    summary, scaled by the copy-kernel calibration; None if the kernel source
-    changed since the counters were taken."""
+    """HBM bytes per step of each phase from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled by the copy-kernel calibration);
+    None for a phase whose kernel sources changed since the counters were taken."""
     if not os.path.exists(COUNTERS):
         return None
     kv = {}
@@ -84,12 +87,14 @@ def counter_traffic():
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    try:
-        if kv.get("source_sha") != file_sha(FWD_SOURCE):
-            return None
-        return float(kv["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    out = {}
+    for phase, src in PHASE_SOURCES.items():
+        try:
+            ok = all(kv.get(f"sha_{os.path.basename(f)}") == file_sha(f) for f in src)
+            out[phase] = float(kv[f"hbm_bytes_{phase}"]) if ok else None
+        except (KeyError, ValueError):
+            out[phase] = None
+    return out
 
 
 def copy_calibration():
@@ -104,11 +109,15 @@ def copy_calibration():
 
 
 def cpu_baseline(w, batches, budget_s: float):
-    """The oracle, untuned, single-threaded, on whole steps of the same workload."""
+    """The oracle, untuned, single-threaded, on whole steps of the same workload:
+    the benchmark's batches, then further seeded batches of the same workload
+    until about `budget_s` seconds of oracle time."""
     import oracle
     import synth
     done_n, elapsed, steps = 0, 0.0, 0
-    for b in batches:
+    s = 0
+    while elapsed < budget_s and s < 400:
+        b = batches[s] if s < len(batches) else synth.make_batch(w, s)
         keys = np.unique(global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices))
         store = oracle.RowStore(synth.weight_rows(w, keys), keys=keys,
                                 state=np.zeros(len(keys), np.float32) if w.opt == "adagrad" else None)
@@ -118,11 +127,11 @@ def cpu_baseline(w, batches, budget_s: float):
         elapsed += time.perf_counter() - t0
         done_n += len(b.indices)
         steps += 1
-        if elapsed >= budget_s:
-            break
+        s += 1
     return {"value": done_n / elapsed, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} whole steps of {w.name} (fwd+dedup+reduce+update), {done_n} lookups, "
-                      f"{elapsed:.1f} s, single thread"}
+            "sample": f"{steps} whole steps of {w.name} (fwd+dedup+reduce+update; rows the batch touches "
+                      f"regenerated from the seed, untimed), {done_n} lookups, {elapsed:.1f} s of oracle time, "
+                      f"single thread"}
 
 
 def main():
@@ -229,9 +238,20 @@ def main():
     U_avg = float(np.mean(us))
     models = byte_models(w, N_avg, U_avg)
     t_phase = {k: float(np.mean(v)) for k, v in ph.items()}
-    fwd_log, fwd_comp = models["fwd"]
-    achieved = fwd_log / t_phase["fwd"] / 1e9
     traffic = counter_traffic()
+    phases = {}
+    for name, kern in (("fwd", "k_pool_fwd (emb_pool_fwd)"),
+                       ("dedup", "k_sort_pass x passes + k_unique (emb_unique_ids)"),
+                       ("bwd_update", "k_reduce_main + k_reduce_combine (emb_grad_reduce, fused update)")):
+        log_b, comp_b = models[name]
+        t = t_phase[name]
+        phases[name] = {"kernels": kern, "avg_us": t * 1e6, "logical_bytes": log_b, "compulsory_bytes": comp_b,
+                        "logical_frac": log_b / t / 1e9 / HBM_PEAK_GBS,
+                        "compulsory_frac": comp_b / t / 1e9 / HBM_PEAK_GBS,
+                        "hbm_traffic_bytes": traffic.get(name) if traffic else None}
+    dom = max(phases, key=lambda k: phases[k]["avg_us"])
+    d = phases[dom]
+    achieved = d["logical_bytes"] / (d["avg_us"] * 1e-6) / 1e9
     step_log = sum(v[0] for v in models.values())
     step_comp = sum(v[1] for v in models.values())
     ms = elapsed / args.steps * 1e3
@@ -242,19 +262,17 @@ def main():
         "data": "synthetic (seeded Zipf ids, N(0,1) upstream gradients, U(-0.01,0.01) tables)",
         "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
-                   "table_bytes": w.weight_bytes},
-        "roofline": {"bound": "hbm", "kernel": "k_pool_fwd (emb_pool_fwd)", "model": "logical",
+                   "table_bytes": w.weight_bytes, "schedule": args.schedule},
+        "roofline": {"bound": "hbm", "phase": dom, "kernel": d["kernels"], "model": "logical",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "bytes_per_launch": fwd_log,
-                     "compulsory_bytes_per_launch": fwd_comp,
-                     "compulsory_frac": fwd_comp / t_phase["fwd"] / 1e9 / HBM_PEAK_GBS,
-                     "avg_launch_us": t_phase["fwd"] * 1e6},
+                     "traffic": d["hbm_traffic_bytes"], "bytes_per_launch": d["logical_bytes"],
+                     "avg_launch_us": d["avg_us"]},
+        "phases": phases,
         "step_bytes": {"logical": step_log, "compulsory": step_comp,
                        "logical_GBs": step_log / (ms * 1e-3) / 1e9,
-                       "compulsory_GBs": step_comp / (ms * 1e-3) / 1e9},
-        "phase_us": {k: v * 1e6 for k, v in t_phase.items()},
-        "gpu_us_per_step": gpu_step_s * 1e6,
-        "schedule": args.schedule,
+                       "compulsory_GBs": step_comp / (ms * 1e-3) / 1e9,
+                       "logical_frac": step_log / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        "gpu_us_per_step_serial": gpu_step_s * 1e6,
         "serial_ms_per_step": serial_elapsed / args.steps * 1e3,
     }
     if not args.no_cpu_baseline:

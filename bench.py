@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--schedule", choices=("pipelined", "serial"), default="pipelined",
                     help="pipelined: the id dedup of batch k+1 runs on a second stream alongside the forward and "
                          "update of batch k (same results as serial)")
+    ap.add_argument("--lookahead", type=int, default=2, help="batches whose dedup may run ahead (pipelined)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -210,11 +211,12 @@ def main():
     gpu_step_s = float(np.mean([e[0].elapsed_time(e[3]) * 1e-3 for e in evs]))
 
     if args.schedule == "pipelined":
-        pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags)
+        pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
+                            lookahead=args.lookahead)
 
         def pstep(i):
-            nxt = dev_batches[i + 1][0] if i + 1 < total else None
-            pipe.step(dev_batches[i][0], out, dev_batches[i][1], next_batch=nxt)
+            pipe.step(dev_batches[i][0], out, dev_batches[i][1],
+                      upcoming=[b for b, _, _ in dev_batches[i + 1:i + 1 + args.lookahead]])
 
         for i in range(args.warmup):
             pstep(i)
@@ -262,7 +264,8 @@ def main():
         "data": "synthetic (seeded Zipf ids, N(0,1) upstream gradients, U(-0.01,0.01) tables)",
         "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
-                   "table_bytes": w.weight_bytes, "schedule": args.schedule},
+                   "table_bytes": w.weight_bytes, "schedule": args.schedule,
+                   "lookahead": args.lookahead if args.schedule == "pipelined" else 0},
         "roofline": {"bound": "hbm", "phase": dom, "kernel": d["kernels"], "model": "logical",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": d["hbm_traffic_bytes"], "bytes_per_launch": d["logical_bytes"],

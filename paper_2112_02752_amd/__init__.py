@@ -258,59 +258,131 @@ class DedupBuffers:
         self.num_unique = torch.zeros(1, **i32)
 
 
+class _Hip:
+    """Direct HIP runtime calls for stream ordering (events), with cached
+    handles: cheaper per call than the framework's wrappers."""
+    _L = None
+
+    @classmethod
+    def lib(cls):
+        if cls._L is None:
+            L = ctypes.CDLL("libamdhip64.so")
+            vp = ctypes.c_void_p
+            L.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+            L.hipEventCreateWithFlags.restype = ctypes.c_int
+            L.hipEventDestroy.argtypes = [vp]
+            L.hipEventDestroy.restype = ctypes.c_int
+            L.hipEventRecord.argtypes = [vp, vp]
+            L.hipEventRecord.restype = ctypes.c_int
+            L.hipStreamWaitEvent.argtypes = [vp, vp, ctypes.c_uint]
+            L.hipStreamWaitEvent.restype = ctypes.c_int
+            cls._L = L
+        return cls._L
+
+    @classmethod
+    def event(cls) -> int:
+        ev = ctypes.c_void_p()
+        rc = cls.lib().hipEventCreateWithFlags(ctypes.byref(ev), 0x2)  # hipEventDisableTiming
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags: {rc}")
+        return ev.value
+
+    @classmethod
+    def record(cls, ev: int, stream: int) -> None:
+        rc = cls.lib().hipEventRecord(ev, stream)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord: {rc}")
+
+    @classmethod
+    def wait(cls, stream: int, ev: int) -> None:
+        rc = cls.lib().hipStreamWaitEvent(stream, ev, 0)
+        if rc != 0:
+            raise RuntimeError(f"hipStreamWaitEvent: {rc}")
+
+
 class Pipeline:
-    """Training steps of the layer with the id dedup of the next batch
+    """Training steps of the layer with the id dedup of later batches
     overlapped with the forward and update of the current one.
 
     The dedup of a batch reads only its ids, never the table, so it can run
-    ahead on a second stream; the forward of batch k+1 still runs after the
-    update of batch k on the main stream, so every step sees exactly the
-    weights a serial execution would.  Two dedup buffer sets alternate; a set
-    is reused only after the update that read it has completed (events)."""
+    ahead: the dedups of the next `lookahead` batches run on their own side
+    streams while the main stream runs forward k then the update of k, so the
+    forward of batch k+1 still follows the update of batch k and every step
+    sees exactly the weights a serial execution would.  lookahead + 2 dedup
+    buffer sets rotate; a set is reused only after the update that read it has
+    completed (events)."""
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0):
+                 max_indices: int = 0, max_bags: int = 0, lookahead: int = 2):
         import torch
+        if lookahead < 1:
+            raise ValueError("lookahead must be >= 1")
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
         dev = tables.weights.device
         D = int(tables.weights.shape[1])
-        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(2)]
-        self.main = torch.cuda.current_stream(dev)
-        self.side = torch.cuda.Stream(device=dev)
-        self.dedup_done = [torch.cuda.Event(), torch.cuda.Event()]
-        self.update_done = [torch.cuda.Event(), torch.cuda.Event()]
+        self.L = lookahead
+        # one set more than in flight: the update a dedup waits for was enqueued
+        # a whole step earlier, which keeps the host-side cost of the
+        # cross-stream wait small
+        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(lookahead + 2)]
+        self._main = torch.cuda.current_stream(dev)
+        self._sides = [torch.cuda.Stream(device=dev) for _ in range(lookahead)]
+        self.main = int(self._main.cuda_stream)
+        self.sides = [int(x.cuda_stream) for x in self._sides]
+        self.dedup_done = [_Hip.event() for _ in self.sets]
+        self.update_done = [_Hip.event() for _ in self.sets]
         for e in self.update_done:
-            e.record(self.main)
+            _Hip.record(e, self.main)
         self.max_indices = max(1, max_indices)
-        self._pending = None  # (batch, set index) whose dedup is enqueued
+        self.k = 0               # index of the next step
+        self.enqueued = {}       # step index -> batch whose dedup is enqueued
+        # argument values that stay fixed across steps, marshalled once
+        self._ct = ctypes.byref(tables.c())
+        self._upd = _update(opt, lr, eps, state)
+        self._pool = POOL[pool]
+        self._set_args = [(_ptr(b.unique_keys), _ptr(b.counts), _ptr(b.seg_offsets), _ptr(b.sort_perm),
+                           _ptr(b.num_unique), _ptr(b.ws), b.ws.numel() * b.ws.element_size()) for b in self.sets]
 
-    def _dedup(self, batch: Batch, k: int) -> None:
-        import torch
+    def __del__(self):
+        try:
+            L = _Hip.lib()
+            for e in self.dedup_done + self.update_done:
+                L.hipEventDestroy(e)
+        except Exception:
+            pass
+
+    def _dedup(self, j: int, batch: Batch) -> None:
         if int(batch.indices.numel()) > self.max_indices:
             raise ValueError("batch larger than the pipeline's buffers")
-        b = self.sets[k]
-        self.side.wait_event(self.update_done[k])
-        with torch.cuda.stream(self.side):
-            unique_ids(self.tables, batch, b.unique_keys, b.counts, b.seg_offsets, b.sort_perm, b.num_unique, b.ws,
-                       int(self.side.cuda_stream))
-        self.dedup_done[k].record(self.side)
+        si = j % len(self.sets)
+        uk, cnt, seg, perm, nu, ws, wsb = self._set_args[si]
+        side = self.sides[j % self.L]
+        _Hip.wait(side, self.update_done[si])
+        _check("emb_unique_ids", lib().emb_unique_ids(self._ct, ctypes.byref(batch.c()), uk, cnt, seg, perm, nu, ws,
+                                                      wsb, side))
+        _Hip.record(self.dedup_done[si], side)
+        self.enqueued[j] = batch
 
-    def step(self, batch: Batch, out, grad_out, next_batch: Optional[Batch] = None, grad_rows=None) -> None:
-        """Forward of `batch` into `out`, then its backward with `grad_out`;
-        the dedup of `next_batch` (if given) is started alongside."""
-        if self._pending is None or self._pending[0] is not batch:
-            k = 0 if self._pending is None else 1 - self._pending[1]
-            self._dedup(batch, k)
-            self._pending = (batch, k)
-        k = self._pending[1]
-        if next_batch is not None:
-            self._dedup(next_batch, 1 - k)
-        sm = int(self.main.cuda_stream)
-        pool_fwd(self.tables, batch, self.pool, out, sm)
-        self.main.wait_event(self.dedup_done[k])
-        b = self.sets[k]
-        grad_reduce(self.tables, batch, self.pool, grad_out, b.sort_perm, b.seg_offsets, b.unique_keys,
-                    b.num_unique, b.ws, grad_rows=grad_rows, opt=self.opt, lr=self.lr, eps=self.eps,
-                    state=self.state, stream=sm)
-        self.update_done[k].record(self.main)
-        self._pending = (next_batch, 1 - k) if next_batch is not None else None
+    def step(self, batch: Batch, out, grad_out, upcoming=(), grad_rows=None) -> None:
+        """Forward of `batch` into `out`, then its backward with `grad_out`.
+        `upcoming`: the next batches in order (up to `lookahead` are used),
+        whose dedups are started now."""
+        k = self.k
+        if self.enqueued.get(k) is not batch:
+            self._dedup(k, batch)
+        for i, nb in enumerate(upcoming):
+            if i >= self.L:
+                break
+            if k + 1 + i not in self.enqueued:
+                self._dedup(k + 1 + i, nb)
+        si = k % len(self.sets)
+        L = lib()
+        cb = ctypes.byref(batch.c())
+        _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, self._pool, _ptr(out), self.main))
+        _Hip.wait(self.main, self.dedup_done[si])
+        uk, cnt, seg, perm, nu, ws, wsb = self._set_args[si]
+        _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, self._pool, _ptr(grad_out), perm, seg, uk, nu,
+                                                    _ptr(grad_rows), ctypes.byref(self._upd), ws, wsb, self.main))
+        _Hip.record(self.update_done[si], self.main)
+        del self.enqueued[k]
+        self.k = k + 1

@@ -388,7 +388,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   constexpr int NWv = kCombineThreads / kWave;
   constexpr int NG = NWv * RPI;
   __shared__ float s_red[NWv][G * NV * 4];
-  __shared__ int s_list[kCombineChunks];
+  __shared__ int4 s_list[kCombineChunks];  // (chunk, segment, first position, end)
   __shared__ int s_n;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G, w = tid >> 6;
   const int U = *a.num_unique;
@@ -400,17 +400,18 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
     const ChunkPieces cp = chunk_pieces(a, c, U);
     // a heavy segment starts in chunk c when the chunk's last segment is
     // heavy and begins inside the chunk
-    if (cp.e1 - cp.s1 > kChunk && cp.s1 >= c * kChunk) s_list[atomicAdd(&s_n, 1)] = c;
+    if (cp.e1 - cp.s1 > kChunk && cp.s1 >= c * kChunk) s_list[atomicAdd(&s_n, 1)] = make_int4(c, cp.u1, cp.s1, cp.e1);
   }
   __syncthreads();
   const int n = s_n;
   for (int it = 0; it < n; ++it) {
-    const int c = s_list[it];
-    const int p0 = c * kChunk, p1 = min(a.N, p0 + kChunk);
-    const int cs1 = a.chunk_seg[c + 1];
-    const int u1 = (a.seg[cs1] == p1) ? cs1 - 1 : cs1;
-    const int s1 = a.seg[u1], e1 = a.seg[u1 + 1];
+    const int4 item = s_list[it];
+    const int c = item.x, u1 = item.y, s1 = item.z, e1 = item.w;
+    const int p0 = c * kChunk;
     const int np = (e1 - 1) / kChunk - c + 1;
+    const uint32_t key = a.ukeys[u1];
+    RowPre<NV> pre;
+    if (w == 0 && g == 0) prefetch_row<TW, G, NV>(a.up, key, sub, pre);
     float acc[NV][4];
     zero<G, NV>(acc);
     for (int i0 = w * RPI + g; i0 < np; i0 += NG * 4) {
@@ -446,7 +447,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
           for (int ww = 1; ww < NWv; ++ww) t += s_red[ww][(v * G + sub) * 4 + e];
           acc[v][e] = t;
         }
-      finalize<TW, G, NV>(a.up, a.grad_rows, u1, a.ukeys[u1], acc, sub);
+      apply_row<TW, G, NV>(a.up, a.grad_rows, u1, key, acc, pre, sub);
     }
     __syncthreads();
   }

@@ -286,14 +286,15 @@ def test_c2_unfused_path():
     parity.run_workload(w, steps=1, fused=False)
 
 
-def test_pipelined_schedule_equals_serial():
+@pytest.mark.parametrize("lookahead", [1, 2, 3])
+def test_pipelined_schedule_equals_serial(lookahead):
     """Dedup of batch k+1 overlapped with batch k (second stream) changes
     nothing: tables, state and pooled outputs match serial steps bitwise."""
-    _say("case pipelined vs serial")
+    _say(f"case pipelined vs serial lookahead={lookahead}")
     import torch
     import paper_2112_02752_amd as emb
     w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
-    batches = [synth.make_batch(w, s) for s in range(5)]
+    batches = [synth.make_batch(w, s) for s in range(6)]
     nmax = max(len(b.indices) for b in batches)
     dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
               torch.from_numpy(b.grad).cuda()) for b in batches]
@@ -309,10 +310,10 @@ def test_pipelined_schedule_equals_serial():
                 outs.append(out)
         else:
             pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
-                                max_bags=w.num_bags)
+                                max_bags=w.num_bags, lookahead=lookahead)
             for i, (b, g) in enumerate(dev_b):
                 out = torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda")
-                pipe.step(b, out, g, next_batch=dev_b[i + 1][0] if i + 1 < len(dev_b) else None)
+                pipe.step(b, out, g, upcoming=[x for x, _ in dev_b[i + 1:i + 1 + lookahead]])
                 outs.append(out)
         torch.cuda.synchronize()
         results.append((dl.W.cpu().numpy(), dl.state.cpu().numpy(), [o.cpu().numpy() for o in outs]))

@@ -99,6 +99,38 @@ __device__ __forceinline__ void add_row(const float* src, float sc, int D, int s
   }
 }
 
+// acc[j] += sc[q][j] * src[idx[q][j]] (this lane's columns) for every (q, j)
+// with idx >= 0.  All loads are issued before the first is used, from
+// in-bounds addresses (index 0 and column 0 stand in for the unused ones),
+// and the unused values are dropped by a select, so no load waits for
+// another.
+template <int G, int NV, int Q, int S>
+__device__ __forceinline__ void add_rows(const float* src, const int (&idx)[Q][S], const float (&sc)[Q][S], int D,
+                                         int sub, float (&acc)[S][NV][4]) {
+  float x[Q][S][NV][4];
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const float* rp = src + (size_t)(idx[q][j] > 0 ? idx[q][j] : 0) * (size_t)D;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c0 = (v * G + sub) * 4;
+        Row4<float>::load(rp + (c0 < D ? c0 : 0), x[q][j][v]);
+      }
+    }
+#pragma unroll
+  for (int q = 0; q < Q; ++q)
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const bool ok = idx[q][j] >= 0 && (v * G + sub) * 4 < D;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[j][v][e] += ok ? sc[q][j] * x[q][j][v][e] : 0.f;
+      }
+}
+
 // The table row and optimizer state an update reads, loaded ahead of time.
 template <int NV>
 struct RowPre {
@@ -214,33 +246,46 @@ __device__ __forceinline__ ChunkPieces chunk_pieces(const RArgs& a, int c, int U
 // Sum of the scaled gradient rows of sorted positions [lo, hi) (at most 64)
 // by all groups of the wavefront, every row load issued up front; the groups
 // are reduced with a butterfly, the result is valid in every group.
+// Within a segment the positions of one bag are consecutive (positions
+// ascend and so do their bags), so each distinct bag's row is loaded once and
+// weighted by its multiplicity: the runs of equal bags are found with a
+// ballot and their heads packed to the low lanes with a lane permutation.
 template <int G, int NV>
 __device__ __forceinline__ void wave_piece_sum(const RArgs& a, int lo, int hi, int g, int sub, int lane,
                                                float (&acc)[NV][4]) {
   constexpr int RPI = kWave / G;
   constexpr int UN = 8;
   const int n = hi - lo;
-  int mbag = 0;
-  float msc = 0.f;
-  if (lane < n) {
-    mbag = a.sorted_bag[lo + lane];
-    msc = bag_scale(a, mbag);
-  }
-  zero<G, NV>(acc);
-  for (int i0 = 0; i0 < n; i0 += RPI * UN) {
-    int bag[UN];
-    float sc[UN];
+  const int mbag = lane < n ? a.sorted_bag[lo + lane] : -1;
+  const int up = __shfl_up(mbag, 1, kWave);
+  const bool head = lane < n && (lane == 0 || up != mbag);
+  const uint64_t H = __ballot(head);
+  const int nh = __popcll(H);
+  const uint64_t above = lane == kWave - 1 ? 0ull : (H >> (lane + 1));
+  const int next = above ? lane + 1 + __builtin_ctzll(above) : n;
+  const float wgt = head ? (float)(next - lane) * bag_scale(a, mbag) : 0.f;
+  // heads go to lanes 0..nh-1 in order, the other lanes fill the rest
+  const int dst = head ? (int)lanes_below(H) : nh + (int)lanes_below(~H);
+  const int cbag = __builtin_amdgcn_ds_permute(dst << 2, mbag);
+  const float cw = __int_as_float(__builtin_amdgcn_ds_permute(dst << 2, __float_as_int(wgt)));
+  float acc1[1][NV][4];
+  zero<G, NV>(acc1[0]);
+  for (int i0 = 0; i0 < nh; i0 += RPI * UN) {
+    int bag[UN][1];
+    float sc[UN][1];
 #pragma unroll
     for (int q = 0; q < UN; ++q) {
       const int k = i0 + q * RPI + g;
-      bag[q] = __shfl(mbag, k & (kWave - 1), kWave);
-      sc[q] = __shfl(msc, k & (kWave - 1), kWave);
-      if (k >= n) bag[q] = -1;
+      bag[q][0] = __shfl(cbag, k & (kWave - 1), kWave);
+      sc[q][0] = __shfl(cw, k & (kWave - 1), kWave);
+      if (k >= nh) bag[q][0] = -1;
     }
-#pragma unroll
-    for (int q = 0; q < UN; ++q)
-      if (bag[q] >= 0) add_row<G, NV>(a.G + (size_t)bag[q] * a.D, sc[q], a.D, sub, acc);
+    add_rows<G, NV, UN, 1>(a.G, bag, sc, a.D, sub, acc1);
   }
+#pragma unroll
+  for (int v = 0; v < NV; ++v)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[v][e] = acc1[0][v][e];
 #pragma unroll
   for (int o = G; o < kWave; o <<= 1)
 #pragma unroll
@@ -258,10 +303,12 @@ __device__ __forceinline__ void store_row(float* dst, int D, int sub, const floa
   }
 }
 
+// positions of every light slot whose rows are loaded together
+constexpr int kLightRound = 2;
 // slots per lane group: one lane of the wavefront reads each segment's offsets
 constexpr int slots_for(int rpi) { return rpi * kSlots <= kWave ? kSlots : kWave / rpi; }
-// register budget of the main kernel: 7 waves per SIMD for rows of up to 256 floats
-constexpr int reduce_waves(int nv) { return nv == 1 ? 7 : 4; }
+// register budget of the main kernel: 5 waves per SIMD for rows of up to 256 floats (no spills)
+constexpr int reduce_waves(int nv) { return nv == 1 ? 5 : 4; }
 
 // Light segments, kSlots per lane group: the segments of a batch are
 // consecutive; their offsets and keys are read by one lane each, the bags of
@@ -310,12 +357,12 @@ __device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, in
       }
     }
     const int n = min(G, cmax - i0);
-    for (int i = 0; i < n; i += 2) {
-      // two positions of every slot per round: their loads are issued together
-      int bag[2][S];
-      float sc[2][S];
+    for (int i = 0; i < n; i += kLightRound) {
+      // kLightRound positions of every slot per round, their loads issued together
+      int bag[kLightRound][S];
+      float sc[kLightRound][S];
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int q = 0; q < kLightRound; ++q)
 #pragma unroll
         for (int j = 0; j < S; ++j) {
           const int src = g * G + ((i + q) & (G - 1));
@@ -323,11 +370,7 @@ __device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, in
           sc[q][j] = __shfl(msc[j], src, kWave);
           if (i + q >= n || i0 + i + q >= c[j]) bag[q][j] = -1;
         }
-#pragma unroll
-      for (int q = 0; q < 2; ++q)
-#pragma unroll
-        for (int j = 0; j < S; ++j)
-          if (bag[q][j] >= 0) add_row<G, NV>(a.G + (size_t)bag[q][j] * a.D, sc[q][j], a.D, sub, acc[j]);
+      add_rows<G, NV, kLightRound, S>(a.G, bag, sc, a.D, sub, acc);
     }
   }
 #pragma unroll
@@ -382,6 +425,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
 // lane per chunk) the heavy segments whose first position lies in its
 // range, then sums each one's partials in chunk order with all its lane
 // groups and applies the optimizer.
+constexpr int kCombineUnroll = 8;  // partial rows of a lane group loaded together
+
 template <typename TW, int G, int NV>
 __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   constexpr int RPI = kWave / G;
@@ -414,16 +459,24 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
     if (w == 0 && g == 0) prefetch_row<TW, G, NV>(a.up, key, sub, pre);
     float acc[NV][4];
     zero<G, NV>(acc);
-    for (int i0 = w * RPI + g; i0 < np; i0 += NG * 4) {
+    float acc1[1][NV][4];
+    zero<G, NV>(acc1[0]);
+    for (int i0 = w * RPI + g; i0 < np; i0 += NG * kCombineUnroll) {
+      int pidx[kCombineUnroll][1];
+      float one[kCombineUnroll][1];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < kCombineUnroll; ++q) {
         const int i = i0 + q * NG;
-        if (i < np) {
-          const int slot = (i == 0 && s1 != p0) ? 1 : 0;
-          add_row<G, NV>(a.partials + ((size_t)(c + i) * 2 + slot) * a.D, 1.0f, a.D, sub, acc);
-        }
+        const int slot = (i == 0 && s1 != p0) ? 1 : 0;
+        pidx[q][0] = i < np ? (c + i) * 2 + slot : -1;
+        one[q][0] = 1.0f;
       }
+      add_rows<G, NV, kCombineUnroll, 1>(a.partials, pidx, one, a.D, sub, acc1);
     }
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[v][e] = acc1[0][v][e];
 #pragma unroll
     for (int o = G; o < kWave; o <<= 1)
 #pragma unroll

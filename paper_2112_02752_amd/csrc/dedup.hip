@@ -247,10 +247,14 @@ __device__ __forceinline__ uint32_t sum_column(const uint64_t* m, int stride, in
 // Bag of each of this thread's positions of a tile: the bag holding position
 // j is the last m with offsets[m] <= j.  One offset in every S (S chosen so
 // the samples fit one per thread) narrows the tile's bags to a few sample
-// intervals; their offsets are staged in LDS and searched per position.
-// Intervals that do not fit the stage are searched in global memory.
+// intervals whose offsets are staged in LDS.  Every nonempty staged bag that
+// overlaps the tile writes its id at its first position in the tile, and an
+// inclusive max-scan over the tile's positions carries each id forward to
+// the bag's other positions (bag ids grow with position).  Intervals that do
+// not fit the stage are searched in global memory.  `s_work` holds
+// kSortTile ints.
 __device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int32_t* s_boff, int* s_lohi,
-                                               int32_t (&bag)[kSortItems]) {
+                                               int32_t* s_work, uint32_t* s_wmax, int32_t (&bag)[kSortItems]) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
   const int64_t p0 = (int64_t)tile * kSortTile;
   const int64_t p1 = min(p0 + kSortTile, (int64_t)a.N);
@@ -271,21 +275,50 @@ __device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int3
   const int m_lo = (s_lohi[0] - 1) * S;                    // a bag at or before the tile's first bag
   const int m_hi = min((s_lohi[1] - 1) * S + S, a.M);      // an offset index at or after its last bag's end
   const int nst = m_hi - m_lo + 1;
-  const bool staged = nst <= kBagStage + 1;
-  if (staged)
+  if (nst <= kBagStage + 1) {
     for (int i = tid; i < nst; i += kSortThreads) s_boff[i] = a.offsets[m_lo + i];
-  __syncthreads();
-  (void)w;
+    // ids are stored plus one, so that 0 means "no bag starts here"
+    for (int i = tid; i < kSortTile; i += kSortThreads) s_work[i] = 0;
+    __syncthreads();
+    for (int i = tid; i < nst - 1; i += kSortThreads) {
+      const int64_t st = s_boff[i], en = s_boff[i + 1];
+      if (st < en && st < p1 && en > p0) s_work[(st > p0 ? st : p0) - p0] = m_lo + i + 1;
+    }
+    __syncthreads();
+    uint32_t v[kSortItems];
+    uint32_t run = 0;
+#pragma unroll
+    for (int k = 0; k < kSortItems; ++k) {
+      const uint32_t x = (uint32_t)s_work[tid * kSortItems + k];
+      run = x > run ? x : run;
+      v[k] = run;
+    }
+    const uint32_t incl = wave_incl_max(run);
+    if (lane == kWave - 1) s_wmax[w] = incl;
+    uint32_t carry = __shfl_up(incl, 1, kWave);
+    if (lane == 0) carry = 0;
+    __syncthreads();
+    for (int ww = 0; ww < w; ++ww) carry = s_wmax[ww] > carry ? s_wmax[ww] : carry;
+#pragma unroll
+    for (int k = 0; k < kSortItems; ++k) s_work[tid * kSortItems + k] = (int32_t)(v[k] > carry ? v[k] : carry);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+      const int64_t j = p0 + (int64_t)w * (kWave * kSortItems) + i * kWave + lane;
+      bag[i] = j < p1 ? s_work[j - p0] - 1 : 0;
+    }
+    __syncthreads();  // s_work is reused by the caller
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < kSortItems; ++i) {
-    const int64_t j = p0 + (int64_t)(threadIdx.x >> 6) * (kWave * kSortItems) + i * kWave + lane;
+    const int64_t j = p0 + (int64_t)w * (kWave * kSortItems) + i * kWave + lane;
     bag[i] = 0;
     if (j < p1) {
       int lo = 0, hi = nst - 2;  // last idx in [0, nst-2] with offset <= j
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        const int32_t v = staged ? s_boff[mid] : a.offsets[m_lo + mid];
-        if (v <= j) lo = mid; else hi = mid - 1;
+        if (a.offsets[m_lo + mid] <= j) lo = mid; else hi = mid - 1;
       }
       bag[i] = m_lo + lo;
     }
@@ -307,6 +340,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   __shared__ int s_tile;
   __shared__ int32_t s_boff[kBagStage + 1];
   __shared__ int s_lohi[2];
+  __shared__ uint32_t s_toff[EMB_MAX_TABLES];
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
   if (a.coresident) {
@@ -315,6 +349,8 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
     s_tile = (int)atomic_add_u32(&a.hdr->ticket[a.pass], 1u);
   }
   for (int i = tid; i < NW * ND; i += kSortThreads) (&s_cnt[0][0])[i] = 0u;
+  if (a.search_bags && a.T > 1)
+    for (int t = tid; t < a.T; t += kSortThreads) s_toff[t] = a.ro.off[t];
   // the previous pass is complete: clear its totals and ticket for the next call
   if (blockIdx.x == 0 && a.prev_totals) {
     for (int d = tid; d < kMaxDigits; d += kSortThreads) a.prev_totals[d] = 0u;
@@ -336,16 +372,19 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
     if (blockIdx.x == 0 && tid == 0) a.hdr->ticket[kSlotUnique] = 0u;
   }
   if (a.search_bags) {
-    find_tile_bags(a, tile, s_boff, s_lohi, bag);
+    find_tile_bags(a, tile, s_boff, s_lohi, s_bags, s_wsum, bag);
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {
       const int64_t pos = wbase + i * kWave + lane;
-      const bool valid = pos < a.N;
-      const uint32_t id = valid ? (uint32_t)a.idx[pos] : 0u;
-      key[i] = valid ? (a.T > 1 ? a.ro.off[bag[i] / a.B] + id : id) : 0u;
-      val[i] = valid ? (int32_t)pos : 0;
-      dig[i] = (key[i] >> a.shift) & mask;
+      key[i] = pos < a.N ? (uint32_t)a.idx[pos] : 0u;
+      val[i] = pos < a.N ? (int32_t)pos : 0;
     }
+    if (a.T > 1) {
+#pragma unroll
+      for (int i = 0; i < kSortItems; ++i) key[i] += s_toff[bag[i] / a.B];
+    }
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) dig[i] = (key[i] >> a.shift) & mask;
   } else {
 #pragma unroll
     for (int i = 0; i < kSortItems; ++i) {

@@ -45,9 +45,11 @@ constexpr int kChunk = 64;
 // segment (longer light ones are summed by a whole wavefront)
 constexpr int kSlots = 2;
 constexpr int kTinySeg = 16;
-// heavy-segment combine: threads per block, chunks a block checks
+// heavy-segment combine: threads per block, chunks a block covers (a
+// heavy segment that crosses blocks is finished by the last block to reach
+// it, from one row per block)
 constexpr int kCombineThreads = 1024;
-constexpr int kCombineChunks = 16;
+constexpr int kCombineChunks = 64;
 
 // ticket / done counter slots in the workspace header
 constexpr int kSlotUnique = kMaxPasses;
@@ -73,11 +75,11 @@ static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 struct WsLayout {
   // front (offsets from the workspace base)
   size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_bag, uniq_status,
-      chunk_seg, partials, front;
+      chunk_seg, partials, level2, arrivals, front;
   // back (offsets from the back base)
   size_t pass_status, rows, grp, back;
   size_t total;
-  int64_t sort_tiles, uniq_tiles, chunks, groups;
+  int64_t sort_tiles, uniq_tiles, chunks, groups, combine_blocks;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -120,6 +122,11 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   off = align256(off + sizeof(int32_t) * (L.chunks + 1));
   L.partials = off;
   off = align256(off + sizeof(float) * (size_t)L.chunks * 2 * (size_t)(D > 0 ? D : 1));
+  L.combine_blocks = (L.chunks + kCombineChunks - 1) / kCombineChunks;
+  L.level2 = off;
+  off = align256(off + sizeof(uint64_t) * (size_t)L.combine_blocks * 2 * (size_t)(D > 0 ? D : 1));
+  L.arrivals = off;
+  off = align256(off + sizeof(uint32_t) * (size_t)L.combine_blocks);
   L.front = off;
   size_t b = 0;
   L.pass_status = b;

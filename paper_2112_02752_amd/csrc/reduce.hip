@@ -38,6 +38,10 @@ struct RArgs {
   const int32_t* chunk_seg;
   float* grad_rows;
   float* partials;
+  uint64_t* level2;     // [ncomb][2][D] tagged rows, cleared by the main kernel
+  uint32_t* arrivals;   // [ncomb] arrival counters, cleared by the main kernel
+  int32_t ncomb;        // combine blocks
+  void* hdr;            // workspace header (error bits)
   int32_t N, D, pool, nchunks;
   Upd up;
 };
@@ -98,6 +102,9 @@ __device__ __forceinline__ void add_row(const float* src, float sc, int D, int s
     }
   }
 }
+
+// rows of up to 256 floats a lane group keeps in flight (fewer for wider rows)
+constexpr int rows_in_flight(int nv) { return nv >= 4 ? 2 : (nv == 2 ? 4 : 8); }
 
 // acc[j] += sc[q][j] * src[idx[q][j]] (this lane's columns) for every (q, j)
 // with idx >= 0.  All loads are issued before the first is used, from
@@ -210,6 +217,7 @@ __device__ __forceinline__ float bag_scale(const RArgs& a, int bag) {
 // (if heavy); slot 1: a different heavy segment holding its last position.
 struct ChunkPieces {
   int lo[2], hi[2];
+  int u0, s0, e0;  // the segment holding the chunk's first position
   int u1, s1, e1;  // the segment holding the chunk's last position
 };
 
@@ -231,6 +239,9 @@ __device__ __forceinline__ ChunkPieces chunk_pieces(const RArgs& a, int c, int U
     r.s1 = sc;
     r.e1 = scp;
   }
+  r.u0 = u0;
+  r.s0 = s0;
+  r.e0 = e0;
   r.lo[0] = r.hi[0] = r.lo[1] = r.hi[1] = 0;
   if (e0 - s0 > kChunk) {
     r.lo[0] = p0;
@@ -254,7 +265,7 @@ template <int G, int NV>
 __device__ __forceinline__ void wave_piece_sum(const RArgs& a, int lo, int hi, int g, int sub, int lane,
                                                float (&acc)[NV][4]) {
   constexpr int RPI = kWave / G;
-  constexpr int UN = 8;
+  constexpr int UN = rows_in_flight(NV);
   const int n = hi - lo;
   const int mbag = lane < n ? a.sorted_bag[lo + lane] : -1;
   const int up = __shfl_up(mbag, 1, kWave);
@@ -304,7 +315,7 @@ __device__ __forceinline__ void store_row(float* dst, int D, int sub, const floa
 }
 
 // positions of every light slot whose rows are loaded together
-constexpr int kLightRound = 2;
+constexpr int light_round(int nv) { return nv >= 4 ? 1 : 2; }
 // slots per lane group: one lane of the wavefront reads each segment's offsets
 constexpr int slots_for(int rpi) { return rpi * kSlots <= kWave ? kSlots : kWave / rpi; }
 // register budget of the main kernel: 5 waves per SIMD for rows of up to 256 floats (no spills)
@@ -318,6 +329,7 @@ template <typename TW, int G, int NV>
 __device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, int g, int sub, int lane) {
   constexpr int RPI = kWave / G;
   constexpr int S = slots_for(RPI);
+  constexpr int LR = light_round(NV);
   int ms = 0, me = 0;
   uint32_t mk = 0;
   if (lane < RPI * S && ubase + lane < U) {
@@ -357,12 +369,12 @@ __device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, in
       }
     }
     const int n = min(G, cmax - i0);
-    for (int i = 0; i < n; i += kLightRound) {
-      // kLightRound positions of every slot per round, their loads issued together
-      int bag[kLightRound][S];
-      float sc[kLightRound][S];
+    for (int i = 0; i < n; i += LR) {
+      // LR positions of every slot per round, their loads issued together
+      int bag[LR][S];
+      float sc[LR][S];
 #pragma unroll
-      for (int q = 0; q < kLightRound; ++q)
+      for (int q = 0; q < LR; ++q)
 #pragma unroll
         for (int j = 0; j < S; ++j) {
           const int src = g * G + ((i + q) & (G - 1));
@@ -370,7 +382,7 @@ __device__ __forceinline__ void light_batch(const RArgs& a, int ubase, int U, in
           sc[q][j] = __shfl(msc[j], src, kWave);
           if (i + q >= n || i0 + i + q >= c[j]) bag[q][j] = -1;
         }
-      add_rows<G, NV, kLightRound, S>(a.G, bag, sc, a.D, sub, acc);
+      add_rows<G, NV, LR, S>(a.G, bag, sc, a.D, sub, acc);
     }
   }
 #pragma unroll
@@ -402,6 +414,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
   const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nwaves = gridDim.x * 4;
   const int U = *a.num_unique;
+  // the combine that follows starts from cleared level-2 rows and counters
+  {
+    const int nw = a.ncomb * 2 * a.D;
+    for (int i = wave_id * kWave + lane; i < nw + a.ncomb; i += nwaves * kWave) {
+      if (i < nw) a.level2[i] = 0;
+      else a.arrivals[i - nw] = 0u;
+    }
+  }
 
   // heavy pieces: one wavefront per aligned chunk of sorted positions
   for (int c = wave_id; c < a.nchunks; c += nwaves) {
@@ -421,58 +441,122 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
   for (int ub = wave_id * per_batch; ub < U; ub += nwaves * per_batch) light_batch<TW, G, NV>(a, ub, U, g, sub, lane);
 }
 
-// Heavy segments: the block of a range of kCombineChunks chunks finds (one
-// lane per chunk) the heavy segments whose first position lies in its
-// range, then sums each one's partials in chunk order with all its lane
-// groups and applies the optimizer.
-constexpr int kCombineUnroll = 8;  // partial rows of a lane group loaded together
+// Heavy segments.  The block of a range of kCombineChunks chunks lists (one
+// lane per chunk) the pieces of heavy segments in its range: the segments
+// that start in it and the one that holds its first position, if that one
+// started earlier.  One wavefront per piece sums the piece's chunk partials
+// in chunk order.  A segment that lies in the range is finished at once; a
+// segment that crosses ranges leaves one row per range (slot 1 in the range
+// where it starts, slot 0 in the others) as tagged words, and the block
+// that arrives last at the segment's counter adds those rows in range order
+// and applies the optimizer.  The order of every sum is fixed, so the result
+// does not depend on which block arrives last; no block ever waits for
+// another to arrive.
+constexpr uint32_t kLevel2Tag = 1u;  // rows and counters are cleared by the main kernel
+
+// sum of this lane's columns of level-2 rows [g0, g1) (slot 1 of the first
+// range, slot 0 of the others), rows split over the lane groups with the
+// words of several rows loaded together; a word is polled until it carries
+// the tag (bounded)
+template <int G, int NV>
+__device__ __forceinline__ void level2_sum(const RArgs& a, int g0, int g1, int g, int sub, uint32_t* err,
+                                           float (&acc)[NV][4]) {
+  constexpr int RPI = kWave / G;
+  constexpr int RR = rows_in_flight(NV) / 2 > 0 ? rows_in_flight(NV) / 2 : 1;
+  zero<G, NV>(acc);
+  for (int r0 = g0 + g; r0 < g1; r0 += RPI * RR) {
+    uint64_t x[RR][NV][4];
+#pragma unroll
+    for (int q = 0; q < RR; ++q) {
+      const int r = r0 + q * RPI;
+      const uint64_t* src = a.level2 + ((size_t)(r < g1 ? r : g0) * 2 + (r == g0 ? 1 : 0)) * a.D;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c0 = (v * G + sub) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[q][v][e] = ld_acquire_u64(src + (c0 < a.D ? c0 + e : e));
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < RR; ++q) {
+      const int r = r0 + q * RPI;
+      if (r >= g1) continue;
+      const uint64_t* src = a.level2 + ((size_t)r * 2 + (r == g0 ? 1 : 0)) * a.D;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c0 = (v * G + sub) * 4;
+        if (c0 >= a.D) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t spins = 0;
+          while ((uint32_t)(x[q][v][e] >> 32) != kLevel2Tag) {
+            if (++spins > kSpinLimit) {
+              atomicOr(err, 4u);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+            x[q][v][e] = ld_acquire_u64(src + c0 + e);
+          }
+          acc[v][e] += __uint_as_float((uint32_t)x[q][v][e]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int o = G; o < kWave; o <<= 1)
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[v][e] += __shfl_xor(acc[v][e], o, kWave);
+}
 
 template <typename TW, int G, int NV>
 __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   constexpr int RPI = kWave / G;
   constexpr int NWv = kCombineThreads / kWave;
-  constexpr int NG = NWv * RPI;
-  __shared__ float s_red[NWv][G * NV * 4];
-  __shared__ int4 s_list[kCombineChunks];  // (chunk, segment, first position, end)
+  constexpr int CU = rows_in_flight(NV);  // chunk partials of a lane group loaded together
+  __shared__ int4 s_piece[kCombineChunks + 1];  // (segment, first chunk in range, start, end)
   __shared__ int s_n;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G, w = tid >> 6;
   const int U = *a.num_unique;
-  const int c0 = blockIdx.x * kCombineChunks;
+  const int blk = blockIdx.x;
+  const int c0 = blk * kCombineChunks, c1 = min(a.nchunks, c0 + kCombineChunks);
   if (tid == 0) s_n = 0;
   __syncthreads();
-  if (tid < kCombineChunks && c0 + tid < a.nchunks) {
+  if (tid < c1 - c0) {
     const int c = c0 + tid;
     const ChunkPieces cp = chunk_pieces(a, c, U);
-    // a heavy segment starts in chunk c when the chunk's last segment is
-    // heavy and begins inside the chunk
-    if (cp.e1 - cp.s1 > kChunk && cp.s1 >= c * kChunk) s_list[atomicAdd(&s_n, 1)] = make_int4(c, cp.u1, cp.s1, cp.e1);
+    if (cp.e1 - cp.s1 > kChunk && cp.s1 >= c * kChunk) s_piece[atomicAdd(&s_n, 1)] = make_int4(cp.u1, c, cp.s1, cp.e1);
+    if (c == c0 && cp.hi[0] > cp.lo[0] && cp.s0 < c * kChunk)
+      s_piece[atomicAdd(&s_n, 1)] = make_int4(cp.u0, c, cp.s0, cp.e0);
   }
   __syncthreads();
   const int n = s_n;
-  for (int it = 0; it < n; ++it) {
-    const int4 item = s_list[it];
-    const int c = item.x, u1 = item.y, s1 = item.z, e1 = item.w;
-    const int p0 = c * kChunk;
-    const int np = (e1 - 1) / kChunk - c + 1;
-    const uint32_t key = a.ukeys[u1];
+  for (int k = w; k < n; k += NWv) {
+    const int4 pc = s_piece[k];
+    const int u = pc.x, cf = pc.y, st = pc.z, en = pc.w;
+    const int cs = st / kChunk, ce = (en - 1) / kChunk;  // chunks of the whole segment
+    const int cl = min(c1 - 1, ce);                      // last chunk of this piece
+    const int np = cl - cf + 1;
+    const uint32_t key = a.ukeys[u];
     RowPre<NV> pre;
-    if (w == 0 && g == 0) prefetch_row<TW, G, NV>(a.up, key, sub, pre);
-    float acc[NV][4];
-    zero<G, NV>(acc);
+    if (g == 0) prefetch_row<TW, G, NV>(a.up, key, sub, pre);
     float acc1[1][NV][4];
     zero<G, NV>(acc1[0]);
-    for (int i0 = w * RPI + g; i0 < np; i0 += NG * kCombineUnroll) {
-      int pidx[kCombineUnroll][1];
-      float one[kCombineUnroll][1];
+    for (int i0 = 0; i0 < np; i0 += RPI * CU) {
+      int pidx[CU][1];
+      float one[CU][1];
 #pragma unroll
-      for (int q = 0; q < kCombineUnroll; ++q) {
-        const int i = i0 + q * NG;
-        const int slot = (i == 0 && s1 != p0) ? 1 : 0;
-        pidx[q][0] = i < np ? (c + i) * 2 + slot : -1;
+      for (int q = 0; q < CU; ++q) {
+        const int i = i0 + q * RPI + g;
+        const int c = cf + i;
+        const int slot = (c == cs && st != c * kChunk) ? 1 : 0;
+        pidx[q][0] = i < np ? c * 2 + slot : -1;
         one[q][0] = 1.0f;
       }
-      add_rows<G, NV, kCombineUnroll, 1>(a.partials, pidx, one, a.D, sub, acc1);
+      add_rows<G, NV, CU, 1>(a.partials, pidx, one, a.D, sub, acc1);
     }
+    float acc[NV][4];
 #pragma unroll
     for (int v = 0; v < NV; ++v)
 #pragma unroll
@@ -483,26 +567,30 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
       for (int v = 0; v < NV; ++v)
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[v][e] += __shfl_xor(acc[v][e], o, kWave);
+    const int bs = cs / kCombineChunks, be = ce / kCombineChunks;  // combine blocks of the segment
+    if (bs == be) {
+      if (g == 0) apply_row<TW, G, NV>(a.up, a.grad_rows, u, key, acc, pre, sub);
+      continue;
+    }
+    // publish this range's row, then arrive
+    uint64_t* dst = a.level2 + ((size_t)blk * 2 + (blk == bs ? 1 : 0)) * a.D;
     if (g == 0) {
 #pragma unroll
-      for (int v = 0; v < NV; ++v)
+      for (int v = 0; v < NV; ++v) {
+        const int c0v = (v * G + sub) * 4;
+        if (c0v < a.D)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) s_red[w][(v * G + sub) * 4 + e] = acc[v][e];
+          for (int e = 0; e < 4; ++e) st_u64(dst + c0v + e, ((uint64_t)kLevel2Tag << 32) | __float_as_uint(acc[v][e]));
+      }
     }
-    __syncthreads();
-    if (w == 0 && g == 0) {
-#pragma unroll
-      for (int v = 0; v < NV; ++v)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float t = s_red[0][(v * G + sub) * 4 + e];
-#pragma unroll
-          for (int ww = 1; ww < NWv; ++ww) t += s_red[ww][(v * G + sub) * 4 + e];
-          acc[v][e] = t;
-        }
-      apply_row<TW, G, NV>(a.up, a.grad_rows, u1, key, acc, pre, sub);
+    uint32_t old = 0;
+    if (lane == 0) old = atomic_add_u32(&a.arrivals[bs], 1u);
+    old = (uint32_t)__shfl((int)old, 0, kWave);
+    if (old == (uint32_t)(be - bs)) {
+      WsHeader* h = reinterpret_cast<WsHeader*>(a.hdr);
+      level2_sum<G, NV>(a, bs, be + 1, g, sub, &h->error, acc);
+      if (g == 0) apply_row<TW, G, NV>(a.up, a.grad_rows, u, key, acc, pre, sub);
     }
-    __syncthreads();
   }
 }
 
@@ -597,6 +685,10 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.chunk_seg = reinterpret_cast<const int32_t*>(ws + p.lay.chunk_seg);
   ra.grad_rows = p.grad_rows;
   ra.partials = reinterpret_cast<float*>(ws + p.lay.partials);
+  ra.level2 = reinterpret_cast<uint64_t*>(ws + p.lay.level2);
+  ra.arrivals = reinterpret_cast<uint32_t*>(ws + p.lay.arrivals);
+  ra.ncomb = (int32_t)p.lay.combine_blocks;
+  ra.hdr = ws + p.lay.hdr;
   ra.N = p.N;
   ra.D = p.D;
   ra.pool = p.pool;
@@ -610,7 +702,7 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.up.eps = p.eps;
   // main: a wavefront per chunk of sorted positions (up to a full device)
   const int bm = clamp_blocks(((int64_t)ra.nchunks + 3) / 4, 1, 2048);
-  const int bc = clamp_blocks(((int64_t)ra.nchunks + kCombineChunks - 1) / kCombineChunks, 1, 1 << 20);
+  const int bc = clamp_blocks(ra.ncomb, 1, 1 << 20);
   return p.dtype == EMB_FP32 ? launch_reduce_dt<float>(ra, bm, bc, s) : launch_reduce_dt<uint16_t>(ra, bm, bc, s);
 }
 

@@ -26,6 +26,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# workloads on which the pipelined schedule has run without fault
+PIPELINED_OK = ("c1", "c3")
 METRIC = "pooled lookups/sec (fwd+bwd+update) and achieved HBM GB/s vs peak, 1 GPU"
 COUNTERS = os.path.join(ROOT, "profiles", "c3_step_hbm_counters.txt")
 _CSRC = os.path.join(ROOT, "paper_2112_02752_amd", "csrc")
@@ -150,6 +152,11 @@ def main():
         return
 
     w = synth.workload(args.workload)
+    if args.schedule == "pipelined" and w.name not in PIPELINED_OK:
+        print(f"bench.py: the pipelined schedule is switched off for {w.name}: its first run (8 x 1M x 64, "
+              f"4096 bags per table) ended in a GPU memory fault whose cause is not yet found; use --schedule serial",
+              file=sys.stderr)
+        sys.exit(2)
     dev = "cuda"
     total = args.warmup + args.steps
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)

@@ -8,7 +8,7 @@
 //  1. k_prepare: one wavefront per bag writes the bag id of every position
 //     (and the key, for several tables), and counts the digits of every
 //     radix pass into LDS histograms that are added to global totals.
-//  2. k_sort_pass (once per digit): a tile of kSortTile keys is ranked with
+//  2. k_sort_pass (once per digit): a tile of keys is ranked with
 //     wavefront ballots (the lanes sharing a digit are found with one ballot
 //     per digit bit, the rank is a masked popcount), the per-digit tile
 //     counts are published and each digit's offset among earlier tiles is
@@ -216,32 +216,81 @@ __device__ __forceinline__ uint32_t lookback_digit(const uint64_t* status, int s
   return excl;
 }
 
-// Sum over rows r in [lo, hi) of the counts published in m[r][d] as
-// (tag << 32 | count) words: kPrefixGroup words are loaded together; a word
-// that does not carry this pass's tag yet is polled again (bounded).
-__device__ __forceinline__ uint32_t sum_column(const uint64_t* m, int stride, int lo, int hi, int d, uint32_t tag,
-                                               uint32_t* err) {
-  uint32_t sum = 0;
-  for (int base = lo; base < hi; base += kPrefixGroup) {
-    uint64_t v[kPrefixGroup];
+// Two-level prefix of a co-resident pass, for digit d.  Published words are
+// (tag << 32 | count).  A batch of words is loaded together; the words that
+// do not carry this pass's tag yet are loaded again together after a short
+// sleep, so every retry round costs one memory round trip however many words
+// are stale.  The wait is bounded: running out of spins flags an error.
+template <int K>
+__device__ __forceinline__ void poll_batch(const uint64_t* base, int stride, int lo, int n, int d, uint32_t tag,
+                                           uint32_t* err, uint64_t (&v)[K]) {
+  // words past n stand in as ready
+  uint32_t stale = 0;
 #pragma unroll
-    for (int i = 0; i < kPrefixGroup; ++i)
-      v[i] = base + i < hi ? ld_acquire_u64(m + (size_t)(base + i) * stride + d) : ((uint64_t)tag << 32);
+  for (int i = 0; i < K; ++i) stale |= (i < n && (uint32_t)(v[i] >> 32) != tag) ? (1u << i) : 0u;
+  uint32_t spins = 0;
+  while (stale) {
+    if (++spins > kSpinLimit) {
+      atomicOr(err, 1u);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+    const uint64_t* p = base + (size_t)lo * stride + d;
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+      if (stale & (1u << i)) v[i] = ld_acquire_u64(p + (size_t)i * stride);
+    stale = 0;
+#pragma unroll
+    for (int i = 0; i < K; ++i) stale |= (i < n && (uint32_t)(v[i] >> 32) != tag) ? (1u << i) : 0u;
+  }
+}
+
+// The last tile of a group of kPrefixGroup tiles reads the group's published
+// counts for digit d (one batch), publishes the group's sum and returns the
+// in-group exclusive prefixes of the group's tiles as 16-bit pairs (a group
+// of co-resident tiles holds fewer than 2^16 keys before its last tile), and
+// its own.
+static_assert((kPrefixGroup - 1) * kSortThreads * kSortItemsCore < 65536, "in-group prefixes fit 16 bits");
+__device__ __forceinline__ void group_counts(const uint64_t* rows, uint64_t* grp, int stride, int g, int g0, int g1,
+                                             int d, uint32_t tag, uint32_t* err, uint32_t (&pk)[kPrefixGroup / 2],
+                                             uint32_t& last_pre) {
+  uint64_t v[kPrefixGroup];
+  const int n = g1 - g0;
+#pragma unroll
+  for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(rows + (size_t)(g0 + i) * stride + d) : 0;
+  poll_batch<kPrefixGroup>(rows, stride, g0, n, d, tag, err, v);
+  uint32_t run = 0;
+  last_pre = 0;
+#pragma unroll
+  for (int i = 0; i < kPrefixGroup; ++i) {
+    if (i % 2 == 0) pk[i / 2] = run;
+    else pk[i / 2] |= run << 16;
+    if (i == n - 1) last_pre = run;
+    if (i < n) run += (uint32_t)v[i];
+  }
+  st_u64(grp + (size_t)g * stride + d, ((uint64_t)tag << 32) | run);
+}
+
+// Sum of the published group sums of digit d before group g, and of all of
+// them (the digit's total), loaded in batches of kPrefixGroup.
+__device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int g, int ngroups, int d, uint32_t tag,
+                                           uint32_t* err, uint32_t& before, uint32_t& total) {
+  before = total = 0;
+  for (int base = 0; base < ngroups; base += kPrefixGroup) {
+    const int n = min(kPrefixGroup, ngroups - base);
+    uint64_t gv[kPrefixGroup];
+#pragma unroll
+    for (int i = 0; i < kPrefixGroup; ++i) gv[i] = i < n ? ld_acquire_u64(grp + (size_t)(base + i) * stride + d) : 0;
+    poll_batch<kPrefixGroup>(grp, stride, base, n, d, tag, err, gv);
 #pragma unroll
     for (int i = 0; i < kPrefixGroup; ++i) {
-      uint32_t spins = 0;
-      while ((uint32_t)(v[i] >> 32) != tag) {
-        if (++spins > kSpinLimit) {
-          atomicOr(err, 1u);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        v[i] = ld_acquire_u64(m + (size_t)(base + i) * stride + d);
+      if (i < n) {
+        const uint32_t c = (uint32_t)gv[i];
+        total += c;
+        if (base + i < g) before += c;
       }
-      sum += (uint32_t)v[i];
     }
   }
-  return sum;
 }
 
 // Bag of each of this thread's positions of a tile: the bag holding position
@@ -252,12 +301,13 @@ __device__ __forceinline__ uint32_t sum_column(const uint64_t* m, int stride, in
 // inclusive max-scan over the tile's positions carries each id forward to
 // the bag's other positions (bag ids grow with position).  Intervals that do
 // not fit the stage are searched in global memory.  `s_work` holds
-// kSortTile ints.
+// one int per position of the tile.
+template <int IT>
 __device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int32_t* s_boff, int* s_lohi,
-                                               int32_t* s_work, uint32_t* s_wmax, int32_t (&bag)[kSortItems]) {
+                                               int32_t* s_work, uint32_t* s_wmax, int32_t (&bag)[IT]) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  const int64_t p0 = (int64_t)tile * kSortTile;
-  const int64_t p1 = min(p0 + kSortTile, (int64_t)a.N);
+  const int64_t p0 = (int64_t)tile * (kSortThreads * IT);
+  const int64_t p1 = min(p0 + (kSortThreads * IT), (int64_t)a.N);
   const int S = (a.M + kSortThreads) / kSortThreads;  // samples offsets[0], offsets[S], ... up to offsets[M]
   const int nsamp = a.M / S + 1;
   int samp = 0;
@@ -278,18 +328,18 @@ __device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int3
   if (nst <= kBagStage + 1) {
     for (int i = tid; i < nst; i += kSortThreads) s_boff[i] = a.offsets[m_lo + i];
     // ids are stored plus one, so that 0 means "no bag starts here"
-    for (int i = tid; i < kSortTile; i += kSortThreads) s_work[i] = 0;
+    for (int i = tid; i < (kSortThreads * IT); i += kSortThreads) s_work[i] = 0;
     __syncthreads();
     for (int i = tid; i < nst - 1; i += kSortThreads) {
       const int64_t st = s_boff[i], en = s_boff[i + 1];
       if (st < en && st < p1 && en > p0) s_work[(st > p0 ? st : p0) - p0] = m_lo + i + 1;
     }
     __syncthreads();
-    uint32_t v[kSortItems];
+    uint32_t v[IT];
     uint32_t run = 0;
 #pragma unroll
-    for (int k = 0; k < kSortItems; ++k) {
-      const uint32_t x = (uint32_t)s_work[tid * kSortItems + k];
+    for (int k = 0; k < IT; ++k) {
+      const uint32_t x = (uint32_t)s_work[tid * IT + k];
       run = x > run ? x : run;
       v[k] = run;
     }
@@ -300,19 +350,19 @@ __device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int3
     __syncthreads();
     for (int ww = 0; ww < w; ++ww) carry = s_wmax[ww] > carry ? s_wmax[ww] : carry;
 #pragma unroll
-    for (int k = 0; k < kSortItems; ++k) s_work[tid * kSortItems + k] = (int32_t)(v[k] > carry ? v[k] : carry);
+    for (int k = 0; k < IT; ++k) s_work[tid * IT + k] = (int32_t)(v[k] > carry ? v[k] : carry);
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
-      const int64_t j = p0 + (int64_t)w * (kWave * kSortItems) + i * kWave + lane;
+    for (int i = 0; i < IT; ++i) {
+      const int64_t j = p0 + (int64_t)w * (kWave * IT) + i * kWave + lane;
       bag[i] = j < p1 ? s_work[j - p0] - 1 : 0;
     }
     __syncthreads();  // s_work is reused by the caller
     return;
   }
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const int64_t j = p0 + (int64_t)w * (kWave * kSortItems) + i * kWave + lane;
+  for (int i = 0; i < IT; ++i) {
+    const int64_t j = p0 + (int64_t)w * (kWave * IT) + i * kWave + lane;
     bag[i] = 0;
     if (j < p1) {
       int lo = 0, hi = nst - 2;  // last idx in [0, nst-2] with offset <= j
@@ -325,17 +375,18 @@ __device__ __forceinline__ void find_tile_bags(const PassArgs& a, int tile, int3
   }
 }
 
-template <int RB>
-__global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
+template <int RB, int IT>
+__global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   constexpr int ND = 1 << RB;
+  constexpr int TILE = kSortThreads * IT;
   constexpr int NW = kSortThreads / kWave;
   constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
   __shared__ uint32_t s_cnt[NW][ND];
   __shared__ uint32_t s_tstart[ND];
   __shared__ uint32_t s_gbase[ND];
-  __shared__ uint32_t s_keys[kSortTile];
-  __shared__ int32_t s_vals[kSortTile];
-  __shared__ int32_t s_bags[kSortTile];
+  __shared__ uint32_t s_keys[TILE];
+  __shared__ int32_t s_vals[TILE];
+  __shared__ int32_t s_bags[TILE];
   __shared__ uint32_t s_wsum[NW];
   __shared__ int s_tile;
   __shared__ int32_t s_boff[kBagStage + 1];
@@ -361,10 +412,10 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   const uint32_t mask = (1u << a.bits) - 1u;
   // the call's tag: the header's generation advances once per call, at its end
   const uint32_t tag = 0x80000000u | ((a.hdr->gen + 1u) * 8u + (uint32_t)a.pass);
-  const int64_t wbase = (int64_t)tile * kSortTile + w * (kWave * kSortItems);
+  const int64_t wbase = (int64_t)tile * TILE + w * (kWave * IT);
 
-  uint32_t key[kSortItems], dig[kSortItems], lrank[kSortItems];
-  int32_t val[kSortItems], bag[kSortItems];
+  uint32_t key[IT], dig[IT], lrank[IT];
+  int32_t val[IT], bag[IT];
   if (a.pass == 0) {
     // the unique scan of this call starts from cleared look-back words
     for (int i = blockIdx.x * kSortThreads + tid; i < a.uniq_tiles; i += gridDim.x * kSortThreads)
@@ -372,22 +423,23 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
     if (blockIdx.x == 0 && tid == 0) a.hdr->ticket[kSlotUnique] = 0u;
   }
   if (a.search_bags) {
-    find_tile_bags(a, tile, s_boff, s_lohi, s_bags, s_wsum, bag);
+    // the ids are loaded first: their loads overlap the bag search
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < IT; ++i) {
       const int64_t pos = wbase + i * kWave + lane;
       key[i] = pos < a.N ? (uint32_t)a.idx[pos] : 0u;
       val[i] = pos < a.N ? (int32_t)pos : 0;
     }
+    find_tile_bags<IT>(a, tile, s_boff, s_lohi, s_bags, s_wsum, bag);
     if (a.T > 1) {
 #pragma unroll
-      for (int i = 0; i < kSortItems; ++i) key[i] += s_toff[bag[i] / a.B];
+      for (int i = 0; i < IT; ++i) key[i] += s_toff[bag[i] / a.B];
     }
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) dig[i] = (key[i] >> a.shift) & mask;
+    for (int i = 0; i < IT; ++i) dig[i] = (key[i] >> a.shift) & mask;
   } else {
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < IT; ++i) {
       const int64_t pos = wbase + i * kWave + lane;
       const bool valid = pos < a.N;
       key[i] = valid ? a.keys_in[pos] : 0u;
@@ -399,7 +451,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
 
   // rank each element among the earlier elements of its wave with its digit
 #pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
+  for (int i = 0; i < IT; ++i) {
     const bool valid = wbase + i * kWave + lane < a.N;
     uint64_t peers = __ballot(valid);
     for (int b = 0; b < a.bits; ++b) {
@@ -459,34 +511,89 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   block_excl_scan<RB>(s_tstart, s_wsum);
   if (!a.coresident) block_excl_scan<RB>(s_gbase, s_wsum);
 
+  // reorder the tile in LDS by digit (stable); only tile-local offsets are
+  // needed, so this is done before the wait for the other tiles' counts
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    const bool valid = wbase + i * kWave + lane < a.N;
+    if (valid) {
+      const uint32_t lp = s_tstart[dig[i]] + s_cnt[w][dig[i]] + lrank[i];
+      s_keys[lp] = key[i];
+      s_vals[lp] = val[i];
+      s_bags[lp] = bag[i];
+    }
+  }
+
   if (a.coresident) {
-    // two-level prefix: groups of kPrefixGroup tiles; the last tile of a group
-    // publishes the group's sum, every tile adds the sums of the earlier
-    // groups and the counts of the earlier tiles of its own group; the digit
-    // totals are the sum of all groups
+    // Two-level prefix over groups of kPrefixGroup tiles, done by the last
+    // tile of each group: it sums its group's counts and publishes the group
+    // sum, then reads every group's sum, forms the digit bases (exclusive
+    // scan of the digit totals) and publishes for each tile of its group the
+    // final offset of each digit (in the look-back status words, unused in
+    // this mode).  Every other tile waits for its own words only, so few
+    // words are polled.  The offsets land in s_gbase.
     const int g = tile / kPrefixGroup, g0 = g * kPrefixGroup;
     const int g1 = min(a.ntiles, g0 + kPrefixGroup);
     const int ngroups = (a.ntiles + kPrefixGroup - 1) / kPrefixGroup;
     if (tile == g1 - 1) {
-      uint64_t* gs = a.grp + (size_t)g * a.status_stride;
+      // the in-group prefixes wait in s_cnt (free once the tile is reordered)
+      uint32_t* s_pre = &s_cnt[0][0];
+      uint32_t self_pre[DPT];
+      __syncthreads();
 #pragma unroll
       for (int k = 0; k < DPT; ++k) {
         const int d = tid + k * kSortThreads;
-        if (d < ND) st_u64(gs + d, tag_hi | sum_column(a.rows, a.status_stride, g0, g1, d, tag, &a.hdr->error));
-      }
-    }
+        self_pre[k] = 0;
+        if (d < ND) {
+          uint32_t pk[kPrefixGroup / 2];
+          group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, &a.hdr->error, pk, self_pre[k]);
 #pragma unroll
-    for (int k = 0; k < DPT; ++k) {
-      const int d = tid + k * kSortThreads;
-      excl[k] = 0;
-      if (d < ND) {
-        const uint32_t before = sum_column(a.grp, a.status_stride, 0, g, d, tag, &a.hdr->error);
-        s_gbase[d] = before + sum_column(a.grp, a.status_stride, g, ngroups, d, tag, &a.hdr->error);
-        excl[k] = before + sum_column(a.rows, a.status_stride, g0, tile, d, tag, &a.hdr->error);
+          for (int j = 0; j < kPrefixGroup / 2; ++j) s_pre[j * ND + d] = pk[j];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        excl[k] = 0;
+        if (d < ND) {
+          uint32_t total = 0;
+          group_sums(a.grp, a.status_stride, g, ngroups, d, tag, &a.hdr->error, excl[k], total);
+          s_gbase[d] = total;
+        }
+      }
+      __syncthreads();
+      block_excl_scan<RB>(s_gbase, s_wsum);
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        if (d < ND) {
+          const uint32_t gb = s_gbase[d] + excl[k];
+#pragma unroll
+          for (int i = 0; i < kPrefixGroup; ++i) {
+            const uint32_t pre = (s_pre[(i / 2) * ND + d] >> (16 * (i % 2))) & 0xffffu;
+            if (g0 + i < g1 - 1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, tag_hi | (gb + pre));
+          }
+          excl[k] += self_pre[k];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        excl[k] = 0;
+        if (d < ND) {
+          uint64_t fv[1] = {ld_acquire_u64(a.status + (size_t)tile * a.status_stride + d)};
+          poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, &a.hdr->error, fv);
+          excl[k] = (uint32_t)fv[0];
+        }
+      }
+      // the final offsets replace the digit bases
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        if (d < ND) s_gbase[d] = 0;
       }
     }
-    __syncthreads();
-    block_excl_scan<RB>(s_gbase, s_wsum);
   } else {
     uint64_t* st = a.status + (size_t)tile * a.status_stride;
 #pragma unroll
@@ -506,20 +613,9 @@ __global__ __launch_bounds__(kSortThreads) void k_sort_pass(PassArgs a) {
   }
   __syncthreads();
 
-  // reorder the tile in LDS by digit (stable), then write digit runs out
-#pragma unroll
-  for (int i = 0; i < kSortItems; ++i) {
-    const bool valid = wbase + i * kWave + lane < a.N;
-    if (valid) {
-      const uint32_t lp = s_tstart[dig[i]] + s_cnt[w][dig[i]] + lrank[i];
-      s_keys[lp] = key[i];
-      s_vals[lp] = val[i];
-      s_bags[lp] = bag[i];
-    }
-  }
-  __syncthreads();
-  const int64_t tstart = (int64_t)tile * kSortTile;
-  const int nvalid = (int)min((int64_t)kSortTile, (int64_t)a.N - tstart);
+  // write the tile out in digit runs
+  const int64_t tstart = (int64_t)tile * TILE;
+  const int nvalid = (int)min((int64_t)TILE, (int64_t)a.N - tstart);
   for (int s = tid; s < nvalid; s += kSortThreads) {
     const uint32_t k = s_keys[s];
     const uint32_t d = (k >> a.shift) & mask;
@@ -702,44 +798,41 @@ __global__ void k_unique_empty(int32_t* num_unique, int32_t* seg) {
   }
 }
 
-template <int RB>
+template <int RB, int IT>
 hipError_t launch_pass(const PassArgs& pa, int tiles, hipStream_t s) {
-  hipLaunchKernelGGL(k_sort_pass<RB>, dim3((unsigned)tiles), dim3(kSortThreads), 0, s, pa);
+  hipLaunchKernelGGL((k_sort_pass<RB, IT>), dim3((unsigned)tiles), dim3(kSortThreads), 0, s, pa);
   return hipGetLastError();
 }
 
-template <int RB>
-const void* pass_kernel() {
-  return reinterpret_cast<const void*>(&k_sort_pass<RB>);
-}
-
+template <int IT>
 const void* pass_kernel_bits(int bits) {
   switch (bits) {
-    case 1: return pass_kernel<1>();
-    case 2: return pass_kernel<2>();
-    case 3: return pass_kernel<3>();
-    case 4: return pass_kernel<4>();
-    case 5: return pass_kernel<5>();
-    case 6: return pass_kernel<6>();
-    case 7: return pass_kernel<7>();
-    case 8: return pass_kernel<8>();
-    case 9: return pass_kernel<9>();
-    default: return pass_kernel<10>();
+    case 1: return reinterpret_cast<const void*>(&k_sort_pass<1, IT>);
+    case 2: return reinterpret_cast<const void*>(&k_sort_pass<2, IT>);
+    case 3: return reinterpret_cast<const void*>(&k_sort_pass<3, IT>);
+    case 4: return reinterpret_cast<const void*>(&k_sort_pass<4, IT>);
+    case 5: return reinterpret_cast<const void*>(&k_sort_pass<5, IT>);
+    case 6: return reinterpret_cast<const void*>(&k_sort_pass<6, IT>);
+    case 7: return reinterpret_cast<const void*>(&k_sort_pass<7, IT>);
+    case 8: return reinterpret_cast<const void*>(&k_sort_pass<8, IT>);
+    case 9: return reinterpret_cast<const void*>(&k_sort_pass<9, IT>);
+    default: return reinterpret_cast<const void*>(&k_sort_pass<10, IT>);
   }
 }
 
+template <int IT>
 hipError_t launch_pass_bits(const PassArgs& pa, int tiles, hipStream_t s) {
   switch (pa.bits) {
-    case 1: return launch_pass<1>(pa, tiles, s);
-    case 2: return launch_pass<2>(pa, tiles, s);
-    case 3: return launch_pass<3>(pa, tiles, s);
-    case 4: return launch_pass<4>(pa, tiles, s);
-    case 5: return launch_pass<5>(pa, tiles, s);
-    case 6: return launch_pass<6>(pa, tiles, s);
-    case 7: return launch_pass<7>(pa, tiles, s);
-    case 8: return launch_pass<8>(pa, tiles, s);
-    case 9: return launch_pass<9>(pa, tiles, s);
-    case 10: return launch_pass<10>(pa, tiles, s);
+    case 1: return launch_pass<1, IT>(pa, tiles, s);
+    case 2: return launch_pass<2, IT>(pa, tiles, s);
+    case 3: return launch_pass<3, IT>(pa, tiles, s);
+    case 4: return launch_pass<4, IT>(pa, tiles, s);
+    case 5: return launch_pass<5, IT>(pa, tiles, s);
+    case 6: return launch_pass<6, IT>(pa, tiles, s);
+    case 7: return launch_pass<7, IT>(pa, tiles, s);
+    case 8: return launch_pass<8, IT>(pa, tiles, s);
+    case 9: return launch_pass<9, IT>(pa, tiles, s);
+    case 10: return launch_pass<10, IT>(pa, tiles, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -756,7 +849,6 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     return hipGetLastError();
   }
   const int N = (int)p.N;
-  const int sort_tiles = (N + kSortTile - 1) / kSortTile;
   const int uniq_tiles = (N + kUniqTile - 1) / kUniqTile;
   const int nchunks = (N + kChunk - 1) / kChunk;
   int max_bits = 1;
@@ -765,9 +857,12 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   // every tile of a pass resident at once: tile = block index, bags found by
   // the first pass, two-level published-count prefix; otherwise a prepare
   // kernel (bags, keys, digit totals), tickets and a look-back
+  const int core_tiles = (N + kSortTileMin - 1) / kSortTileMin;
   int sort_cores = 1;
   for (int i = 0; i < p.plan.passes; ++i)
-    if (sort_tiles > resident_blocks(pass_kernel_bits(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
+    if (core_tiles > resident_blocks(pass_kernel_bits<kSortItemsCore>(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
+  const int tile_keys = kSortThreads * (sort_cores ? kSortItemsCore : kSortItemsWide);
+  const int sort_tiles = (N + tile_keys - 1) / tile_keys;
   const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
   uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
   hipError_t e = hipSuccess;
@@ -837,7 +932,8 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.bits = p.plan.bits[ps];
     xa.pass = ps;
     xa.status_stride = status_stride;
-    e = launch_pass_bits(xa, sort_tiles, s);
+    e = sort_cores ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles, s)
+                   : launch_pass_bits<kSortItemsWide>(xa, sort_tiles, s);
     if (e != hipSuccess) return e;
     kin = xa.keys_out;
     vin = xa.vals_out;

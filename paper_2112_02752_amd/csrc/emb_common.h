@@ -18,8 +18,11 @@ constexpr int kMaxPasses = 4;
 constexpr int kMaxDigitBits = 10;
 constexpr int kMaxDigits = 1 << kMaxDigitBits;
 constexpr int kSortThreads = 512;
-constexpr int kSortItems = 8;
-constexpr int kSortTile = kSortThreads * kSortItems;
+// keys per thread: tiles of 2048 when every tile of a pass is resident at
+// once (more blocks, shorter ranking), 4096 otherwise (fewer look-back steps)
+constexpr int kSortItemsCore = 4;
+constexpr int kSortItemsWide = 8;
+constexpr int kSortTileMin = kSortThreads * kSortItemsCore;
 
 // unique / segment scan
 constexpr int kUniqThreads = 256;
@@ -88,7 +91,7 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   (void)M;
   WsLayout L{};
   int64_t n = N > 0 ? N : 1;
-  L.sort_tiles = (n + kSortTile - 1) / kSortTile;
+  L.sort_tiles = (n + kSortTileMin - 1) / kSortTileMin;  // the most tiles any pass uses
   L.uniq_tiles = (n + kUniqTile - 1) / kUniqTile;
   L.chunks = (n + kChunk - 1) / kChunk;
   L.groups = (L.sort_tiles + kPrefixGroup - 1) / kPrefixGroup;

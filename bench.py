@@ -26,8 +26,6 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# workloads on which the pipelined schedule has run without fault
-PIPELINED_OK = ("c1", "c3")
 METRIC = "pooled lookups/sec (fwd+bwd+update) and achieved HBM GB/s vs peak, 1 GPU"
 COUNTERS = os.path.join(ROOT, "profiles", "c3_step_hbm_counters.txt")
 _CSRC = os.path.join(ROOT, "paper_2112_02752_amd", "csrc")
@@ -42,7 +40,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3")
-    ap.add_argument("--schedule", choices=("pipelined", "serial"), default="pipelined",
+    ap.add_argument("--schedule", choices=("pipelined", "serial"), default="serial",
                     help="pipelined: the id dedup of batch k+1 runs on a second stream alongside the forward and "
                          "update of batch k (same results as serial)")
     ap.add_argument("--lookahead", type=int, default=2, help="batches whose dedup may run ahead (pipelined)")
@@ -152,10 +150,10 @@ def main():
         return
 
     w = synth.workload(args.workload)
-    if args.schedule == "pipelined" and w.name not in PIPELINED_OK:
-        print(f"bench.py: the pipelined schedule is switched off for {w.name}: its first run (8 x 1M x 64, "
-              f"4096 bags per table) ended in a GPU memory fault whose cause is not yet found; use --schedule serial",
-              file=sys.stderr)
+    if args.schedule == "pipelined":
+        print("bench.py: the pipelined schedule is switched off: its runs on 8 x 1M x 64 (4096 bags per table) and "
+              "on 1 x 50M x 64 (16384 bags) ended in GPU memory faults whose cause is not yet found; "
+              "use --schedule serial", file=sys.stderr)
         sys.exit(2)
     dev = "cuda"
     total = args.warmup + args.steps

@@ -300,6 +300,11 @@ class _Hip:
             raise RuntimeError(f"hipStreamWaitEvent: {rc}")
 
 
+# The pipelined schedule stays off until the cause of the GPU memory faults
+# seen with it is found (it is kept, unused, for that work).
+PIPELINE_ENABLED = False
+
+
 class Pipeline:
     """Training steps of the layer with the id dedup of later batches
     overlapped with the forward and update of the current one.
@@ -314,6 +319,10 @@ class Pipeline:
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
                  max_indices: int = 0, max_bags: int = 0, lookahead: int = 2):
+        if not PIPELINE_ENABLED:
+            raise RuntimeError("the pipelined schedule is switched off: runs of it on MI355X ended in GPU memory "
+                               "faults (two dedups of many tiles in flight together) whose cause is not yet found; "
+                               "use Layer.step")
         import torch
         if lookahead < 1:
             raise ValueError("lookahead must be >= 1")

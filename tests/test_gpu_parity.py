@@ -286,6 +286,8 @@ def test_c2_unfused_path():
     parity.run_workload(w, steps=1, fused=False)
 
 
+@pytest.mark.skip(reason="the pipelined schedule is switched off: bench runs of it (two dedups of 204 and 240 "
+                         "tiles in flight together) ended in GPU memory faults whose cause is not yet found")
 @pytest.mark.parametrize("lookahead", [1, 2, 3])
 def test_pipelined_schedule_equals_serial(lookahead):
     """Dedup of batch k+1 overlapped with batch k (second stream) changes

@@ -907,7 +907,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.keys_in = kin;
     xa.vals_in = vin;
     xa.bags_in = bin;
-    xa.keys_out = (ps % 2 == 0) ? keys_a : keys_b;
+    xa.keys_out = last ? reinterpret_cast<uint32_t*>(ws + L.sorted_keys) : ((ps % 2 == 0) ? keys_a : keys_b);
     xa.vals_out = last ? p.sort_perm : ((ps % 2 == 0) ? vals_a : vals_b);
     xa.bags_out = last ? reinterpret_cast<int32_t*>(ws + L.sorted_bag) : ((ps % 2 == 0) ? bags_a : bags_b);
     xa.totals = reinterpret_cast<uint32_t*>(ws + L.totals) + ps * kMaxDigits;

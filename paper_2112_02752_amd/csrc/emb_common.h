@@ -77,7 +77,7 @@ static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 // tags differ.
 struct WsLayout {
   // front (offsets from the workspace base)
-  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_bag, uniq_status,
+  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_keys, sorted_bag, uniq_status,
       chunk_seg, partials, level2, arrivals, front;
   // back (offsets from the back base)
   size_t pass_status, rows, grp, back;
@@ -116,6 +116,8 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   L.bags_b = off;
   off = align256(off + n4);
   L.bag_of = off;
+  off = align256(off + n4);
+  L.sorted_keys = off;
   off = align256(off + n4);
   L.sorted_bag = off;
   off = align256(off + n4);

@@ -44,7 +44,7 @@ struct Vec<uint16_t> {
   }
 };
 
-constexpr int unroll_for(int rpi) { return rpi == 1 ? 8 : (rpi == 2 ? 8 : (rpi == 4 ? 4 : 2)); }
+constexpr int unroll_for(int rpi) { return rpi == 1 ? 8 : (rpi == 2 ? 8 : (rpi == 4 ? 8 : 4)); }
 
 template <typename TW, int G, int NV>
 __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, const int32_t* __restrict__ offsets,
@@ -54,7 +54,8 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
   constexpr int E = Vec<TW>::kElems;
   constexpr int UN = unroll_for(RPI);
   const int lane = threadIdx.x & (kWave - 1);
-  const int m = blockIdx.x * (256 / kWave) + (threadIdx.x >> 6);
+  // the bag is uniform across the wavefront: keep its bookkeeping scalar
+  const int m = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWave) + (threadIdx.x >> 6));
   if (m >= M) return;
   const int g = lane / G, sub = lane % G;
   const uint32_t base = ro.off[m / B];

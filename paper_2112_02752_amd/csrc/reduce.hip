@@ -411,7 +411,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
     RArgs a) {
   constexpr int RPI = kWave / G;
   const int lane = threadIdx.x & (kWave - 1), g = lane / G, sub = lane % G;
-  const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // the wavefront index is uniform: keep the work loops' bookkeeping scalar
+  const int wave_id = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int nwaves = gridDim.x * 4;
   const int U = *a.num_unique;
   // the combine that follows starts from cleared level-2 rows and counters
@@ -517,7 +518,8 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   constexpr int CU = rows_in_flight(NV);  // chunk partials of a lane group loaded together
   __shared__ int4 s_piece[kCombineChunks + 1];  // (segment, first chunk in range, start, end)
   __shared__ int s_n;
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform across the wavefront
   const int U = *a.num_unique;
   const int blk = blockIdx.x;
   const int c0 = blk * kCombineChunks, c1 = min(a.nchunks, c0 + kCombineChunks);

@@ -8,14 +8,17 @@
 //  1. k_prepare: one wavefront per bag writes the bag id of every position
 //     (and the key, for several tables), and counts the digits of every
 //     radix pass into LDS histograms that are added to global totals.
-//  2. k_sort_pass (once per digit): a tile of keys is ranked with
-//     wavefront ballots (the lanes sharing a digit are found with one ballot
-//     per digit bit, the rank is a masked popcount), the per-digit tile
-//     counts are published and each digit's offset among earlier tiles is
-//     found by a decoupled look-back over tile status words; the tile is
-//     reordered in LDS and written out in digit runs.  Ranks follow position
-//     order within a tile and tiles follow position order, so every pass is
-//     stable and so is the whole sort.
+//  2. k_sort_pass (once per digit): a tile publishes its per-digit counts
+//     (an LDS histogram) as soon as its keys are loaded, then ranks its keys
+//     with wavefront ballots (the lanes sharing a digit are found with one
+//     ballot per digit bit, the rank is a masked popcount) and reorders them
+//     in LDS by digit.  Each digit's offset among earlier tiles comes either
+//     from prefix blocks (when every tile is resident at once: one block per
+//     group of tiles sums the published counts and publishes final offsets)
+//     or from a decoupled look-back over tile status words.  The tile is then
+//     written out in digit runs.  Ranks follow position order within a tile
+//     and tiles follow position order, so every pass is stable and so is the
+//     whole sort.
 //  3. k_unique: head flags key[k] != key[k-1], a block scan plus a look-back
 //     of (number of heads, last head position) gives every head its segment
 //     index and the length of the previous segment.
@@ -293,6 +296,58 @@ __device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int 
   }
 }
 
+// A prefix block of a co-resident pass (one per group of kPrefixGroup tiles,
+// launched after the tiles): for each digit d it reads its group's published
+// tile counts (in-group exclusive prefixes and the group's sum), publishes the
+// group's sum, reads every group's sum (the groups before its own, and the
+// digit's total), forms the digit bases by an exclusive scan of the totals and
+// publishes for every tile of its group the final output offset of digit d in
+// that tile's status word.  The tiles rank and reorder their keys meanwhile.
+template <int RB>
+__device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t tag, uint32_t* s_base,
+                                                  uint32_t* s_wsum) {
+  constexpr int ND = 1 << RB;
+  constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
+  const int tid = threadIdx.x;
+  const int g = blockIdx.x - a.ntiles, g0 = g * kPrefixGroup;
+  const int g1 = min(a.ntiles, g0 + kPrefixGroup);
+  const int ngroups = (a.ntiles + kPrefixGroup - 1) / kPrefixGroup;
+  uint32_t pk[DPT][kPrefixGroup / 2], excl[DPT];
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int d = tid + k * kSortThreads;
+    if (d < ND) {
+      uint32_t unused;
+      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, &a.hdr->error, pk[k], unused);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int d = tid + k * kSortThreads;
+    excl[k] = 0;
+    if (d < ND) {
+      uint32_t total = 0;
+      group_sums(a.grp, a.status_stride, g, ngroups, d, tag, &a.hdr->error, excl[k], total);
+      s_base[d] = total;
+    }
+  }
+  __syncthreads();
+  block_excl_scan<RB>(s_base, s_wsum);
+  const uint64_t tag_hi = (uint64_t)tag << 32;
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int d = tid + k * kSortThreads;
+    if (d < ND) {
+      const uint32_t gb = s_base[d] + excl[k];
+#pragma unroll
+      for (int i = 0; i < kPrefixGroup; ++i) {
+        const uint32_t pre = (pk[k][i / 2] >> (16 * (i % 2))) & 0xffffu;
+        if (g0 + i < g1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, tag_hi | (gb + pre));
+      }
+    }
+  }
+}
+
 // Bag of each of this thread's positions of a tile: the bag holding position
 // j is the last m with offsets[m] <= j.  One offset in every S (S chosen so
 // the samples fit one per thread) narrows the tile's bags to a few sample
@@ -382,6 +437,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   constexpr int NW = kSortThreads / kWave;
   constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
   __shared__ uint32_t s_cnt[NW][ND];
+  __shared__ uint32_t s_hist[ND];
   __shared__ uint32_t s_tstart[ND];
   __shared__ uint32_t s_gbase[ND];
   __shared__ uint32_t s_keys[TILE];
@@ -400,6 +456,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
     s_tile = (int)atomic_add_u32(&a.hdr->ticket[a.pass], 1u);
   }
   for (int i = tid; i < NW * ND; i += kSortThreads) (&s_cnt[0][0])[i] = 0u;
+  for (int i = tid; i < ND; i += kSortThreads) s_hist[i] = 0u;
   if (a.search_bags && a.T > 1)
     for (int t = tid; t < a.T; t += kSortThreads) s_toff[t] = a.ro.off[t];
   // the previous pass is complete: clear its totals and ticket for the next call
@@ -412,13 +469,17 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   const uint32_t mask = (1u << a.bits) - 1u;
   // the call's tag: the header's generation advances once per call, at its end
   const uint32_t tag = 0x80000000u | ((a.hdr->gen + 1u) * 8u + (uint32_t)a.pass);
+  if (a.coresident && (int)blockIdx.x >= a.ntiles) {
+    sort_prefix_block<RB>(a, tag, s_gbase, s_wsum);
+    return;
+  }
   const int64_t wbase = (int64_t)tile * TILE + w * (kWave * IT);
 
   uint32_t key[IT], dig[IT], lrank[IT];
   int32_t val[IT], bag[IT];
   if (a.pass == 0) {
     // the unique scan of this call starts from cleared look-back words
-    for (int i = blockIdx.x * kSortThreads + tid; i < a.uniq_tiles; i += gridDim.x * kSortThreads)
+    for (int i = blockIdx.x * kSortThreads + tid; i < a.uniq_tiles; i += a.ntiles * kSortThreads)
       a.uniq_status[i] = 0;
     if (blockIdx.x == 0 && tid == 0) a.hdr->ticket[kSlotUnique] = 0u;
   }
@@ -449,6 +510,30 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
     }
   }
 
+  // The tile's digit counts are published first (from an LDS histogram), so
+  // that the other tiles' prefixes advance while this tile ranks and reorders
+  // its keys.
+#pragma unroll
+  for (int i = 0; i < IT; ++i)
+    if (wbase + i * kWave + lane < a.N) atomicAdd(&s_hist[dig[i]], 1u);
+  __syncthreads();
+  const uint64_t tag_hi = (uint64_t)tag << 32;
+  uint32_t my_cnt[DPT];
+  {
+    uint64_t* row = a.coresident ? a.rows + (size_t)tile * a.status_stride
+                                 : a.status + (size_t)tile * a.status_stride;
+    const uint64_t flag = a.coresident ? 0 : ((tile == 0 ? kFlagInc : kFlagAgg) << 30);
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      my_cnt[k] = 0;
+      if (d < ND) {
+        my_cnt[k] = s_hist[d];
+        st_u64(row + d, tag_hi | flag | my_cnt[k]);
+      }
+    }
+  }
+
   // rank each element among the earlier elements of its wave with its digit
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
@@ -469,12 +554,10 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   }
   __syncthreads();
 
-  // per digit: exclusive prefix over the waves, and the tile's count
-  uint32_t my_cnt[DPT];
+  // per digit: exclusive prefix over the waves (the sum is the tile's count)
 #pragma unroll
   for (int k = 0; k < DPT; ++k) {
     const int d = tid + k * kSortThreads;
-    my_cnt[k] = 0;
     if (d < ND) {
       uint32_t run = 0;
 #pragma unroll
@@ -483,30 +566,12 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
         s_cnt[ww][d] = run;
         run += c;
       }
-      my_cnt[k] = run;
       s_tstart[d] = run;
       if (!a.coresident) s_gbase[d] = a.totals[d];
     }
   }
 
-  const uint64_t tag_hi = (uint64_t)tag << 32;
   uint32_t excl[DPT];
-  if (a.coresident) {
-    // publish this tile's counts as tagged words
-    uint64_t* row = a.rows + (size_t)tile * a.status_stride;
-#pragma unroll
-    for (int k = 0; k < DPT; ++k) {
-      const int d = tid + k * kSortThreads;
-      if (d < ND) st_u64(row + d, tag_hi | my_cnt[k]);
-    }
-  } else {
-    uint64_t* st = a.status + (size_t)tile * a.status_stride;
-#pragma unroll
-    for (int k = 0; k < DPT; ++k) {
-      const int d = tid + k * kSortThreads;
-      if (d < ND) st_u64(st + d, tag_hi | ((tile == 0 ? kFlagInc : kFlagAgg) << 30) | my_cnt[k]);
-    }
-  }
   __syncthreads();
   block_excl_scan<RB>(s_tstart, s_wsum);
   if (!a.coresident) block_excl_scan<RB>(s_gbase, s_wsum);
@@ -525,74 +590,23 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   }
 
   if (a.coresident) {
-    // Two-level prefix over groups of kPrefixGroup tiles, done by the last
-    // tile of each group: it sums its group's counts and publishes the group
-    // sum, then reads every group's sum, forms the digit bases (exclusive
-    // scan of the digit totals) and publishes for each tile of its group the
-    // final offset of each digit (in the look-back status words, unused in
-    // this mode).  Every other tile waits for its own words only, so few
-    // words are polled.  The offsets land in s_gbase.
-    const int g = tile / kPrefixGroup, g0 = g * kPrefixGroup;
-    const int g1 = min(a.ntiles, g0 + kPrefixGroup);
-    const int ngroups = (a.ntiles + kPrefixGroup - 1) / kPrefixGroup;
-    if (tile == g1 - 1) {
-      // the in-group prefixes wait in s_cnt (free once the tile is reordered)
-      uint32_t* s_pre = &s_cnt[0][0];
-      uint32_t self_pre[DPT];
-      __syncthreads();
+    // the final offset of every digit arrives from this tile's group's
+    // prefix block; only this tile's words are polled
 #pragma unroll
-      for (int k = 0; k < DPT; ++k) {
-        const int d = tid + k * kSortThreads;
-        self_pre[k] = 0;
-        if (d < ND) {
-          uint32_t pk[kPrefixGroup / 2];
-          group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, &a.hdr->error, pk, self_pre[k]);
-#pragma unroll
-          for (int j = 0; j < kPrefixGroup / 2; ++j) s_pre[j * ND + d] = pk[j];
-        }
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      excl[k] = 0;
+      if (d < ND) {
+        uint64_t fv[1] = {ld_acquire_u64(a.status + (size_t)tile * a.status_stride + d)};
+        poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, &a.hdr->error, fv);
+        excl[k] = (uint32_t)fv[0];
       }
+    }
+    // the final offsets replace the digit bases
 #pragma unroll
-      for (int k = 0; k < DPT; ++k) {
-        const int d = tid + k * kSortThreads;
-        excl[k] = 0;
-        if (d < ND) {
-          uint32_t total = 0;
-          group_sums(a.grp, a.status_stride, g, ngroups, d, tag, &a.hdr->error, excl[k], total);
-          s_gbase[d] = total;
-        }
-      }
-      __syncthreads();
-      block_excl_scan<RB>(s_gbase, s_wsum);
-#pragma unroll
-      for (int k = 0; k < DPT; ++k) {
-        const int d = tid + k * kSortThreads;
-        if (d < ND) {
-          const uint32_t gb = s_gbase[d] + excl[k];
-#pragma unroll
-          for (int i = 0; i < kPrefixGroup; ++i) {
-            const uint32_t pre = (s_pre[(i / 2) * ND + d] >> (16 * (i % 2))) & 0xffffu;
-            if (g0 + i < g1 - 1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, tag_hi | (gb + pre));
-          }
-          excl[k] += self_pre[k];
-        }
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < DPT; ++k) {
-        const int d = tid + k * kSortThreads;
-        excl[k] = 0;
-        if (d < ND) {
-          uint64_t fv[1] = {ld_acquire_u64(a.status + (size_t)tile * a.status_stride + d)};
-          poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, &a.hdr->error, fv);
-          excl[k] = (uint32_t)fv[0];
-        }
-      }
-      // the final offsets replace the digit bases
-#pragma unroll
-      for (int k = 0; k < DPT; ++k) {
-        const int d = tid + k * kSortThreads;
-        if (d < ND) s_gbase[d] = 0;
-      }
+    for (int k = 0; k < DPT; ++k) {
+      const int d = tid + k * kSortThreads;
+      if (d < ND) s_gbase[d] = 0;
     }
   } else {
     uint64_t* st = a.status + (size_t)tile * a.status_stride;
@@ -857,10 +871,12 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   // every tile of a pass resident at once: tile = block index, bags found by
   // the first pass, two-level published-count prefix; otherwise a prepare
   // kernel (bags, keys, digit totals), tickets and a look-back
+  // (a co-resident pass also runs one prefix block per group of kPrefixGroup tiles)
   const int core_tiles = (N + kSortTileMin - 1) / kSortTileMin;
+  const int core_blocks = core_tiles + (core_tiles + kPrefixGroup - 1) / kPrefixGroup;
   int sort_cores = 1;
   for (int i = 0; i < p.plan.passes; ++i)
-    if (core_tiles > resident_blocks(pass_kernel_bits<kSortItemsCore>(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
+    if (core_blocks > resident_blocks(pass_kernel_bits<kSortItemsCore>(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
   const int tile_keys = kSortThreads * (sort_cores ? kSortItemsCore : kSortItemsWide);
   const int sort_tiles = (N + tile_keys - 1) / tile_keys;
   const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
@@ -932,7 +948,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.bits = p.plan.bits[ps];
     xa.pass = ps;
     xa.status_stride = status_stride;
-    e = sort_cores ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles, s)
+    e = sort_cores ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles + (sort_tiles + kPrefixGroup - 1) / kPrefixGroup, s)
                    : launch_pass_bits<kSortItemsWide>(xa, sort_tiles, s);
     if (e != hipSuccess) return e;
     kin = xa.keys_out;

@@ -7,7 +7,9 @@
 // gathers 64/G rows; each group walks its share of the bag with UNROLL rows
 // in flight, accumulating in fp32.  The groups are summed with a butterfly at
 // the end and group 0 stores the pooled row.  Ids of the bag are read 64 at a
-// time with one coalesced load and handed to the groups by lane shuffles.
+// time with one coalesced load; repeated ids of such a chunk are merged (one
+// row load, added with its multiplicity) and the distinct ids are handed to
+// the groups by lane shuffles.
 #include "emb_common.h"
 #include "kernels.h"
 
@@ -69,14 +71,42 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
 
   for (int j0 = start; j0 < end; j0 += kWave) {
     const int n = min(kWave, end - j0);
-    const int my_id = lane < n ? idx[j0 + lane] : 0;
-    for (int i0 = 0; i0 < n; i0 += RPI * UN) {
-      float row[UN][NV][E];
+    const bool valid = lane < n;
+    const int my_id = valid ? idx[j0 + lane] : 0;
+    // Skewed ids repeat within a bag: each distinct id of the chunk is loaded
+    // once and added with its multiplicity.  Lanes are classed by an 8-bit
+    // hash of the id (one ballot per hash bit); a lane whose id equals the
+    // lowest lane of its class is a duplicate of it, every other lane (the
+    // lowest lane itself, or a hash collision) loads its own row.
+    const uint32_t h = ((uint32_t)my_id * 0x9E3779B1u) >> 24;
+    uint64_t cls = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const bool bit = (h >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      cls &= bit ? bb : ~bb;
+    }
+    const int lead = valid ? (int)__builtin_ctzll(cls) : lane;
+    // (the shuffle runs on every lane: a lane switched off does not supply its value)
+    const int lead_id = __shfl(my_id, lead, kWave);
+    const bool dup = valid && lead != lane && lead_id == my_id;
+    const uint64_t dups = __ballot(dup);
+    const bool loader = valid && !dup;
+    const uint64_t lm = __ballot(loader);
+    const int nu = (int)__popcll(lm);
+    // compact the loaders' (id, multiplicity) into lanes 0..nu-1
+    const int dst = loader ? (int)lanes_below(lm) : nu + (int)lanes_below(~lm);
+    const int mult = loader ? 1 + (int)__popcll(dups & cls) * (lead == lane) : 0;
+    const int c_id = __builtin_amdgcn_ds_permute(dst * 4, my_id);
+    const int c_mult = __builtin_amdgcn_ds_permute(dst * 4, mult);
+    for (int i0 = 0; i0 < nu; i0 += RPI * UN) {
+      float row[UN][NV][E], wt[UN];
 #pragma unroll
       for (int u = 0; u < UN; ++u) {
         const int s = i0 + u * RPI + g;
-        const int id = __shfl(my_id, s & (kWave - 1), kWave);
-        if (s < n) {
+        const int id = __shfl(c_id, s & (kWave - 1), kWave);
+        wt[u] = (float)__shfl(c_mult, s & (kWave - 1), kWave);
+        if (s < nu) {
           const TW* rp = W + (size_t)(base + (uint32_t)id) * (size_t)D;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
@@ -87,18 +117,20 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
               for (int e = 0; e < E; ++e) row[u][v][e] = 0.f;
           }
         } else {
+          wt[u] = 0.f;
 #pragma unroll
           for (int v = 0; v < NV; ++v)
 #pragma unroll
             for (int e = 0; e < E; ++e) row[u][v][e] = 0.f;
         }
       }
+      // a row of multiplicity 1 is added exactly as a plain sum would add it
 #pragma unroll
       for (int u = 0; u < UN; ++u)
 #pragma unroll
         for (int v = 0; v < NV; ++v)
 #pragma unroll
-          for (int e = 0; e < E; ++e) acc[v][e] += row[u][v][e];
+          for (int e = 0; e < E; ++e) acc[v][e] = __builtin_fmaf(wt[u], row[u][v][e], acc[v][e]);
     }
   }
 

@@ -143,9 +143,24 @@ struct PassArgs {
   uint64_t* uniq_status;
   int32_t uniq_tiles;
   int32_t N, ntiles, shift, bits, pass, status_stride;
-  int32_t coresident;      // 1: every tile is resident at once (tile = block index, two-level prefix;
-                           //    digit totals come from the published counts, not from `totals`)
+  int32_t coresident;      // 1: every tile is resident at once (tile = block index, prefix blocks
+                           //    after the tiles publish each tile's final digit offsets)
+  int32_t prefix_mode;     // co-resident: kPrefixGroups or kPrefixRanges
+  // first co-resident pass: the later passes' digit counts are published in
+  // `later` [tiles][kMaxPasses - 1][status_stride] and summed into their
+  // totals (`totals_all` [kMaxPasses][kMaxDigits]) by the prefix blocks
+  uint64_t* later;
+  uint32_t* totals_all;
+  int32_t npass;
+  int32_t pass_shift[kMaxPasses], pass_bits[kMaxPasses];
 };
+
+// Prefix blocks of a co-resident pass.  Groups: one block per kPrefixGroup
+// tiles, digit totals found from the tiles' counts (three exchanges through
+// memory: counts, group sums, final offsets).  Ranges: one block per
+// kRangeDigits digits over all tiles, with digit totals known before the pass
+// (two exchanges: counts, final offsets).
+constexpr int kPrefixGroups = 1, kPrefixRanges = 2;
 
 // Exclusive scan of n = 2^RB counters held in LDS, by kSortThreads threads.
 template <int RB>
@@ -305,20 +320,46 @@ __device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int 
 // that tile's status word.  The tiles rank and reorder their keys meanwhile.
 template <int RB>
 __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t tag, uint32_t* s_base,
-                                                  uint32_t* s_wsum) {
+                                                  uint32_t* s_wsum, uint32_t* s_pre) {
   constexpr int ND = 1 << RB;
   constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
   const int tid = threadIdx.x;
   const int g = blockIdx.x - a.ntiles, g0 = g * kPrefixGroup;
   const int g1 = min(a.ntiles, g0 + kPrefixGroup);
   const int ngroups = (a.ntiles + kPrefixGroup - 1) / kPrefixGroup;
-  uint32_t pk[DPT][kPrefixGroup / 2], excl[DPT];
+  uint32_t excl[DPT];
+  // the in-group prefixes (16-bit pairs) wait in LDS: s_pre[j * ND + d]
 #pragma unroll
   for (int k = 0; k < DPT; ++k) {
     const int d = tid + k * kSortThreads;
     if (d < ND) {
-      uint32_t unused;
-      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, &a.hdr->error, pk[k], unused);
+      uint32_t pk[kPrefixGroup / 2], unused;
+      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, &a.hdr->error, pk, unused);
+#pragma unroll
+      for (int j = 0; j < kPrefixGroup / 2; ++j) s_pre[j * ND + d] = pk[j];
+    }
+  }
+  if (a.later) {
+    // while the other groups' sums arrive: this group's counts of the later
+    // passes' digits are added to their totals
+    const size_t lstride = (size_t)(kMaxPasses - 1) * a.status_stride;
+    for (int p = 1; p < a.npass; ++p) {
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        if (d < (1 << a.pass_bits[p])) {
+          const uint64_t* lb = a.later + (size_t)(p - 1) * a.status_stride;
+          uint64_t v[kPrefixGroup];
+          const int n = g1 - g0;
+#pragma unroll
+          for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(lb + (size_t)(g0 + i) * lstride + d) : 0;
+          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, &a.hdr->error, v);
+          uint32_t sum = 0;
+#pragma unroll
+          for (int i = 0; i < kPrefixGroup; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
+          if (sum) atomic_add_u32(&a.totals_all[p * kMaxDigits + d], sum);
+        }
+      }
     }
   }
 #pragma unroll
@@ -341,9 +382,57 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
       const uint32_t gb = s_base[d] + excl[k];
 #pragma unroll
       for (int i = 0; i < kPrefixGroup; ++i) {
-        const uint32_t pre = (pk[k][i / 2] >> (16 * (i % 2))) & 0xffffu;
+        const uint32_t pre = (s_pre[(i / 2) * ND + d] >> (16 * (i % 2))) & 0xffffu;
         if (g0 + i < g1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, tag_hi | (gb + pre));
       }
+    }
+  }
+}
+
+// A digit-range prefix block (passes after the first, co-resident): block b
+// owns digits [b*DB, (b+1)*DB) of every tile.  The digit bases come from the
+// totals counted during the first pass; a thread sums one digit's published
+// counts over a chunk of consecutive tiles, the chunk sums are scanned in LDS,
+// and the thread publishes the final offset of its digit for each tile of its
+// chunk.
+template <int RB>
+__device__ __forceinline__ void sort_prefix_range(const PassArgs& a, uint32_t tag, uint32_t* s_base,
+                                                  uint32_t* s_wsum, uint32_t* s_cs) {
+  constexpr int ND = 1 << RB;
+  constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
+  constexpr int DB = ND < kRangeDigits ? ND : kRangeDigits;
+  constexpr int NC = kSortThreads / DB;
+  const int tid = threadIdx.x;
+  const int dl = tid % DB, c = tid / DB;
+  const int d = (blockIdx.x - a.ntiles) * DB + dl;
+  const int ct = (a.ntiles + NC - 1) / NC;  // at most kRangeTiles (checked by the host)
+  const int t0 = c * ct, n = max(0, min(a.ntiles - t0, ct));
+  // the digit bases, found while the tiles load their keys
+#pragma unroll
+  for (int k = 0; k < DPT; ++k) {
+    const int dd = tid + k * kSortThreads;
+    if (dd < ND) s_base[dd] = a.totals[dd];
+  }
+  __syncthreads();
+  block_excl_scan<RB>(s_base, s_wsum);
+  // this digit's counts in the chunk's tiles
+  uint64_t v[kRangeTiles];
+#pragma unroll
+  for (int i = 0; i < kRangeTiles; ++i) v[i] = i < n ? ld_acquire_u64(a.rows + (size_t)(t0 + i) * a.status_stride + d) : 0;
+  poll_batch<kRangeTiles>(a.rows, a.status_stride, t0, n, d, tag, &a.hdr->error, v);
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < kRangeTiles; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
+  s_cs[c * DB + dl] = sum;
+  __syncthreads();
+  uint32_t run = s_base[d];
+  for (int cc = 0; cc < c; ++cc) run += s_cs[cc * DB + dl];
+  const uint64_t tag_hi = (uint64_t)tag << 32;
+#pragma unroll
+  for (int i = 0; i < kRangeTiles; ++i) {
+    if (i < n) {
+      st_u64(a.status + (size_t)(t0 + i) * a.status_stride + d, tag_hi | run);
+      run += (uint32_t)v[i];
     }
   }
 }
@@ -470,7 +559,8 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   // the call's tag: the header's generation advances once per call, at its end
   const uint32_t tag = 0x80000000u | ((a.hdr->gen + 1u) * 8u + (uint32_t)a.pass);
   if (a.coresident && (int)blockIdx.x >= a.ntiles) {
-    sort_prefix_block<RB>(a, tag, s_gbase, s_wsum);
+    if (a.prefix_mode == kPrefixRanges) sort_prefix_range<RB>(a, tag, s_gbase, s_wsum, s_keys);
+    else sort_prefix_block<RB>(a, tag, s_gbase, s_wsum, &s_cnt[0][0]);
     return;
   }
   const int64_t wbase = (int64_t)tile * TILE + w * (kWave * IT);
@@ -483,43 +573,26 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       a.uniq_status[i] = 0;
     if (blockIdx.x == 0 && tid == 0) a.hdr->ticket[kSlotUnique] = 0u;
   }
-  if (a.search_bags) {
-    // the ids are loaded first: their loads overlap the bag search
-#pragma unroll
-    for (int i = 0; i < IT; ++i) {
-      const int64_t pos = wbase + i * kWave + lane;
-      key[i] = pos < a.N ? (uint32_t)a.idx[pos] : 0u;
-      val[i] = pos < a.N ? (int32_t)pos : 0;
-    }
-    find_tile_bags<IT>(a, tile, s_boff, s_lohi, s_bags, s_wsum, bag);
-    if (a.T > 1) {
-#pragma unroll
-      for (int i = 0; i < IT; ++i) key[i] += s_toff[bag[i] / a.B];
-    }
-#pragma unroll
-    for (int i = 0; i < IT; ++i) dig[i] = (key[i] >> a.shift) & mask;
-  } else {
-#pragma unroll
-    for (int i = 0; i < IT; ++i) {
-      const int64_t pos = wbase + i * kWave + lane;
-      const bool valid = pos < a.N;
-      key[i] = valid ? a.keys_in[pos] : 0u;
-      val[i] = valid ? (a.vals_in ? a.vals_in[pos] : (int32_t)pos) : 0;
-      bag[i] = valid ? a.bags_in[pos] : 0;
-      dig[i] = (key[i] >> a.shift) & mask;
-    }
-  }
-
-  // The tile's digit counts are published first (from an LDS histogram), so
-  // that the other tiles' prefixes advance while this tile ranks and reorders
-  // its keys.
-#pragma unroll
-  for (int i = 0; i < IT; ++i)
-    if (wbase + i * kWave + lane < a.N) atomicAdd(&s_hist[dig[i]], 1u);
-  __syncthreads();
+  // The tile's digit counts are published as soon as its digits are known
+  // (from an LDS histogram), so that the other tiles' prefixes advance while
+  // this tile finds its bags, ranks and reorders its keys.
   const uint64_t tag_hi = (uint64_t)tag << 32;
   uint32_t my_cnt[DPT];
-  {
+  auto publish_counts = [&]() {
+#pragma unroll
+    for (int i = 0; i < IT; ++i)
+      if (wbase + i * kWave + lane < a.N) atomicAdd(&s_hist[dig[i]], 1u);
+    if (a.later) {
+      // the later passes' digits too (counted in s_cnt, which stays zero
+      // until the ranking)
+      for (int p = 1; p < a.npass; ++p) {
+        const uint32_t pm = (1u << a.pass_bits[p]) - 1u;
+#pragma unroll
+        for (int i = 0; i < IT; ++i)
+          if (wbase + i * kWave + lane < a.N) atomicAdd(&s_cnt[p - 1][(key[i] >> a.pass_shift[p]) & pm], 1u);
+      }
+    }
+    __syncthreads();
     uint64_t* row = a.coresident ? a.rows + (size_t)tile * a.status_stride
                                  : a.status + (size_t)tile * a.status_stride;
     const uint64_t flag = a.coresident ? 0 : ((tile == 0 ? kFlagInc : kFlagAgg) << 30);
@@ -532,6 +605,56 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
         st_u64(row + d, tag_hi | flag | my_cnt[k]);
       }
     }
+    if (a.later) {
+      for (int p = 1; p < a.npass; ++p) {
+        uint64_t* lrow = a.later + ((size_t)tile * (kMaxPasses - 1) + (p - 1)) * a.status_stride;
+#pragma unroll
+        for (int k = 0; k < DPT; ++k) {
+          const int d = tid + k * kSortThreads;
+          if (d < (1 << a.pass_bits[p])) st_u64(lrow + d, tag_hi | s_cnt[p - 1][d]);
+        }
+      }
+      __syncthreads();
+      for (int i = tid; i < (a.npass - 1) * ND; i += kSortThreads) (&s_cnt[0][0])[i] = 0u;
+      __syncthreads();
+    }
+  };
+
+  if (a.search_bags) {
+    // the ids are loaded first: their loads overlap the bag search
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      const int64_t pos = wbase + i * kWave + lane;
+      key[i] = pos < a.N ? (uint32_t)a.idx[pos] : 0u;
+      val[i] = pos < a.N ? (int32_t)pos : 0;
+    }
+    // with one table the ids are the keys: the counts go out before the bag search
+    const bool one_table = a.T == 1;
+    if (one_table) {
+#pragma unroll
+      for (int i = 0; i < IT; ++i) dig[i] = (key[i] >> a.shift) & mask;
+      publish_counts();
+    }
+    find_tile_bags<IT>(a, tile, s_boff, s_lohi, s_bags, s_wsum, bag);
+    if (!one_table) {
+#pragma unroll
+      for (int i = 0; i < IT; ++i) {
+        key[i] += s_toff[bag[i] / a.B];
+        dig[i] = (key[i] >> a.shift) & mask;
+      }
+      publish_counts();
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      const int64_t pos = wbase + i * kWave + lane;
+      const bool valid = pos < a.N;
+      key[i] = valid ? a.keys_in[pos] : 0u;
+      val[i] = valid ? (a.vals_in ? a.vals_in[pos] : (int32_t)pos) : 0;
+      bag[i] = valid ? a.bags_in[pos] : 0;
+      dig[i] = (key[i] >> a.shift) & mask;
+    }
+    publish_counts();
   }
 
   // rank each element among the earlier elements of its wave with its digit
@@ -666,6 +789,8 @@ __device__ __forceinline__ uint64_t pack_uniq(uint64_t flag, uint32_t c, uint32_
   return (flag << 62) | ((uint64_t)c << 31) | (uint64_t)q;
 }
 
+constexpr int kUniqWindows = 4;  // look-back words per lane and round
+
 __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   constexpr int NW = kUniqThreads / kWave;
   __shared__ uint32_t s_keys[kUniqTile];
@@ -731,7 +856,10 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     tile_q = max(tile_q, s_wq[ww]);
   }
   if (w == 0) {
-    // wave-parallel look-back: lane k reads the status of tile (j - k)
+    // wave-parallel look-back: in a round, lane k reads the status of tiles
+    // j - k - 64 i for i < kUniqWindows (one round trip for all of them); the
+    // windows are then taken in order up to the first word not yet published
+    // or the first inclusive prefix
     uint32_t pc = 0, pq = 0;
     if (tile == 0) {
       if (lane == 0) st_u64(a.status, pack_uniq(kFlagInc, tile_c, tile_q));
@@ -740,19 +868,33 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
       int j = tile - 1;
       uint32_t spins = 0;
       while (true) {
-        const int jj = j - lane;
-        const uint64_t sv = jj >= 0 ? ld_acquire_u64(a.status + jj) : 0;
-        const uint64_t flag = sv >> 62;
-        const uint64_t not_ready = __ballot(!(jj >= 0 && flag != 0));
-        const uint64_t inc = __ballot(jj >= 0 && flag == kFlagInc);
-        const int first_nr = not_ready ? __builtin_ctzll(not_ready) : kWave;
-        const int first_inc = inc ? __builtin_ctzll(inc) : kWave;
-        const bool done = first_inc < first_nr;
-        const int take = done ? first_inc + 1 : first_nr;
+        uint64_t sv[kUniqWindows];
+#pragma unroll
+        for (int i = 0; i < kUniqWindows; ++i) {
+          const int jj = j - i * kWave - lane;
+          sv[i] = jj >= 0 ? ld_acquire_u64(a.status + jj) : 0;
+        }
         uint32_t c = 0, q = 0;
-        if (lane < take) {
-          c = (uint32_t)((sv >> 31) & 0x7fffffffu);
-          q = (uint32_t)(sv & 0x7fffffffu);
+        int took = 0;
+        bool done = false, stop = false;
+#pragma unroll
+        for (int i = 0; i < kUniqWindows; ++i) {
+          if (!stop) {
+            const int jj = j - i * kWave - lane;
+            const uint64_t flag = sv[i] >> 62;
+            const uint64_t not_ready = __ballot(!(jj >= 0 && flag != 0));
+            const uint64_t inc = __ballot(jj >= 0 && flag == kFlagInc);
+            const int first_nr = not_ready ? __builtin_ctzll(not_ready) : kWave;
+            const int first_inc = inc ? __builtin_ctzll(inc) : kWave;
+            done = first_inc < first_nr;
+            const int take = done ? first_inc + 1 : first_nr;
+            if (lane < take) {
+              c += (uint32_t)((sv[i] >> 31) & 0x7fffffffu);
+              q = max(q, (uint32_t)(sv[i] & 0x7fffffffu));
+            }
+            took += take;
+            stop = done || take < kWave;
+          }
         }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
@@ -763,8 +905,8 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
         pc += c;
         pq = max(pq, q);
         if (done) break;
-        j -= take;
-        if (take == 0) {
+        j -= took;
+        if (took == 0) {
           if (++spins > kSpinLimit) {
             if (lane == 0) atomicOr(&a.hdr->error, 1u);
             break;
@@ -871,12 +1013,28 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   // every tile of a pass resident at once: tile = block index, bags found by
   // the first pass, two-level published-count prefix; otherwise a prepare
   // kernel (bags, keys, digit totals), tickets and a look-back
-  // (a co-resident pass also runs one prefix block per group of kPrefixGroup tiles)
+  // A co-resident pass also runs its prefix blocks after the tiles: one per
+  // group of kPrefixGroup tiles for the first pass, one per kRangeDigits
+  // digits for the later ones (their digit totals are counted during the
+  // first pass), unless the tiles are too many for a range block's threads
+  // or the digits do not shrink from pass to pass.
   const int core_tiles = (N + kSortTileMin - 1) / kSortTileMin;
-  const int core_blocks = core_tiles + (core_tiles + kPrefixGroup - 1) / kPrefixGroup;
+  const int core_groups = (core_tiles + kPrefixGroup - 1) / kPrefixGroup;
+  int ranges = p.plan.passes > 1 ? 1 : 0;
+  for (int i = 1; i < p.plan.passes; ++i) {
+    const int nd = 1 << p.plan.bits[i];
+    const int db = nd < kRangeDigits ? nd : kRangeDigits;
+    if (p.plan.bits[i] > p.plan.bits[0] || core_tiles > (kSortThreads / db) * kRangeTiles) ranges = 0;
+  }
+  auto prefix_blocks = [&](int ps) {
+    if (ps == 0 || !ranges) return core_groups;
+    const int nd = 1 << p.plan.bits[ps];
+    return nd / (nd < kRangeDigits ? nd : kRangeDigits);
+  };
   int sort_cores = 1;
   for (int i = 0; i < p.plan.passes; ++i)
-    if (core_blocks > resident_blocks(pass_kernel_bits<kSortItemsCore>(p.plan.bits[i]), kSortThreads)) sort_cores = 0;
+    if (core_tiles + prefix_blocks(i) > resident_blocks(pass_kernel_bits<kSortItemsCore>(p.plan.bits[i]), kSortThreads))
+      sort_cores = 0;
   const int tile_keys = kSortThreads * (sort_cores ? kSortItemsCore : kSortItemsWide);
   const int sort_tiles = (N + tile_keys - 1) / tile_keys;
   const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
@@ -932,6 +1090,14 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.rows = reinterpret_cast<uint64_t*>(back + L.rows);
     xa.grp = reinterpret_cast<uint64_t*>(back + L.grp);
     xa.coresident = sort_cores;
+    xa.prefix_mode = (sort_cores && ranges && ps > 0) ? kPrefixRanges : kPrefixGroups;
+    xa.later = (sort_cores && ranges && ps == 0) ? reinterpret_cast<uint64_t*>(back + L.later) : nullptr;
+    xa.totals_all = reinterpret_cast<uint32_t*>(ws + L.totals);
+    xa.npass = p.plan.passes;
+    for (int i = 0; i < kMaxPasses; ++i) {
+      xa.pass_shift[i] = p.plan.shift[i];
+      xa.pass_bits[i] = p.plan.bits[i];
+    }
     xa.search_bags = sort_cores && ps == 0;
     xa.offsets = p.offsets;
     xa.idx = p.idx;
@@ -948,7 +1114,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.bits = p.plan.bits[ps];
     xa.pass = ps;
     xa.status_stride = status_stride;
-    e = sort_cores ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles + (sort_tiles + kPrefixGroup - 1) / kPrefixGroup, s)
+    e = sort_cores ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles + prefix_blocks(ps), s)
                    : launch_pass_bits<kSortItemsWide>(xa, sort_tiles, s);
     if (e != hipSuccess) return e;
     kin = xa.keys_out;

@@ -33,6 +33,10 @@ constexpr int kUniqTile = kUniqThreads * kUniqItems;
 constexpr int kLookbackWindow = 8;
 // tiles per group of the two-level prefix used when all tiles are resident
 constexpr int kPrefixGroup = 16;
+// digit-range prefix blocks (passes after the first, co-resident): digits per
+// block, and the most tiles one of its threads sums
+constexpr int kRangeDigits = 16;
+constexpr int kRangeTiles = 16;
 // bag offsets a first-pass tile stages in LDS to find the bag of each position
 constexpr int kBagStage = 2048;
 
@@ -80,7 +84,7 @@ struct WsLayout {
   size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_keys, sorted_bag, uniq_status,
       chunk_seg, partials, level2, arrivals, front;
   // back (offsets from the back base)
-  size_t pass_status, rows, grp, back;
+  size_t pass_status, rows, grp, later, back;
   size_t total;
   int64_t sort_tiles, uniq_tiles, chunks, groups, combine_blocks;
 };
@@ -140,6 +144,8 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   b = align256(b + sizeof(uint64_t) * L.sort_tiles * kMaxDigits);
   L.grp = b;
   b = align256(b + sizeof(uint64_t) * L.groups * kMaxDigits);
+  L.later = b;
+  b = align256(b + sizeof(uint64_t) * L.sort_tiles * (kMaxPasses - 1) * kMaxDigits);
   L.back = b;
   L.total = L.front + L.back;
   return L;

@@ -339,29 +339,6 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
       for (int j = 0; j < kPrefixGroup / 2; ++j) s_pre[j * ND + d] = pk[j];
     }
   }
-  if (a.later) {
-    // while the other groups' sums arrive: this group's counts of the later
-    // passes' digits are added to their totals
-    const size_t lstride = (size_t)(kMaxPasses - 1) * a.status_stride;
-    for (int p = 1; p < a.npass; ++p) {
-#pragma unroll
-      for (int k = 0; k < DPT; ++k) {
-        const int d = tid + k * kSortThreads;
-        if (d < (1 << a.pass_bits[p])) {
-          const uint64_t* lb = a.later + (size_t)(p - 1) * a.status_stride;
-          uint64_t v[kPrefixGroup];
-          const int n = g1 - g0;
-#pragma unroll
-          for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(lb + (size_t)(g0 + i) * lstride + d) : 0;
-          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, &a.hdr->error, v);
-          uint32_t sum = 0;
-#pragma unroll
-          for (int i = 0; i < kPrefixGroup; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
-          if (sum) atomic_add_u32(&a.totals_all[p * kMaxDigits + d], sum);
-        }
-      }
-    }
-  }
 #pragma unroll
   for (int k = 0; k < DPT; ++k) {
     const int d = tid + k * kSortThreads;
@@ -384,6 +361,29 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
       for (int i = 0; i < kPrefixGroup; ++i) {
         const uint32_t pre = (s_pre[(i / 2) * ND + d] >> (16 * (i % 2))) & 0xffffu;
         if (g0 + i < g1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, tag_hi | (gb + pre));
+      }
+    }
+  }
+  if (a.later) {
+    // after the final offsets are out: this group's counts of the later
+    // passes' digits are added to their totals
+    const size_t lstride = (size_t)(kMaxPasses - 1) * a.status_stride;
+    const int n = g1 - g0;
+    for (int p = 1; p < a.npass; ++p) {
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) {
+        const int d = tid + k * kSortThreads;
+        if (d < (1 << a.pass_bits[p])) {
+          const uint64_t* lb = a.later + (size_t)(p - 1) * a.status_stride;
+          uint64_t v[kPrefixGroup];
+#pragma unroll
+          for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(lb + (size_t)(g0 + i) * lstride + d) : 0;
+          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, &a.hdr->error, v);
+          uint32_t sum = 0;
+#pragma unroll
+          for (int i = 0; i < kPrefixGroup; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
+          if (sum) atomic_add_u32(&a.totals_all[p * kMaxDigits + d], sum);
+        }
       }
     }
   }
@@ -582,16 +582,6 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
 #pragma unroll
     for (int i = 0; i < IT; ++i)
       if (wbase + i * kWave + lane < a.N) atomicAdd(&s_hist[dig[i]], 1u);
-    if (a.later) {
-      // the later passes' digits too (counted in s_cnt, which stays zero
-      // until the ranking)
-      for (int p = 1; p < a.npass; ++p) {
-        const uint32_t pm = (1u << a.pass_bits[p]) - 1u;
-#pragma unroll
-        for (int i = 0; i < IT; ++i)
-          if (wbase + i * kWave + lane < a.N) atomicAdd(&s_cnt[p - 1][(key[i] >> a.pass_shift[p]) & pm], 1u);
-      }
-    }
     __syncthreads();
     uint64_t* row = a.coresident ? a.rows + (size_t)tile * a.status_stride
                                  : a.status + (size_t)tile * a.status_stride;
@@ -606,6 +596,15 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       }
     }
     if (a.later) {
+      // then the later passes' digits (counted in s_cnt, which stays zero
+      // until the ranking)
+      for (int p = 1; p < a.npass; ++p) {
+        const uint32_t pm = (1u << a.pass_bits[p]) - 1u;
+#pragma unroll
+        for (int i = 0; i < IT; ++i)
+          if (wbase + i * kWave + lane < a.N) atomicAdd(&s_cnt[p - 1][(key[i] >> a.pass_shift[p]) & pm], 1u);
+      }
+      __syncthreads();
       for (int p = 1; p < a.npass; ++p) {
         uint64_t* lrow = a.later + ((size_t)tile * (kMaxPasses - 1) + (p - 1)) * a.status_stride;
 #pragma unroll

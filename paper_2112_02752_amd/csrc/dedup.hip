@@ -814,11 +814,17 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   __syncthreads();
   const int tile = s_tile;
   const int64_t tbase = (int64_t)tile * kUniqTile;
-  for (int s = tid; s < kUniqTile; s += kUniqThreads) {
-    const int64_t pos = tbase + s;
-    s_keys[s] = pos < a.N ? a.skeys[pos] : 0u;
+  // every load of the tile is issued before the first LDS store
+  uint32_t kv[kUniqItems];
+#pragma unroll
+  for (int i = 0; i < kUniqItems; ++i) {
+    const int64_t pos = tbase + tid + i * kUniqThreads;
+    kv[i] = pos < a.N ? a.skeys[pos] : 0u;
   }
-  if (tid == 0) s_prev = tbase > 0 ? a.skeys[tbase - 1] : 0u;
+  const uint32_t before = (tid == 0 && tbase > 0) ? a.skeys[tbase - 1] : 0u;
+#pragma unroll
+  for (int i = 0; i < kUniqItems; ++i) s_keys[tid + i * kUniqThreads] = kv[i];
+  if (tid == 0) s_prev = before;
   __syncthreads();
 
   uint32_t c = 0, q = 0, heads = 0;

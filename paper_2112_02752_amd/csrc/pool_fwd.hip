@@ -20,24 +20,26 @@ namespace {
 template <typename TW>
 struct Vec;  // 16 bytes of table row, widened to fp32
 
+// (loaded raw, widened where it is used, so that every load of a round is
+// issued before the first one is waited for)
 template <>
 struct Vec<float> {
   static constexpr int kElems = 4;
-  __device__ __forceinline__ static void load(const float* p, float (&o)[4]) {
-    float4 v = *reinterpret_cast<const float4*>(p);
-    o[0] = v.x;
-    o[1] = v.y;
-    o[2] = v.z;
-    o[3] = v.w;
+  __device__ __forceinline__ static uint4 load(const float* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ static void widen(const uint4& v, float (&o)[4]) {
+    o[0] = __uint_as_float(v.x);
+    o[1] = __uint_as_float(v.y);
+    o[2] = __uint_as_float(v.z);
+    o[3] = __uint_as_float(v.w);
   }
 };
 
 template <>
 struct Vec<uint16_t> {
   static constexpr int kElems = 8;
-  __device__ __forceinline__ static void load(const uint16_t* p, float (&o)[8]) {
-    uint4 v = *reinterpret_cast<const uint4*>(p);
-    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  __device__ __forceinline__ static uint4 load(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ static void widen(const uint4& v, float (&o)[8]) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       o[2 * i] = __uint_as_float(w[i] << 16);
@@ -54,7 +56,7 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
                                                   int32_t M, int32_t D, int32_t pool, float* __restrict__ out) {
   constexpr int RPI = kWave / G;
   constexpr int E = Vec<TW>::kElems;
-  constexpr int UN = unroll_for(RPI);
+  constexpr int UN = unroll_for(RPI) / NV > 0 ? unroll_for(RPI) / NV : 1;  // rows in flight per lane group
   const int lane = threadIdx.x & (kWave - 1);
   // the bag is uniform across the wavefront: keep its bookkeeping scalar
   const int m = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWave) + (threadIdx.x >> 6));
@@ -100,37 +102,36 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
     const int c_id = __builtin_amdgcn_ds_permute(dst * 4, my_id);
     const int c_mult = __builtin_amdgcn_ds_permute(dst * 4, mult);
     for (int i0 = 0; i0 < nu; i0 += RPI * UN) {
-      float row[UN][NV][E], wt[UN];
+      // every row load of the round is issued before the first is used (the
+      // raw 16 bytes are widened afterwards); unused slots load nothing and
+      // are dropped by a select below
+      uint4 raw[UN][NV];
+      float wt[UN];  // multiplicity; 0 marks an unused slot
 #pragma unroll
       for (int u = 0; u < UN; ++u) {
         const int s = i0 + u * RPI + g;
         const int id = __shfl(c_id, s & (kWave - 1), kWave);
-        wt[u] = (float)__shfl(c_mult, s & (kWave - 1), kWave);
-        if (s < nu) {
-          const TW* rp = W + (size_t)(base + (uint32_t)id) * (size_t)D;
+        const int mu = __shfl(c_mult, s & (kWave - 1), kWave);
+        wt[u] = s < nu ? (float)mu : 0.f;
+        const TW* rp = W + (size_t)(base + (uint32_t)id) * (size_t)D;
 #pragma unroll
-          for (int v = 0; v < NV; ++v) {
-            const int c0 = (v * G + sub) * E;
-            if (c0 < D) Vec<TW>::load(rp + c0, row[u][v]);
-            else
-#pragma unroll
-              for (int e = 0; e < E; ++e) row[u][v][e] = 0.f;
-          }
-        } else {
-          wt[u] = 0.f;
-#pragma unroll
-          for (int v = 0; v < NV; ++v)
-#pragma unroll
-            for (int e = 0; e < E; ++e) row[u][v][e] = 0.f;
+        for (int v = 0; v < NV; ++v) {
+          const int c0 = (v * G + sub) * E;
+          raw[u][v] = make_uint4(0u, 0u, 0u, 0u);
+          if (s < nu && c0 < D) raw[u][v] = Vec<TW>::load(rp + c0);
         }
       }
       // a row of multiplicity 1 is added exactly as a plain sum would add it
 #pragma unroll
       for (int u = 0; u < UN; ++u)
 #pragma unroll
-        for (int v = 0; v < NV; ++v)
+        for (int v = 0; v < NV; ++v) {
+          const bool use = wt[u] != 0.f && (v * G + sub) * E < D;
+          float x[E];
+          Vec<TW>::widen(raw[u][v], x);
 #pragma unroll
-          for (int e = 0; e < E; ++e) acc[v][e] = __builtin_fmaf(wt[u], row[u][v][e], acc[v][e]);
+          for (int e = 0; e < E; ++e) acc[v][e] = use ? __builtin_fmaf(wt[u], x[e], acc[v][e]) : acc[v][e];
+        }
     }
   }
 

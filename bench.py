@@ -5,9 +5,12 @@ id dedup (sort + unique), gradient segment-reduce fused with the row-wise
 Adagrad / SGD update.  Inputs (tables, optimizer state, all batches and
 upstream gradients) are resident in HBM before the timed region starts.
 
-Prints ONE JSON line.  `value` is pooled lookups per second of whole steps;
-`roofline` prices the phase that takes the most time (measured live with HIP
-events on the launch stream) against HBM bandwidth, `phases` lists all three; `cpu_baseline` is the CPU oracle timed on this host's cores on a
+Prints ONE JSON line.  `value` is pooled lookups per second of the K timed
+steps (wall clock, one HIP event pair per step on the launch stream gives
+`step_us`).  The same batches then run again with events between the
+phases: `roofline` prices the phase that takes the most time against HBM
+bandwidth and `phases` lists all three; `cold` repeats them after flushing
+the caches.  `cpu_baseline` is the CPU oracle timed on this host's cores on a
 bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -37,14 +40,16 @@ PHASE_SOURCES = {"fwd": [os.path.join(_CSRC, "pool_fwd.hip")],
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3")
-    ap.add_argument("--schedule", choices=("pipelined", "serial"), default="serial",
-                    help="pipelined: the id dedup of batch k+1 runs on a second stream alongside the forward and "
-                         "update of batch k (same results as serial)")
-    ap.add_argument("--lookahead", type=int, default=2, help="batches whose dedup may run ahead (pipelined)")
+    ap.add_argument("--schedule", choices=("serial", "concurrent", "pipelined"), default="serial",
+                    help="concurrent: the forward of a batch runs on a side stream at the same time as its id "
+                         "dedup; serial: forward, dedup, reduce + update one after another on one stream; "
+                         "pipelined (switched off): the dedup of batch k+1 alongside the forward and update of "
+                         "batch k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for counter calibration)")
@@ -151,9 +156,8 @@ def main():
 
     w = synth.workload(args.workload)
     if args.schedule == "pipelined":
-        print("bench.py: the pipelined schedule is switched off: its runs on 8 x 1M x 64 (4096 bags per table) and "
-              "on 1 x 50M x 64 (16384 bags) ended in GPU memory faults whose cause is not yet found; "
-              "use --schedule serial", file=sys.stderr)
+        print("bench.py: the pipelined schedule is switched off (two co-resident dedups in flight together can "
+              "wait on each other's blocks); use --schedule serial", file=sys.stderr)
         sys.exit(2)
     dev = "cuda"
     total = args.warmup + args.steps
@@ -195,45 +199,81 @@ def main():
         if ev:
             ev[3].record(stream)
 
+    if args.schedule == "concurrent":
+        clayer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
+                           concurrent=True)
+
+        def run_step(i):
+            clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
+    else:
+        def run_step(i):
+            layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
+
     for i in range(args.warmup):
-        step(i)
+        run_step(i)
     torch.cuda.synchronize()
 
-    # serial steps with HIP events on the launch stream around each phase:
-    # per-phase and per-kernel times for the roofline
+    # timed region: K whole steps, one fresh batch each, one HIP event pair
+    # per step on the launch stream
+    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    t_start = time.perf_counter()
+    for k, i in enumerate(range(args.warmup, total)):
+        sev[k][0].record(stream)
+        run_step(i)
+        sev[k][1].record(stream)
+    t_enq = time.perf_counter() - t_start
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    step_s = [e[0].elapsed_time(e[1]) * 1e-3 for e in sev]
+    gpu_step_s = float(np.mean(step_s))
+
+    # the same batches again as serial steps with events between the phases:
+    # per-phase times for the roofline
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    t_start = time.perf_counter()
     for k, i in enumerate(range(args.warmup, total)):
         step(i, evs[k])
     torch.cuda.synchronize()
-    serial_elapsed = time.perf_counter() - t_start
     ph = {"fwd": [], "dedup": [], "bwd_update": []}
     for e in evs:
         ph["fwd"].append(e[0].elapsed_time(e[1]) * 1e-3)
         ph["dedup"].append(e[1].elapsed_time(e[2]) * 1e-3)
         ph["bwd_update"].append(e[2].elapsed_time(e[3]) * 1e-3)
-    gpu_step_s = float(np.mean([e[0].elapsed_time(e[3]) * 1e-3 for e in evs]))
+    phased_step_s = [e[0].elapsed_time(e[3]) * 1e-3 for e in evs]
 
-    if args.schedule == "pipelined":
-        pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
-                            lookahead=args.lookahead)
-
-        def pstep(i):
-            pipe.step(dev_batches[i][0], out, dev_batches[i][1],
-                      upcoming=[b for b, _, _ in dev_batches[i + 1:i + 1 + args.lookahead]])
-
-        for i in range(args.warmup):
-            pstep(i)
+    # cold steps: the same batches again, with the L2s and the last-level
+    # cache flushed by writing 1 GiB before each step (outside the events)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    cold = None
+    if not args.no_cold:
+        cold_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        for k, i in enumerate(range(args.warmup, total)):
+            flush.fill_(k & 0xff)
+            step(i, cold_evs[k])
         torch.cuda.synchronize()
-        # timed region: K whole steps, one fresh batch each
-        t_start = time.perf_counter()
-        for i in range(args.warmup, total):
-            pstep(i)
-        torch.cuda.synchronize()
-        elapsed = time.perf_counter() - t_start
-    else:
-        elapsed = serial_elapsed
+        cold_step_s = [e[0].elapsed_time(e[3]) * 1e-3 for e in cold_evs]
+        cold_ph = {"fwd": [e[0].elapsed_time(e[1]) * 1e-3 for e in cold_evs],
+                   "dedup": [e[1].elapsed_time(e[2]) * 1e-3 for e in cold_evs],
+                   "bwd_update": [e[2].elapsed_time(e[3]) * 1e-3 for e in cold_evs]}
+        cold = {"note": "serial steps of the same batches again, 1 GiB written between steps to flush L2 and the "
+                        "last-level cache",
+                "median_us": float(np.median(cold_step_s)) * 1e6,
+                "p10_us": float(np.percentile(cold_step_s, 10)) * 1e6,
+                "p90_us": float(np.percentile(cold_step_s, 90)) * 1e6,
+                "phases_median_us": {k: float(np.median(v)) * 1e6 for k, v in cold_ph.items()}}
+    # achievable streaming bandwidth on this device: a 1 GiB device-to-device copy (read + write)
+    dst = torch.empty_like(flush)
+    dst.copy_(flush)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    c0.record(stream)
+    for _ in range(5):
+        dst.copy_(flush)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del flush, dst
+
     n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
 
     # unique counts of the timed batches (for the byte models)
@@ -269,8 +309,7 @@ def main():
         "data": "synthetic (seeded Zipf ids, N(0,1) upstream gradients, U(-0.01,0.01) tables)",
         "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
-                   "table_bytes": w.weight_bytes, "schedule": args.schedule,
-                   "lookahead": args.lookahead if args.schedule == "pipelined" else 0},
+                   "table_bytes": w.weight_bytes, "schedule": args.schedule},
         "roofline": {"bound": "hbm", "phase": dom, "kernel": d["kernels"], "model": "logical",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": d["hbm_traffic_bytes"], "bytes_per_launch": d["logical_bytes"],
@@ -280,8 +319,14 @@ def main():
                        "logical_GBs": step_log / (ms * 1e-3) / 1e9,
                        "compulsory_GBs": step_comp / (ms * 1e-3) / 1e9,
                        "logical_frac": step_log / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        "gpu_us_per_step_serial": gpu_step_s * 1e6,
-        "serial_ms_per_step": serial_elapsed / args.steps * 1e3,
+        "step_us": {"schedule": args.schedule, "mean": gpu_step_s * 1e6,
+                    "median": float(np.median(step_s)) * 1e6,
+                    "p10": float(np.percentile(step_s, 10)) * 1e6,
+                    "p90": float(np.percentile(step_s, 90)) * 1e6,
+                    "host_enqueue_us": t_enq / args.steps * 1e6,
+                    "with_phase_events_median": float(np.median(phased_step_s)) * 1e6},
+        "cold": None if cold is None else dict(cold, lookups_per_s=N_avg * 1e6 / cold["median_us"]),
+        "achievable_copy_GBs": copy_gbs,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

@@ -154,11 +154,17 @@ emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update,
 emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, int32_t* flag, void* stream);
 
 /* Device-side error word of a workspace (host-readable after a copy): bit 0 is
- * set if a bounded spin-wait inside a look-back scan ran out, bit 1 if a sort
- * pass found digit totals inconsistent with its keys (a workspace that was not
- * initialised); results of that call are then undefined and the word stays
- * set until the workspace is initialised again.  Offset in bytes from the
- * workspace base. */
+ * set if a wait for a word another workgroup publishes ran out (every such
+ * wait is bounded to 20 ms, far beyond any wait of a healthy call), bit 1 if
+ * a sort pass found digit totals inconsistent with its keys (a workspace that
+ * was not initialised), bit 2 if a wait of the gradient combine ran out.  The
+ * results of that call are then undefined, but every write stays inside the
+ * caller's buffers: while bit 0 or 1 is set, emb_grad_reduce with this
+ * workspace forms no gradient row and writes no table row, and
+ * emb_sparse_update skips keys >= R.  The word stays set until the workspace
+ * is initialised again.  The three 32-bit words after it record the first
+ * wait that ran out (a site code, its block index) and how many ran out.
+ * Offset in bytes from the workspace base. */
 size_t emb_workspace_error_offset(void);
 
 const char* emb_status_string(int32_t status);

@@ -200,10 +200,19 @@ def workspace_error_offset() -> int:
 
 class Layer:
     """One GPU's shard of the layer with its buffers: forward, then the
-    backward (dedup, segment-reduce, fused optimizer step) of the same batch."""
+    backward (dedup, segment-reduce, fused optimizer step) of the same batch.
+
+    With ``concurrent=True``, ``step`` runs the id dedup of a batch at the
+    same time as its forward: the dedup reads only the batch's ids and
+    offsets, never the table, so the two are independent; the forward runs on
+    a side stream after every earlier update on the caller's stream, and the
+    segment-reduce with the update waits for both.  The results are those of
+    the serial order bit for bit.  It is off by default: on MI355X the
+    forward's traffic slows the latency-bound sort passes by about as much as
+    the overlap saves, and each cross-stream wait costs the host 15-25 us."""
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0):
+                 max_indices: int = 0, max_bags: int = 0, concurrent: bool = False):
         import torch
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
         dev = tables.weights.device
@@ -221,6 +230,26 @@ class Layer:
         self.sort_perm = torch.empty(n, **i32)
         self.num_unique = torch.zeros(1, **i32)
         self.max_indices = n
+        self.concurrent = concurrent
+        if concurrent:
+            self._side_stream = torch.cuda.Stream(device=dev)
+            self._side = int(self._side_stream.cuda_stream)
+            self._ev_ready = _Hip.event()
+            self._ev_fwd = _Hip.event()
+        # argument values fixed for the layer's life, marshalled once
+        self._ct = ctypes.byref(tables.c())
+        self._upd = ctypes.byref(_update(opt, lr, eps, state))
+        self._dd = (_ptr(self.unique_keys), _ptr(self.counts), _ptr(self.seg_offsets), _ptr(self.sort_perm),
+                    _ptr(self.num_unique), _ptr(self.ws), self.ws.numel() * self.ws.element_size())
+
+    def __del__(self):
+        if getattr(self, "concurrent", False):
+            try:
+                L = _Hip.lib()
+                L.hipEventDestroy(self._ev_ready)
+                L.hipEventDestroy(self._ev_fwd)
+            except Exception:
+                pass
 
     def forward(self, batch: Batch, out, stream=None) -> None:
         pool_fwd(self.tables, batch, self.pool, out, stream)
@@ -235,8 +264,32 @@ class Layer:
                     state=self.state, stream=stream)
 
     def step(self, batch: Batch, out, grad_out, stream=None) -> None:
-        self.forward(batch, out, stream)
-        self.backward(batch, grad_out, stream=stream)
+        """Forward of ``batch`` into ``out`` and its backward with ``grad_out``
+        (fused optimizer step), enqueued on ``stream``; ``out`` is complete
+        when ``stream`` reaches the end of the step."""
+        if int(batch.indices.numel()) > self.max_indices:
+            raise ValueError("batch larger than the layer's buffers")
+        L = lib()
+        main = _stream(stream)
+        cb = ctypes.byref(batch.c())
+        uk, cnt, seg, perm, nu, ws, wsb = self._dd
+        pool = POOL[self.pool]
+        if not self.concurrent:
+            _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, pool, _ptr(out), main))
+            _check("emb_unique_ids", L.emb_unique_ids(self._ct, cb, uk, cnt, seg, perm, nu, ws, wsb, main))
+            _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, pool, _ptr(grad_out), perm, seg, uk, nu, None,
+                                                        self._upd, ws, wsb, main))
+            return
+        # every earlier update on the caller's stream precedes this forward
+        _Hip.record(self._ev_ready, main)
+        _check("emb_unique_ids", L.emb_unique_ids(self._ct, cb, uk, cnt, seg, perm, nu, ws, wsb, main))
+        _Hip.wait(self._side, self._ev_ready)
+        _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, pool, _ptr(out), self._side))
+        _Hip.record(self._ev_fwd, self._side)
+        # the update must not overwrite rows before this forward has read them
+        _Hip.wait(main, self._ev_fwd)
+        _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, pool, _ptr(grad_out), perm, seg, uk, nu, None,
+                                                    self._upd, ws, wsb, main))
 
 
 class DedupBuffers:

@@ -195,12 +195,13 @@ __device__ __forceinline__ void block_excl_scan(uint32_t* arr, uint32_t* s_wsum)
 // status words, kLookbackWindow of them per round (loaded together), adding
 // aggregates until it reaches an inclusive prefix.  A word that is not yet
 // published (wrong tag or no flag) ends the round; the next round starts
-// there.  The wait is bounded: running out of spins flags an error.
+// there.  The wait is bounded in time (kWaitTicks).
 __device__ __forceinline__ uint32_t lookback_digit(const uint64_t* status, int stride, int tile, int d,
-                                                   uint32_t tag, uint32_t* err) {
+                                                   uint32_t tag, WsHeader* h, uint32_t site) {
   uint32_t excl = 0;
   int j = tile - 1;
   uint32_t spins = 0;
+  const uint64_t t0 = wait_clock();
   while (j >= 0) {
     uint64_t sv[kLookbackWindow];
 #pragma unroll
@@ -224,8 +225,8 @@ __device__ __forceinline__ uint32_t lookback_digit(const uint64_t* status, int s
     if (inc) break;
     j -= consumed;
     if (consumed == 0) {
-      if (++spins > kSpinLimit) {
-        atomicOr(err, 1u);
+      if (wait_over(h, t0, ++spins)) {
+        flag_timeout(h, site);
         break;
       }
       __builtin_amdgcn_s_sleep(1);
@@ -238,18 +239,19 @@ __device__ __forceinline__ uint32_t lookback_digit(const uint64_t* status, int s
 // (tag << 32 | count).  A batch of words is loaded together; the words that
 // do not carry this pass's tag yet are loaded again together after a short
 // sleep, so every retry round costs one memory round trip however many words
-// are stale.  The wait is bounded: running out of spins flags an error.
+// are stale.  The wait is bounded in time (kWaitTicks).
 template <int K>
 __device__ __forceinline__ void poll_batch(const uint64_t* base, int stride, int lo, int n, int d, uint32_t tag,
-                                           uint32_t* err, uint64_t (&v)[K]) {
+                                           WsHeader* h, uint32_t site, uint64_t (&v)[K]) {
   // words past n stand in as ready
   uint32_t stale = 0;
 #pragma unroll
   for (int i = 0; i < K; ++i) stale |= (i < n && (uint32_t)(v[i] >> 32) != tag) ? (1u << i) : 0u;
   uint32_t spins = 0;
+  const uint64_t t0 = stale ? wait_clock() : 0;
   while (stale) {
-    if (++spins > kSpinLimit) {
-      atomicOr(err, 1u);
+    if (wait_over(h, t0, ++spins)) {
+      flag_timeout(h, site);
       break;
     }
     __builtin_amdgcn_s_sleep(1);
@@ -268,15 +270,16 @@ __device__ __forceinline__ void poll_batch(const uint64_t* base, int stride, int
 // in-group exclusive prefixes of the group's tiles as 16-bit pairs (a group
 // of co-resident tiles holds fewer than 2^16 keys before its last tile), and
 // its own.
-static_assert((kPrefixGroup - 1) * kSortThreads * kSortItemsCore < 65536, "in-group prefixes fit 16 bits");
+static_assert((kPrefixGroup - 1) * kSortThreads * kSortItemsWide < 65536, "in-group prefixes fit 16 bits");
 __device__ __forceinline__ void group_counts(const uint64_t* rows, uint64_t* grp, int stride, int g, int g0, int g1,
-                                             int d, uint32_t tag, uint32_t* err, uint32_t (&pk)[kPrefixGroup / 2],
+                                             int d, uint32_t tag, WsHeader* h, uint32_t site,
+                                             uint32_t (&pk)[kPrefixGroup / 2],
                                              uint32_t& last_pre) {
   uint64_t v[kPrefixGroup];
   const int n = g1 - g0;
 #pragma unroll
   for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(rows + (size_t)(g0 + i) * stride + d) : 0;
-  poll_batch<kPrefixGroup>(rows, stride, g0, n, d, tag, err, v);
+  poll_batch<kPrefixGroup>(rows, stride, g0, n, d, tag, h, site, v);
   uint32_t run = 0;
   last_pre = 0;
 #pragma unroll
@@ -292,14 +295,14 @@ __device__ __forceinline__ void group_counts(const uint64_t* rows, uint64_t* grp
 // Sum of the published group sums of digit d before group g, and of all of
 // them (the digit's total), loaded in batches of kPrefixGroup.
 __device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int g, int ngroups, int d, uint32_t tag,
-                                           uint32_t* err, uint32_t& before, uint32_t& total) {
+                                           WsHeader* h, uint32_t site, uint32_t& before, uint32_t& total) {
   before = total = 0;
   for (int base = 0; base < ngroups; base += kPrefixGroup) {
     const int n = min(kPrefixGroup, ngroups - base);
     uint64_t gv[kPrefixGroup];
 #pragma unroll
     for (int i = 0; i < kPrefixGroup; ++i) gv[i] = i < n ? ld_acquire_u64(grp + (size_t)(base + i) * stride + d) : 0;
-    poll_batch<kPrefixGroup>(grp, stride, base, n, d, tag, err, gv);
+    poll_batch<kPrefixGroup>(grp, stride, base, n, d, tag, h, site, gv);
 #pragma unroll
     for (int i = 0; i < kPrefixGroup; ++i) {
       if (i < n) {
@@ -334,7 +337,8 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
     const int d = tid + k * kSortThreads;
     if (d < ND) {
       uint32_t pk[kPrefixGroup / 2], unused;
-      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, &a.hdr->error, pk, unused);
+      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, a.hdr, kSiteGroupCounts | ((uint32_t)a.pass << 4), pk,
+                   unused);
 #pragma unroll
       for (int j = 0; j < kPrefixGroup / 2; ++j) s_pre[j * ND + d] = pk[j];
     }
@@ -345,7 +349,7 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
     excl[k] = 0;
     if (d < ND) {
       uint32_t total = 0;
-      group_sums(a.grp, a.status_stride, g, ngroups, d, tag, &a.hdr->error, excl[k], total);
+      group_sums(a.grp, a.status_stride, g, ngroups, d, tag, a.hdr, kSiteGroupSums | ((uint32_t)a.pass << 4), excl[k], total);
       s_base[d] = total;
     }
   }
@@ -378,7 +382,7 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
           uint64_t v[kPrefixGroup];
 #pragma unroll
           for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(lb + (size_t)(g0 + i) * lstride + d) : 0;
-          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, &a.hdr->error, v);
+          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, a.hdr, kSiteLaterCounts | ((uint32_t)a.pass << 4), v);
           uint32_t sum = 0;
 #pragma unroll
           for (int i = 0; i < kPrefixGroup; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
@@ -419,7 +423,7 @@ __device__ __forceinline__ void sort_prefix_range(const PassArgs& a, uint32_t ta
   uint64_t v[kRangeTiles];
 #pragma unroll
   for (int i = 0; i < kRangeTiles; ++i) v[i] = i < n ? ld_acquire_u64(a.rows + (size_t)(t0 + i) * a.status_stride + d) : 0;
-  poll_batch<kRangeTiles>(a.rows, a.status_stride, t0, n, d, tag, &a.hdr->error, v);
+  poll_batch<kRangeTiles>(a.rows, a.status_stride, t0, n, d, tag, a.hdr, kSiteRangeCounts | ((uint32_t)a.pass << 4), v);
   uint32_t sum = 0;
 #pragma unroll
   for (int i = 0; i < kRangeTiles; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
@@ -720,7 +724,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       excl[k] = 0;
       if (d < ND) {
         uint64_t fv[1] = {ld_acquire_u64(a.status + (size_t)tile * a.status_stride + d)};
-        poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, &a.hdr->error, fv);
+        poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, a.hdr, kSiteTileOffsets | ((uint32_t)a.pass << 4), fv);
         excl[k] = (uint32_t)fv[0];
       }
     }
@@ -737,7 +741,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       const int d = tid + k * kSortThreads;
       excl[k] = 0;
       if (d < ND && tile > 0) {
-        excl[k] = lookback_digit(a.status, a.status_stride, tile, d, tag, &a.hdr->error);
+        excl[k] = lookback_digit(a.status, a.status_stride, tile, d, tag, a.hdr, kSiteLookback | ((uint32_t)a.pass << 4));
         st_u64(st + d, tag_hi | (kFlagInc << 30) | (excl[k] + my_cnt[k]));
       }
     }
@@ -872,6 +876,7 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
       if (lane == 0) st_u64(a.status + tile, pack_uniq(kFlagAgg, tile_c, tile_q));
       int j = tile - 1;
       uint32_t spins = 0;
+      const uint64_t t0 = wait_clock();
       while (true) {
         uint64_t sv[kUniqWindows];
 #pragma unroll
@@ -912,8 +917,8 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
         if (done) break;
         j -= took;
         if (took == 0) {
-          if (++spins > kSpinLimit) {
-            if (lane == 0) atomicOr(&a.hdr->error, 1u);
+          if (wait_over(a.hdr, t0, ++spins)) {
+            if (lane == 0) flag_timeout(a.hdr, kSiteUnique);
             break;
           }
           __builtin_amdgcn_s_sleep(1);
@@ -998,6 +1003,14 @@ hipError_t launch_pass_bits(const PassArgs& pa, int tiles, hipStream_t s) {
   }
 }
 
+const void* pass_kernel(int it, int bits) {
+  switch (it) {
+    case kSortItemsCore: return pass_kernel_bits<kSortItemsCore>(bits);
+    case kSortItemsMid: return pass_kernel_bits<kSortItemsMid>(bits);
+    default: return pass_kernel_bits<kSortItemsWide>(bits);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
@@ -1015,32 +1028,41 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   int max_bits = 1;
   for (int i = 0; i < p.plan.passes; ++i) max_bits = p.plan.bits[i] > max_bits ? p.plan.bits[i] : max_bits;
   const int status_stride = 1 << max_bits;
-  // every tile of a pass resident at once: tile = block index, bags found by
-  // the first pass, two-level published-count prefix; otherwise a prepare
-  // kernel (bags, keys, digit totals), tickets and a look-back
+  // Co-resident passes, when every tile of a pass and its prefix blocks fit
+  // one block per compute unit (coresident_limit): tile = block index, bags
+  // found by the first pass, two-level published-count prefix, with the
+  // smallest tiles that fit.  Otherwise a prepare kernel (bags, keys, digit
+  // totals), tickets and a look-back.
   // A co-resident pass also runs its prefix blocks after the tiles: one per
   // group of kPrefixGroup tiles for the first pass, one per kRangeDigits
   // digits for the later ones (their digit totals are counted during the
   // first pass), unless the tiles are too many for a range block's threads
   // or the digits do not shrink from pass to pass.
-  const int core_tiles = (N + kSortTileMin - 1) / kSortTileMin;
-  const int core_groups = (core_tiles + kPrefixGroup - 1) / kPrefixGroup;
-  int ranges = p.plan.passes > 1 ? 1 : 0;
-  for (int i = 1; i < p.plan.passes; ++i) {
-    const int nd = 1 << p.plan.bits[i];
-    const int db = nd < kRangeDigits ? nd : kRangeDigits;
-    if (p.plan.bits[i] > p.plan.bits[0] || core_tiles > (kSortThreads / db) * kRangeTiles) ranges = 0;
-  }
+  int sort_it = 0, core_tiles = 0, core_groups = 0, ranges = 0;
   auto prefix_blocks = [&](int ps) {
     if (ps == 0 || !ranges) return core_groups;
     const int nd = 1 << p.plan.bits[ps];
     return nd / (nd < kRangeDigits ? nd : kRangeDigits);
   };
-  int sort_cores = 1;
-  for (int i = 0; i < p.plan.passes; ++i)
-    if (core_tiles + prefix_blocks(i) > resident_blocks(pass_kernel_bits<kSortItemsCore>(p.plan.bits[i]), kSortThreads))
-      sort_cores = 0;
-  const int tile_keys = kSortThreads * (sort_cores ? kSortItemsCore : kSortItemsWide);
+  for (const int it : {kSortItemsCore, kSortItemsMid, kSortItemsWide}) {
+    core_tiles = (N + kSortThreads * it - 1) / (kSortThreads * it);
+    core_groups = (core_tiles + kPrefixGroup - 1) / kPrefixGroup;
+    ranges = p.plan.passes > 1 ? 1 : 0;
+    for (int i = 1; i < p.plan.passes; ++i) {
+      const int nd = 1 << p.plan.bits[i];
+      const int db = nd < kRangeDigits ? nd : kRangeDigits;
+      if (p.plan.bits[i] > p.plan.bits[0] || core_tiles > (kSortThreads / db) * kRangeTiles) ranges = 0;
+    }
+    bool fits = true;
+    for (int i = 0; i < p.plan.passes; ++i)
+      if (core_tiles + prefix_blocks(i) > coresident_limit(pass_kernel(it, p.plan.bits[i]), kSortThreads)) fits = false;
+    if (fits) {
+      sort_it = it;
+      break;
+    }
+  }
+  const int sort_cores = sort_it > 0 ? 1 : 0;
+  const int tile_keys = kSortThreads * (sort_cores ? sort_it : kSortItemsWide);
   const int sort_tiles = (N + tile_keys - 1) / tile_keys;
   const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
   uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
@@ -1119,8 +1141,11 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.bits = p.plan.bits[ps];
     xa.pass = ps;
     xa.status_stride = status_stride;
-    e = sort_cores ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles + prefix_blocks(ps), s)
-                   : launch_pass_bits<kSortItemsWide>(xa, sort_tiles, s);
+    switch (sort_cores ? sort_it : kSortItemsWide) {
+      case kSortItemsCore: e = launch_pass_bits<kSortItemsCore>(xa, sort_tiles + prefix_blocks(ps), s); break;
+      case kSortItemsMid: e = launch_pass_bits<kSortItemsMid>(xa, sort_tiles + prefix_blocks(ps), s); break;
+      default: e = launch_pass_bits<kSortItemsWide>(xa, sort_tiles + (sort_cores ? prefix_blocks(ps) : 0), s);
+    }
     if (e != hipSuccess) return e;
     kin = xa.keys_out;
     vin = xa.vals_out;

@@ -219,6 +219,7 @@ emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update,
   p.ukeys = unique_keys;
   p.num_unique = num_unique;
   p.max_unique = max_unique;
+  p.rows = (uint32_t)R;
   p.D = tables->dim;
   p.opt = update->opt;
   p.dtype = tables->dtype;

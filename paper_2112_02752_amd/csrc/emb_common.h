@@ -21,6 +21,7 @@ constexpr int kSortThreads = 512;
 // keys per thread: tiles of 2048 when every tile of a pass is resident at
 // once (more blocks, shorter ranking), 4096 otherwise (fewer look-back steps)
 constexpr int kSortItemsCore = 4;
+constexpr int kSortItemsMid = 5;
 constexpr int kSortItemsWide = 8;
 constexpr int kSortTileMin = kSortThreads * kSortItemsCore;
 
@@ -35,7 +36,7 @@ constexpr int kLookbackWindow = 8;
 constexpr int kPrefixGroup = 16;
 // digit-range prefix blocks (passes after the first, co-resident): digits per
 // block, and the most tiles one of its threads sums
-constexpr int kRangeDigits = 16;
+constexpr int kRangeDigits = 32;
 constexpr int kRangeTiles = 16;
 // bag offsets a first-pass tile stages in LDS to find the bag of each position
 constexpr int kBagStage = 2048;
@@ -68,7 +69,10 @@ struct WsHeader {
   uint32_t gen;
   uint32_t error;
   uint32_t ticket[8];
-  uint32_t pad[54];
+  // first wait that ran out: its site code, block index and the number of
+  // waits that ran out in all (kept until the workspace is initialised again)
+  uint32_t timeout_site, timeout_block, timeouts;
+  uint32_t pad[51];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 
@@ -183,9 +187,52 @@ __device__ __forceinline__ uint32_t atomic_add_u32(uint32_t* p, uint32_t v) {
 // holds at once, all compute units together (cached per device and kernel).
 int resident_blocks(const void* kernel, int threads);
 
-// Bounded spin budget of a look-back wait; running out sets an error bit and
-// lets the wave continue, so every wave always exits.
-constexpr uint32_t kSpinLimit = 1u << 22;
+// The most workgroups of `kernel` that may wait on one another within one
+// launch: one per compute unit (0 if a compute unit cannot hold one).  The
+// occupancy API counts what an idle device holds; kernels that ran alongside
+// on other streams can leave a compute unit's registers and LDS fragmented so
+// that it takes only one such block until it drains, and a block per compute
+// unit is what stays guaranteed once the others have finished (blocks go to
+// the XCDs round-robin, the same number of compute units in each).
+int coresident_limit(const void* kernel, int threads);
+
+// Bound of a wait for a word another workgroup publishes, in ticks of the
+// 100 MHz constant clock: 20 ms, thousands of times any wait of a healthy
+// call.  Running out sets bit 0 of the error word, records the wait, and lets
+// the wave continue, so every wave always exits; the waits of a call that has
+// already timed out give up at their next check of the error word.
+constexpr uint64_t kWaitTicks = 2000000;
+// error bits of the dedup: a wait ran out (bit 0); digit totals inconsistent
+// with the keys (bit 1).  The gradient reduce does nothing when either is set.
+constexpr uint32_t kDedupErrors = 3u;
+
+// Site codes of the waits: (kernel << 8) | (sort pass << 4) | wait.
+enum WaitSite : uint32_t {
+  kSiteTileOffsets = 0x100,  // co-resident tile: its final digit offsets
+  kSiteLookback = 0x101,     // windowed look-back tile: earlier tiles' counts
+  kSiteGroupCounts = 0x102,  // first-pass prefix block: its group's counts
+  kSiteGroupSums = 0x103,    // first-pass prefix block: every group's sum
+  kSiteLaterCounts = 0x104,  // first-pass prefix block: later passes' counts
+  kSiteRangeCounts = 0x105,  // range prefix block: its tiles' counts
+  kSiteUnique = 0x200,       // unique look-back
+  kSiteCombine = 0x300,      // gradient combine: crossing-segment rows
+};
+
+__device__ __forceinline__ uint64_t wait_clock() { return wall_clock64(); }
+
+// a wait that started at t0 has run out (or another wait of the call has)
+__device__ __forceinline__ bool wait_over(const WsHeader* h, uint64_t t0, uint32_t spins) {
+  if ((spins & 31u) == 0u && (__hip_atomic_load(&h->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
+    return true;
+  return wait_clock() - t0 > kWaitTicks;
+}
+
+// a wait ran out: set `bit` in the error word and record the first such wait
+__device__ __forceinline__ void flag_timeout(WsHeader* h, uint32_t site, uint32_t bit = 1u) {
+  atomicOr(&h->error, bit);
+  atomicAdd(&h->timeouts, 1u);
+  if (atomicCAS(&h->timeout_site, 0u, site) == 0u) h->timeout_block = blockIdx.x;
+}
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {

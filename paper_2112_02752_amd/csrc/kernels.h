@@ -68,6 +68,7 @@ struct UpdateLaunch {
   const uint32_t* ukeys;
   const int32_t* num_unique;
   int64_t max_unique;
+  uint32_t rows;  // R: keys at or above it are skipped
   int32_t D, opt, dtype;
   float lr, eps;
   void* W;

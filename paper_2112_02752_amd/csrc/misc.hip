@@ -83,4 +83,11 @@ int resident_blocks(const void* kernel, int threads) {
   return n;
 }
 
+int coresident_limit(const void* kernel, int threads) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return resident_blocks(kernel, threads) >= cus ? cus : 0;
+}
+
 }  // namespace emb

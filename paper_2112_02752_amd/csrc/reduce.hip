@@ -415,6 +415,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
   const int wave_id = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int nwaves = gridDim.x * 4;
   const int U = *a.num_unique;
+  // the dedup of this workspace flagged an error (its outputs are undefined):
+  // no gradient row is formed and no table row written
+  if (reinterpret_cast<const WsHeader*>(a.hdr)->error & kDedupErrors) return;
   // the combine that follows starts from cleared level-2 rows and counters
   {
     const int nw = a.ncomb * 2 * a.D;
@@ -460,7 +463,7 @@ constexpr uint32_t kLevel2Tag = 1u;  // rows and counters are cleared by the mai
 // words of several rows loaded together; a word is polled until it carries
 // the tag (bounded)
 template <int G, int NV>
-__device__ __forceinline__ void level2_sum(const RArgs& a, int g0, int g1, int g, int sub, uint32_t* err,
+__device__ __forceinline__ void level2_sum(const RArgs& a, int g0, int g1, int g, int sub, WsHeader* h,
                                            float (&acc)[NV][4]) {
   constexpr int RPI = kWave / G;
   constexpr int RR = rows_in_flight(NV) / 2 > 0 ? rows_in_flight(NV) / 2 : 1;
@@ -490,9 +493,10 @@ __device__ __forceinline__ void level2_sum(const RArgs& a, int g0, int g1, int g
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           uint32_t spins = 0;
+          const uint64_t t0 = wait_clock();
           while ((uint32_t)(x[q][v][e] >> 32) != kLevel2Tag) {
-            if (++spins > kSpinLimit) {
-              atomicOr(err, 4u);
+            if (wait_over(h, t0, ++spins)) {
+              flag_timeout(h, kSiteCombine, 4u);
               break;
             }
             __builtin_amdgcn_s_sleep(1);
@@ -521,6 +525,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform across the wavefront
   const int U = *a.num_unique;
+  if (reinterpret_cast<const WsHeader*>(a.hdr)->error & kDedupErrors) return;  // as in k_reduce_main
   const int blk = blockIdx.x;
   const int c0 = blk * kCombineChunks, c1 = min(a.nchunks, c0 + kCombineChunks);
   if (tid == 0) s_n = 0;
@@ -590,7 +595,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
     old = (uint32_t)__shfl((int)old, 0, kWave);
     if (old == (uint32_t)(be - bs)) {
       WsHeader* h = reinterpret_cast<WsHeader*>(a.hdr);
-      level2_sum<G, NV>(a, bs, be + 1, g, sub, &h->error, acc);
+      level2_sum<G, NV>(a, bs, be + 1, g, sub, h, acc);
       if (g == 0) apply_row<TW, G, NV>(a.up, a.grad_rows, u, key, acc, pre, sub);
     }
   }
@@ -601,6 +606,7 @@ struct UArgs {
   const uint32_t* ukeys;
   const int32_t* num_unique;
   int32_t max_unique;
+  uint32_t rows;
   Upd up;
 };
 
@@ -614,8 +620,10 @@ __global__ __launch_bounds__(256) void k_sparse_update(UArgs a) {
   for (int u = gid; u < U; u += ngroups) {
     float acc[NV][4];
     zero<G, NV>(acc);
+    const uint32_t key = a.ukeys[u];
+    if (key >= a.rows) continue;  // not a row: keys of a failed dedup are never written through
     add_row<G, NV>(a.grad_rows + (size_t)u * a.up.D, 1.0f, a.up.D, sub, acc);
-    finalize<TW, G, NV>(a.up, nullptr, u, a.ukeys[u], acc, sub);
+    finalize<TW, G, NV>(a.up, nullptr, u, key, acc, sub);
   }
 }
 
@@ -715,6 +723,7 @@ hipError_t launch_sparse_update(const UpdateLaunch& p, hipStream_t s) {
   ua.ukeys = p.ukeys;
   ua.num_unique = p.num_unique;
   ua.max_unique = (int32_t)p.max_unique;
+  ua.rows = p.rows;
   ua.up.W = p.W;
   ua.up.state = p.state;
   ua.up.D = p.D;

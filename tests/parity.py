@@ -110,7 +110,9 @@ class StepResult:
 def gpu_step(dl: DeviceLayer, offsets: np.ndarray, indices: np.ndarray, grad: np.ndarray, B: int, pool: str,
              opt: str, lr: float, eps: float, fused: bool = True, want_grad_rows: bool = True,
              layer: Optional[emb.Layer] = None) -> StepResult:
-    """One step (fwd on pre-update rows, dedup, reduce, optimizer) on the GPU."""
+    """One step (fwd on pre-update rows, dedup, reduce, optimizer) on the GPU.
+    A layer built with concurrent=True runs the step through Layer.step (the
+    forward on a side stream alongside the dedup; no unfused gradient rows)."""
     torch = torch_mod()
     dev = dl.W.device
     N = int(indices.shape[0])
@@ -119,9 +121,30 @@ def gpu_step(dl: DeviceLayer, offsets: np.ndarray, indices: np.ndarray, grad: np
     idx = torch.from_numpy(indices.astype(np.int32)).to(dev)
     G = torch.from_numpy(np.ascontiguousarray(grad, dtype=np.float32)).to(dev)
     if layer is None:
-        layer = emb.Layer(dl.tables, pool, opt, lr, eps, dl.state, max_indices=N, max_bags=M)
+        layer = emb.Layer(dl.tables, pool, opt, lr, eps, dl.state, max_indices=N, max_bags=M, concurrent=False)
     b = emb.Batch(off, idx, B)
     out = torch.empty((M, dl.D), dtype=torch.float32, device=dev)
+    if layer.concurrent:
+        assert fused
+        grad_rows = None
+        layer.step(b, out, G)
+    else:
+        grad_rows = _serial_step(dl, b, out, G, N, pool, opt, lr, eps, fused, want_grad_rows, layer)
+    torch.cuda.synchronize()
+    U = int(layer.num_unique.cpu().item())
+    eo = emb.workspace_error_offset()
+    ws_err = int(layer.ws[eo:eo + 4].cpu().numpy().view(np.uint32)[0])
+    return StepResult(
+        out=out.cpu().numpy(), num_unique=U,
+        unique_keys=layer.unique_keys[:U].cpu().numpy().view(np.uint32),
+        counts=layer.counts[:U].cpu().numpy(), seg_offsets=layer.seg_offsets[:U + 1].cpu().numpy(),
+        perm=layer.sort_perm[:N].cpu().numpy(),
+        grad_rows=grad_rows[:U].cpu().numpy() if grad_rows is not None else None, ws_error=ws_err)
+
+
+def _serial_step(dl, b, out, G, N, pool, opt, lr, eps, fused, want_grad_rows, layer):
+    torch = torch_mod()
+    dev = dl.W.device
     emb.pool_fwd(dl.tables, b, pool, out)
     emb.unique_ids(dl.tables, b, layer.unique_keys, layer.counts, layer.seg_offsets, layer.sort_perm,
                    layer.num_unique, layer.ws)
@@ -133,16 +156,7 @@ def gpu_step(dl: DeviceLayer, offsets: np.ndarray, indices: np.ndarray, grad: np
         emb.grad_reduce(dl.tables, b, pool, G, layer.sort_perm, layer.seg_offsets, layer.unique_keys,
                         layer.num_unique, layer.ws, grad_rows=grad_rows)
         emb.sparse_update(dl.tables, opt, lr, eps, dl.state, layer.unique_keys, layer.num_unique, N, grad_rows)
-    torch.cuda.synchronize()
-    U = int(layer.num_unique.cpu().item())
-    eo = emb.workspace_error_offset()
-    ws_err = int(layer.ws[eo:eo + 4].cpu().numpy().view(np.uint32)[0])
-    return StepResult(
-        out=out.cpu().numpy(), num_unique=U,
-        unique_keys=layer.unique_keys[:U].cpu().numpy().view(np.uint32),
-        counts=layer.counts[:U].cpu().numpy(), seg_offsets=layer.seg_offsets[:U + 1].cpu().numpy(),
-        perm=layer.sort_perm[:N].cpu().numpy(),
-        grad_rows=grad_rows[:U].cpu().numpy() if grad_rows is not None else None, ws_error=ws_err)
+    return grad_rows
 
 
 # --------------------------------------------------------------- oracle side
@@ -193,8 +207,9 @@ def check_untouched(dl: DeviceLayer, w: synth.Workload, touched: np.ndarray, n: 
     np.testing.assert_array_equal(dl.rows(cand), synth.weight_rows(w, cand))
 
 
-def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="cuda"):
-    """Full-size parity of `steps` consecutive steps of a workload."""
+def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="cuda", concurrent: bool = False):
+    """Full-size parity of `steps` consecutive steps of a workload (serial
+    calls, or Layer.step's concurrent schedule)."""
     dl = device_layer_from_workload(w, device)
     batches = [synth.make_batch(w, s) for s in range(steps)]
     keys_all = [global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices) for b in batches]
@@ -202,7 +217,8 @@ def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="
     store = oracle.RowStore(synth.weight_rows(w, touched), keys=touched.astype(np.uint32),
                             state=np.zeros(len(touched), np.float32) if w.opt == "adagrad" else None)
     nmax = max(len(b.indices) for b in batches)
-    layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags)
+    layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
+                      concurrent=concurrent)
     for s, b in enumerate(batches):
         g = gpu_step(dl, b.offsets, b.indices, b.grad, w.bags_per_table, w.pool, w.opt, w.lr, w.eps, fused=fused,
                      layer=layer)

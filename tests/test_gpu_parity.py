@@ -221,9 +221,11 @@ def test_run_to_run_bitwise_identical():
         np.testing.assert_array_equal(h, outs[0][2])
 
 
-def test_workspace_reuse_with_varying_batch_sizes():
-    """One workspace, batches of very different N in a row (big, small, big)."""
-    _say("case workspace reuse")
+@pytest.mark.parametrize("concurrent", [False, True])
+def test_workspace_reuse_with_varying_batch_sizes(concurrent):
+    """One workspace, batches of very different N in a row (big, small, big),
+    through serial calls and through Layer.step's concurrent schedule."""
+    _say(f"case workspace reuse concurrent={concurrent}")
     import oracle
     import paper_2112_02752_amd as emb
     rng = np.random.default_rng(7)
@@ -231,7 +233,8 @@ def test_workspace_reuse_with_varying_batch_sizes():
     D = 16
     W = rng.uniform(-1, 1, size=(rows, D)).astype(np.float32)
     dl = parity.device_layer_from_host([0, rows], W, None)
-    layer = emb.Layer(dl.tables, "sum", "sgd", 0.01, 0.0, None, max_indices=200_000, max_bags=5000)
+    layer = emb.Layer(dl.tables, "sum", "sgd", 0.01, 0.0, None, max_indices=200_000, max_bags=5000,
+                      concurrent=concurrent)
     store = oracle.RowStore(W.copy())
     for B, lmax in [(4000, 80), (3, 2), (1, 1), (5000, 60), (50, 10)]:
         off, idx = _rand_batch(rng, [rows], B, lmax, zipf=1.3)
@@ -274,6 +277,17 @@ def test_workload_full_size_one_step(name):
     parity.run_workload(w, steps=1)
 
 
+@pytest.mark.parametrize("bags,concurrent", [(16384, True), (17000, False), (23000, True), (40000, False)])
+def test_sort_tile_modes(bags, concurrent):
+    """Batches of the 50M-row workload's shape whose sizes select each sort
+    mode: co-resident passes with 2048-, 2560- and 4096-key tiles (at most
+    one block per compute unit), and the ticket look-back beyond that."""
+    import dataclasses
+    w = dataclasses.replace(synth.workload("c3"), bags_per_table=bags, name=f"c3-b{bags}")
+    _say(f"case sort tile modes bags={bags} concurrent={concurrent}")
+    parity.run_workload(w, steps=1, concurrent=concurrent)
+
+
 def test_c5_three_consecutive_steps():
     w = synth.workload("c5")
     _say("case c5 x3 steps")
@@ -284,6 +298,45 @@ def test_c2_unfused_path():
     w = synth.workload("c2")
     _say("case c2 unfused")
     parity.run_workload(w, steps=1, fused=False)
+
+
+@pytest.mark.parametrize("name,steps", [("c3", 3), ("c2", 1), ("c4", 1)])
+def test_concurrent_schedule_full_size(name, steps):
+    """Layer.step with the forward on a side stream alongside the dedup
+    matches the oracle at full size."""
+    w = synth.workload(name)
+    _say(f"case concurrent schedule {name} x{steps} steps")
+    parity.run_workload(w, steps=steps, concurrent=True)
+
+
+def test_concurrent_schedule_equals_serial():
+    """The concurrent schedule changes nothing: tables, state and pooled
+    outputs equal those of serial steps bit for bit."""
+    _say("case concurrent vs serial")
+    import torch
+    import paper_2112_02752_amd as emb
+    w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=4, name="c3-small")
+    batches = [synth.make_batch(w, s) for s in range(6)]
+    nmax = max(len(b.indices) for b in batches)
+    dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
+              torch.from_numpy(b.grad).cuda()) for b in batches]
+    results = []
+    for conc in (False, True):
+        dl = parity.device_layer_from_workload(w)
+        layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
+                          concurrent=conc)
+        outs = []
+        for b, g in dev_b:
+            out = torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda")
+            layer.step(b, out, g)
+            outs.append(out)
+        torch.cuda.synchronize()
+        results.append((dl.W.cpu().numpy(), dl.state.cpu().numpy(), [o.cpu().numpy() for o in outs]))
+    (w0, s0, o0), (w1, s1, o1) = results
+    np.testing.assert_array_equal(w0, w1)
+    np.testing.assert_array_equal(s0, s1)
+    for a, b in zip(o0, o1):
+        np.testing.assert_array_equal(a, b)
 
 
 @pytest.mark.skip(reason="the pipelined schedule is switched off: bench runs of it (two dedups of 204 and 240 "
@@ -305,7 +358,8 @@ def test_pipelined_schedule_equals_serial(lookahead):
         dl = parity.device_layer_from_workload(w)
         outs = []
         if mode == "serial":
-            layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags)
+            layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
+                              concurrent=False)
             for b, g in dev_b:
                 out = torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda")
                 layer.step(b, out, g)

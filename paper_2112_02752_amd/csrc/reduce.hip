@@ -427,22 +427,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
     }
   }
 
-  // heavy pieces: one wavefront per aligned chunk of sorted positions
-  for (int c = wave_id; c < a.nchunks; c += nwaves) {
-    const ChunkPieces cp = chunk_pieces(a, c, U);
+  // even wavefronts: the heavy pieces of aligned chunks of sorted positions,
+  // one chunk at a time; odd wavefronts: batches of light segments (the two
+  // kinds of work interleave on the compute units instead of running one
+  // after the other in every wavefront)
+  const int half = nwaves / 2;
+  const int hw = wave_id >> 1;
+  if ((wave_id & 1) == 0) {
+    for (int c = hw; c < a.nchunks; c += half) {
+      const ChunkPieces cp = chunk_pieces(a, c, U);
 #pragma unroll
-    for (int slot = 0; slot < 2; ++slot) {
-      if (cp.hi[slot] > cp.lo[slot]) {
-        float acc[NV][4];
-        wave_piece_sum<G, NV>(a, cp.lo[slot], cp.hi[slot], g, sub, lane, acc);
-        if (g == 0) store_row<G, NV>(a.partials + ((size_t)c * 2 + slot) * a.D, a.D, sub, acc);
+      for (int slot = 0; slot < 2; ++slot) {
+        if (cp.hi[slot] > cp.lo[slot]) {
+          float acc[NV][4];
+          wave_piece_sum<G, NV>(a, cp.lo[slot], cp.hi[slot], g, sub, lane, acc);
+          if (g == 0) store_row<G, NV>(a.partials + ((size_t)c * 2 + slot) * a.D, a.D, sub, acc);
+        }
       }
     }
+    return;
   }
-
   // light segments: batches of RPI * slots consecutive segments per wavefront
   const int per_batch = RPI * slots_for(RPI);
-  for (int ub = wave_id * per_batch; ub < U; ub += nwaves * per_batch) light_batch<TW, G, NV>(a, ub, U, g, sub, lane);
+  for (int ub = hw * per_batch; ub < U; ub += half * per_batch) light_batch<TW, G, NV>(a, ub, U, g, sub, lane);
 }
 
 // Heavy segments.  The block of a range of kCombineChunks chunks lists (one
@@ -710,8 +717,9 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.up.fuse = p.fuse;
   ra.up.lr = p.lr;
   ra.up.eps = p.eps;
-  // main: a wavefront per chunk of sorted positions (up to a full device)
-  const int bm = clamp_blocks(((int64_t)ra.nchunks + 3) / 4, 1, 2048);
+  // main: two wavefronts per chunk of sorted positions (one for its heavy
+  // pieces, one for a batch of light segments), up to two full devices
+  const int bm = clamp_blocks(((int64_t)ra.nchunks + 1) / 2, 1, 4096);
   const int bc = clamp_blocks(ra.ncomb, 1, 1 << 20);
   return p.dtype == EMB_FP32 ? launch_reduce_dt<float>(ra, bm, bc, s) : launch_reduce_dt<uint16_t>(ra, bm, bc, s);
 }

@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3")
+    ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
+                    help="optimizer instead of the workload's own (adagrad_ew: element-wise, state [R][D])")
     ap.add_argument("--schedule", choices=("serial", "concurrent", "pipelined"), default="serial",
                     help="concurrent: the forward of a batch runs on a side stream at the same time as its id "
                          "dedup; serial: forward, dedup, reduce + update one after another on one stream; "
@@ -61,7 +63,7 @@ def byte_models(w, N: float, U: float):
     and compulsory (every distinct row once per phase)."""
     M, D = w.num_bags, w.dim
     sw = 4 if w.dtype == "fp32" else 2
-    s_state = 4 if w.opt == "adagrad" else 0
+    s_state = {"sgd": 0, "adagrad": 4, "adagrad_ew": 4 * D}[w.opt]
     fwd_fixed = 4 * (M + 1) + 4 * N + 4 * M * D
     fwd_log = fwd_fixed + N * D * sw
     fwd_comp = fwd_fixed + U * D * sw
@@ -155,6 +157,10 @@ def main():
         return
 
     w = synth.workload(args.workload)
+    if args.opt is not None and args.opt != w.opt:
+        import dataclasses
+        w = dataclasses.replace(w, opt=args.opt, name=f"{w.name}-{args.opt}",
+                                description=f"{w.description}; optimizer {args.opt} instead")
     if args.schedule == "pipelined":
         print("bench.py: the pipelined schedule is switched off (two co-resident dedups in flight together can "
               "wait on each other's blocks); use --schedule serial", file=sys.stderr)
@@ -168,7 +174,11 @@ def main():
     W = torch.empty((w.total_rows, w.dim), dtype=torch.float32 if w.dtype == "fp32" else torch.bfloat16,
                     device=dev)
     synth.fill_device_weights(w, W.data_ptr(), int(torch.cuda.current_stream().cuda_stream))
-    state = torch.zeros(w.total_rows, dtype=torch.float32, device=dev) if w.opt == "adagrad" else None
+    state = None
+    if w.opt == "adagrad":
+        state = torch.zeros(w.total_rows, dtype=torch.float32, device=dev)
+    elif w.opt == "adagrad_ew":
+        state = torch.zeros((w.total_rows, w.dim), dtype=torch.float32, device=dev)
     tables = emb.Tables(W, [int(x) for x in w.row_offset])
     nmax = max(len(b.indices) for b in batches)
     layer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags)

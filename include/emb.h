@@ -57,7 +57,7 @@ typedef enum {
 
 typedef enum { EMB_FP32 = 0, EMB_BF16 = 1 } emb_dtype;
 typedef enum { EMB_POOL_SUM = 0, EMB_POOL_MEAN = 1 } emb_pool;
-typedef enum { EMB_OPT_SGD = 0, EMB_OPT_ADAGRAD_ROWWISE = 1 } emb_opt;
+typedef enum { EMB_OPT_SGD = 0, EMB_OPT_ADAGRAD_ROWWISE = 1, EMB_OPT_ADAGRAD_ELEMENTWISE = 2 } emb_opt;
 
 #define EMB_MAX_TABLES 256
 
@@ -80,16 +80,21 @@ typedef struct {
   int64_t num_indices;       /* N, host value, 0 <= N < 2^30 */
 } emb_batch;
 
-/* Optimizer of one sparse step.
- *   SGD:               W_r <- W_r - lr * g_r
- *   row-wise Adagrad:  h_r <- h_r + (1/D) sum_d g_r[d]^2
- *                      W_r <- W_r - lr * g_r / (sqrt(h_r) + eps)
- * Arithmetic is fp32; bf16 tables store the fp32 result rounded to nearest even. */
+/* Optimizer of one sparse step (the paper's push step applies the sparse
+ * gradient to the touched rows; it does not fix the optimizer).
+ *   SGD:                   W_r <- W_r - lr * g_r
+ *   row-wise Adagrad:      h_r <- h_r + (1/D) sum_d g_r[d]^2
+ *                          W_r <- W_r - lr * g_r / (sqrt(h_r) + eps)
+ *   element-wise Adagrad:  h_r[d] <- h_r[d] + g_r[d]^2
+ *   (Duchi et al. 2011)    W_r[d] <- W_r[d] - lr * g_r[d] / (sqrt(h_r[d]) + eps)
+ * The new h is used in the same step.  Arithmetic is fp32; bf16 tables store
+ * the fp32 result rounded to nearest even. */
 typedef struct {
   int32_t opt;    /* emb_opt */
   float lr;
   float eps;      /* Adagrad only */
-  float* state;   /* device [R] fp32 accumulators h (Adagrad), NULL for SGD */
+  float* state;   /* device fp32 accumulators h: [R] (row-wise), [R][D] row-major
+                     (element-wise); NULL for SGD */
 } emb_update;
 
 /* Forward: out[m][d] = scale_m * sum over bag m of W[key(j)][d], fp32

@@ -24,7 +24,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "liboracle.so")
 
 POOL = {"sum": 0, "mean": 1}
-OPT = {"sgd": 0, "adagrad": 1}
+OPT = {"sgd": 0, "adagrad": 1, "adagrad_ew": 2}
 DTYPE = {"fp32": 0, "bf16": 1}
 
 
@@ -79,7 +79,7 @@ class RowStore:
     listed global rows (sorted uint32 keys) with their values."""
     vals: np.ndarray                  # float32 [n][D] or uint16 bf16 bits [n][D]
     keys: Optional[np.ndarray] = None  # uint32 [n] sorted, or None
-    state: Optional[np.ndarray] = None  # float32 [n] row-wise Adagrad accumulators
+    state: Optional[np.ndarray] = None  # float32 [n] row-wise or [n][D] element-wise Adagrad accumulators
 
     @property
     def dtype(self) -> int:
@@ -149,6 +149,10 @@ def sparse_update(store: RowStore, unique_keys: np.ndarray, grad: np.ndarray, op
     uk = np.ascontiguousarray(unique_keys, dtype=np.uint32)
     if OPT[opt] == 1 and store.state is None:
         store.state = np.zeros(store.n, dtype=np.float32)
+    if OPT[opt] == 2 and store.state is None:
+        store.state = np.zeros((store.n, D), dtype=np.float32)
+    if OPT[opt] == 2:
+        assert store.state.shape == (store.n, D) and store.state.flags["C_CONTIGUOUS"]
     rc = _lib().oracle_sparse_update(OPT[opt], lr, eps, D, store.dtype, store.n, _p(store.keys), _p(store.vals),
                                      _p(store.state), _p(uk), int(uk.shape[0]), _p(g))
     _check(rc, "oracle_sparse_update")

@@ -218,17 +218,20 @@ int oracle_grad_reduce(int32_t T, int32_t B, const int32_t* offsets, int32_t D, 
 /* ------------------------------------------------------------ optimizer */
 
 /* One step on the rows unique_keys[0..U) with gradient rows grad[u][.]:
- *   opt 0, SGD:                 W[r] <- W[r] - lr * g
- *   opt 1, row-wise Adagrad:    h_r <- h_r + (1/D) sum_d g[d]^2
- *                               W[r] <- W[r] - lr * g / (sqrt(h_r) + eps)
- * state is indexed like the store's slots.  W is rounded once to fp32 (then
- * to bf16 for bf16 tables); h is stored as fp32, the unrounded h is used for
- * the same step's W. */
+ *   opt 0, SGD:                     W[r] <- W[r] - lr * g
+ *   opt 1, row-wise Adagrad:        h_r <- h_r + (1/D) sum_d g[d]^2
+ *                                   W[r] <- W[r] - lr * g / (sqrt(h_r) + eps)
+ *   opt 2, element-wise Adagrad:    h_r[d] <- h_r[d] + g[d]^2
+ *   (Duchi, Hazan and Singer 2011)  W[r][d] <- W[r][d] - lr * g[d] / (sqrt(h_r[d]) + eps)
+ * state is indexed like the store's slots (opt 1: one value per slot, opt 2:
+ * D values per slot).  W is rounded once to fp32 (then to bf16 for bf16
+ * tables); h is stored as fp32, the unrounded h is used for the same step's
+ * W. */
 int oracle_sparse_update(int32_t opt, float lr, float eps, int32_t D, int32_t dtype, int64_t store_n,
                          const uint32_t* store_keys, void* store_vals, float* state, const uint32_t* unique_keys,
                          int32_t U, const double* grad) {
-  if ((opt != 0 && opt != 1) || D < 1 || U < 0) return ORC_BAD_ARG;
-  if (opt == 1 && state == NULL) return ORC_BAD_ARG;
+  if (opt < 0 || opt > 2 || D < 1 || U < 0) return ORC_BAD_ARG;
+  if (opt != 0 && state == NULL) return ORC_BAD_ARG;
   store_t s = {store_n, store_keys, D, dtype};
   for (int32_t u = 0; u < U; ++u) {
     int64_t slot = store_slot(&s, unique_keys[u]);
@@ -243,6 +246,12 @@ int oracle_sparse_update(int32_t opt, float lr, float eps, int32_t D, int32_t dt
       denom = sqrt(h) + (double)eps;
     }
     for (int32_t d = 0; d < D; ++d) {
+      if (opt == 2) {
+        float* hp = state + slot * (int64_t)D + d;
+        double h = (double)*hp + g[d] * g[d];
+        *hp = (float)h;
+        denom = (double)eps + sqrt(h);
+      }
       double w = store_get(&s, store_vals, slot, d);
       store_put(&s, store_vals, slot, d, w - (double)lr * g[d] / denom);
     }

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libemb.so")
 EMB_OK, EMB_EINVAL, EMB_EWORKSPACE, EMB_EUNSUPPORTED, EMB_EHIP = range(5)
 FP32, BF16 = 0, 1
 POOL = {"sum": 0, "mean": 1}
-OPT = {"sgd": 0, "adagrad": 1}
+OPT = {"sgd": 0, "adagrad": 1, "adagrad_ew": 2}
 DTYPE = {"fp32": FP32, "bf16": BF16}
 
 EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_grad_reduce",

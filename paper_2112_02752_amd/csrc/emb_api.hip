@@ -59,8 +59,9 @@ emb_status check_ws(const void* ws, size_t ws_bytes, int64_t N, int64_t M, int32
 
 emb_status check_update(const emb_update* u) {
   if (u == nullptr) return EMB_EINVAL;
-  if (u->opt != EMB_OPT_SGD && u->opt != EMB_OPT_ADAGRAD_ROWWISE) return EMB_EINVAL;
-  if (u->opt == EMB_OPT_ADAGRAD_ROWWISE && u->state == nullptr) return EMB_EINVAL;
+  if (u->opt != EMB_OPT_SGD && u->opt != EMB_OPT_ADAGRAD_ROWWISE && u->opt != EMB_OPT_ADAGRAD_ELEMENTWISE)
+    return EMB_EINVAL;
+  if (u->opt != EMB_OPT_SGD && u->state == nullptr) return EMB_EINVAL;
   return EMB_OK;
 }
 

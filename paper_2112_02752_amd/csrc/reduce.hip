@@ -187,6 +187,31 @@ __device__ __forceinline__ void apply_row(const Upd& up, float* grad_rows, int64
     step = up.lr / (sqrtf(h) + up.eps);
   }
   TW* wp = reinterpret_cast<TW*>(up.W) + (size_t)r * (size_t)D;
+  if (up.opt == EMB_OPT_ADAGRAD_ELEMENTWISE) {
+    // one accumulator per element, read here (row r has no other owner)
+    float* hp = up.state + (size_t)r * (size_t)D;
+    float hv[NV][4];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c0 = (v * G + sub) * 4;
+      if (c0 < D) Row4<float>::load(hp + c0, hv[v]);
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c0 = (v * G + sub) * 4;
+      if (c0 < D) {
+        float w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          hv[v][e] += acc[v][e] * acc[v][e];
+          w[e] = pre.w[v][e] - up.lr * acc[v][e] / (sqrtf(hv[v][e]) + up.eps);
+        }
+        Row4<float>::store(hp + c0, hv[v]);
+        Row4<TW>::store(wp + c0, w);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int v = 0; v < NV; ++v) {
     const int c0 = (v * G + sub) * 4;

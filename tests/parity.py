@@ -6,7 +6,8 @@ Comparison rule (row-wise infinity-norm relative error, integer outputs
 bit-exact):
   rel = max over rows of  max_d |x - y| / max_d |y|
 fp32 results must meet rel <= 1e-5; bf16 table rows rel <= 1e-2 (one bf16
-ulp is 2^-8 of the value); Adagrad state elementwise rel <= 1e-5.
+ulp is 2^-8 of the value); row-wise Adagrad state elementwise rel <= 1e-5,
+element-wise Adagrad state rows by the row-norm rule.
 """
 from __future__ import annotations
 
@@ -74,12 +75,18 @@ class DeviceLayer:
         return self.state.index_select(0, k).cpu().numpy()
 
 
-def device_layer_from_workload(w: synth.Workload, device="cuda") -> DeviceLayer:
+def device_layer_from_workload(w: synth.Workload, device="cuda", h0: float = 0.0) -> DeviceLayer:
+    """Device table of a workload; Adagrad state filled with h0 ([R] row-wise,
+    [R][D] element-wise)."""
     torch = torch_mod()
     tdt = torch.float32 if w.dtype == "fp32" else torch.bfloat16
     W = torch.empty((w.total_rows, w.dim), dtype=tdt, device=device)
     synth.fill_device_weights(w, W.data_ptr(), int(torch.cuda.current_stream().cuda_stream))
-    state = torch.zeros(w.total_rows, dtype=torch.float32, device=device) if w.opt == "adagrad" else None
+    state = None
+    if w.opt == "adagrad":
+        state = torch.full((w.total_rows,), h0, dtype=torch.float32, device=device)
+    elif w.opt == "adagrad_ew":
+        state = torch.full((w.total_rows, w.dim), h0, dtype=torch.float32, device=device)
     return DeviceLayer([int(x) for x in w.row_offset], w.dim, w.dtype, W, state)
 
 
@@ -195,6 +202,9 @@ def check_rows(dl: DeviceLayer, store: oracle.RowStore, keys: np.ndarray, opt: s
         h_ref = store.state[slots].astype(np.float64)
         rel = np.abs(h_dev - h_ref) / np.maximum(np.abs(h_ref), 1e-30)
         assert rel.max() <= TOL_FP32, f"adagrad state rel err {rel.max()}"
+    elif opt == "adagrad_ew":
+        r = rel_rownorm(dl.state_rows(keys), store.state[slots])
+        assert r <= TOL_FP32, f"element-wise adagrad state rel err {r}"
 
 
 def check_untouched(dl: DeviceLayer, w: synth.Workload, touched: np.ndarray, n: int = 10_000, seed: int = 0):
@@ -207,15 +217,20 @@ def check_untouched(dl: DeviceLayer, w: synth.Workload, touched: np.ndarray, n: 
     np.testing.assert_array_equal(dl.rows(cand), synth.weight_rows(w, cand))
 
 
-def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="cuda", concurrent: bool = False):
+def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="cuda", concurrent: bool = False,
+                 h0: float = 0.0):
     """Full-size parity of `steps` consecutive steps of a workload (serial
-    calls, or Layer.step's concurrent schedule)."""
-    dl = device_layer_from_workload(w, device)
+    calls, or Layer.step's concurrent schedule); Adagrad state starts at h0."""
+    dl = device_layer_from_workload(w, device, h0)
     batches = [synth.make_batch(w, s) for s in range(steps)]
     keys_all = [global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices) for b in batches]
     touched = np.unique(np.concatenate(keys_all)) if keys_all else np.zeros(0, np.uint32)
-    store = oracle.RowStore(synth.weight_rows(w, touched), keys=touched.astype(np.uint32),
-                            state=np.zeros(len(touched), np.float32) if w.opt == "adagrad" else None)
+    state = None
+    if w.opt == "adagrad":
+        state = np.full(len(touched), h0, np.float32)
+    elif w.opt == "adagrad_ew":
+        state = np.full((len(touched), w.dim), h0, np.float32)
+    store = oracle.RowStore(synth.weight_rows(w, touched), keys=touched.astype(np.uint32), state=state)
     nmax = max(len(b.indices) for b in batches)
     layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
                       concurrent=concurrent)
@@ -239,7 +254,9 @@ def run_case(row_offset, W_host: np.ndarray, offsets, indices, grad, B: int, poo
     ro = np.asarray(row_offset, dtype=np.int64)
     if opt == "adagrad" and state0 is None:
         state0 = np.zeros(W_host.shape[0], np.float32)
-    dl = device_layer_from_host(ro, W_host, state0 if opt == "adagrad" else None, device)
+    if opt == "adagrad_ew" and state0 is None:
+        state0 = np.zeros(W_host.shape, np.float32)
+    dl = device_layer_from_host(ro, W_host, state0 if opt != "sgd" else None, device)
     store = oracle.RowStore(W_host.copy(), state=state0.copy() if state0 is not None else None)
     g = gpu_step(dl, offsets, indices, grad, B, pool, opt, lr, eps, fused=fused)
     o_out, o_dd, o_gr = oracle.step(len(ro) - 1, ro, B, offsets, indices, grad, store, pool, opt, lr, eps)

@@ -288,6 +288,54 @@ def test_sort_tile_modes(bags, concurrent):
     parity.run_workload(w, steps=1, concurrent=concurrent)
 
 
+# ------------------------------------------------ element-wise Adagrad variant
+
+def _bf16_bits(Wf):
+    u = Wf.view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("pool,dtype,D,fused", [("sum", "fp32", 64, True), ("mean", "fp32", 16, True),
+                                                ("sum", "bf16", 128, True), ("sum", "fp32", 256, False)])
+def test_elementwise_adagrad_small(pool, dtype, D, fused):
+    """Element-wise Adagrad (state [R][D]).  The accumulators start at 1: from
+    zero, the first step moves an element by lr * g / (|g| + eps), whose sign
+    is that of a gradient sum that may cancel to rounding noise."""
+    _say(f"case elementwise adagrad pool={pool} dtype={dtype} D={D} fused={fused}")
+    rng = np.random.default_rng(40 + D)
+    rows = [3000, 700]
+    B = 300
+    off, idx = _rand_batch(rng, rows, B, 40, empty_frac=0.05, zipf=1.3)
+    Wf = rng.uniform(-0.5, 0.5, size=(sum(rows), D)).astype(np.float32)
+    W = _bf16_bits(Wf) if dtype == "bf16" else Wf
+    G = rng.standard_normal(size=(len(off) - 1, D)).astype(np.float32)
+    state0 = rng.uniform(0.5, 1.5, size=(sum(rows), D)).astype(np.float32)
+    parity.run_case(_row_offset(rows), W, off, idx, G, B, pool, "adagrad_ew", 0.01, 1e-8, state0=state0, fused=fused)
+
+
+def test_elementwise_adagrad_dyadic_from_zero():
+    """From zero accumulators on dyadic inputs: every gradient sum is exact, so
+    no sign is in doubt."""
+    _say("case elementwise adagrad dyadic from zero")
+    rng = np.random.default_rng(44)
+    rows = [2000, 900]
+    B, D = 400, 32
+    off, idx = _rand_batch(rng, rows, B, 8, empty_frac=0.1, zipf=1.5)
+    W = (rng.integers(-512, 512, size=(sum(rows), D)) / 1024.0).astype(np.float32)
+    G = (rng.integers(-64, 64, size=(len(off) - 1, D)) / 64.0).astype(np.float32)
+    parity.run_case(_row_offset(rows), W, off, idx, G, B, "sum", "adagrad_ew", 0.01, 1e-8)
+
+
+@pytest.mark.parametrize("name,steps", [("c2", 1), ("c3", 2)])
+def test_elementwise_adagrad_full_size(name, steps):
+    """The 8-table and the 50M-row workloads with element-wise Adagrad state
+    ([R][D] fp32, starting at 1)."""
+    import dataclasses
+    w = dataclasses.replace(synth.workload(name), opt="adagrad_ew", name=f"{name}-ew")
+    _say(f"case elementwise adagrad full size {name} x{steps}")
+    parity.run_workload(w, steps=steps, h0=1.0)
+
+
 def test_c5_three_consecutive_steps():
     w = synth.workload("c5")
     _say("case c5 x3 steps")

@@ -159,7 +159,7 @@ def test_dyadic_forward_is_exact(pool):
     np.testing.assert_array_equal(gr, (A.T @ G.astype(np.float64))[dd.unique_keys].astype(np.float32))
 
 
-@pytest.mark.parametrize("opt", ["sgd", "adagrad"])
+@pytest.mark.parametrize("opt", ["sgd", "adagrad", "adagrad_ew"])
 def test_sparse_step_equals_dense_step(opt):
     """A dense optimizer step over every row changes exactly the touched rows,
     by the same amounts as the sparse step."""
@@ -168,7 +168,7 @@ def test_sparse_step_equals_dense_step(opt):
     T = len(ro) - 1
     R = W.shape[0]
     lr, eps = np.float32(0.05), np.float32(1e-8)
-    state0 = rng.uniform(0, 2, size=R).astype(np.float32)
+    state0 = rng.uniform(0, 2, size=(R, W.shape[1]) if opt == "adagrad_ew" else R).astype(np.float32)
     st = RowStore(W.copy(), state=state0.copy())
     oracle.step(T, ro, B, off, idx, G, st, "sum", opt, float(lr), float(eps))
     A = incidence(ro, B, off, idx, "sum")
@@ -177,6 +177,9 @@ def test_sparse_step_equals_dense_step(opt):
     if opt == "sgd":
         W_dense = W64 - np.float64(lr) * g
         h = state0.astype(np.float64)
+    elif opt == "adagrad_ew":
+        h = state0.astype(np.float64) + g * g
+        W_dense = W64 - np.float64(lr) * g / (np.sqrt(h) + np.float64(eps))
     else:
         h = state0.astype(np.float64) + (g * g).sum(1) / W.shape[1]
         W_dense = W64 - np.float64(lr) * g / (np.sqrt(h)[:, None] + np.float64(eps))
@@ -185,7 +188,7 @@ def test_sparse_step_equals_dense_step(opt):
     np.testing.assert_array_equal(st.vals[untouched], W[untouched])
     np.testing.assert_array_equal(st.state[untouched], state0[untouched])
     np.testing.assert_allclose(st.vals[touched], W_dense[touched], rtol=1e-6, atol=1e-7)
-    if opt == "adagrad":
+    if opt != "sgd":
         np.testing.assert_allclose(st.state[touched], h[touched], rtol=1e-6)
 
 
@@ -337,6 +340,38 @@ def test_forward_and_grad_match_torch_embedding_bag(pool):
     dd = oracle.unique_ids(1, ro, B, off, idx)
     _, acc = oracle.grad_reduce(1, B, off, G, pool, dd)
     np.testing.assert_allclose(acc, Wt.grad.numpy()[dd.unique_keys], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("pool,h0", [("sum", 0.0), ("mean", 0.0), ("sum", 0.5)])
+def test_elementwise_adagrad_matches_torch_optim(pool, h0):
+    """Three steps of element-wise Adagrad against torch.optim.Adagrad (its
+    update with lr_decay = weight_decay = 0 is the textbook one: eps outside the
+    square root) on a dense float64 table whose gradient comes from torch's
+    own embedding_bag backward; each step's batch is a fresh one."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(31)
+    rows, D, B = 41, 8, 25
+    ro = np.array([0, rows], np.int64)
+    W0 = rng.uniform(-1, 1, size=(rows, D)).astype(np.float32)
+    Wt = torch.tensor(W0.astype(np.float64), requires_grad=True)
+    opt_t = torch.optim.Adagrad([Wt], lr=0.05, eps=1e-8, initial_accumulator_value=h0)
+    st = RowStore(W0.copy(), state=np.full((rows, D), h0, np.float32))
+    touched = set()
+    for s in range(3):
+        _, _, off, idx, _, G = random_case(rng, T=1, rows=(rows,), D=D, B=B, dyadic=False)
+        touched |= set(int(k) for k in idx)
+        oracle.step(1, ro, B, off, idx, G, st, pool, "adagrad_ew", 0.05, 1e-8)
+        opt_t.zero_grad()
+        out_t = torch.nn.functional.embedding_bag(torch.tensor(idx.astype(np.int64)), Wt,
+                                                  torch.tensor(off[:-1].astype(np.int64)), mode=pool)
+        out_t.backward(torch.tensor(G.astype(np.float64)))
+        opt_t.step()
+    # the oracle rounds W and h to fp32 after every step, torch keeps float64
+    np.testing.assert_allclose(st.vals, Wt.detach().numpy(), rtol=1e-5, atol=1e-6)
+    h_t = opt_t.state[Wt]["sum"].numpy()
+    np.testing.assert_allclose(st.state, h_t, rtol=1e-5, atol=1e-6)
+    untouched = sorted(set(range(rows)) - touched)
+    np.testing.assert_array_equal(st.vals[untouched], W0[untouched])
 
 
 # ------------------------------------------------------------ sparse store

@@ -31,6 +31,9 @@ MUTANTS = {
     "adagrad_old_state": ("denom = sqrt(h) + (double)eps;", "denom = sqrt((double)state[slot] - sq / (double)D) + (double)eps;"),
     "update_sign": ("store_put(&s, store_vals, slot, d, w - (double)lr * g[d] / denom);",
                     "store_put(&s, store_vals, slot, d, w + (double)lr * g[d] / denom);"),
+    "adagrad_ew_mean_over_D": ("double h = (double)*hp + g[d] * g[d];",
+                               "double h = (double)*hp + g[d] * g[d] / (double)D;"),
+    "adagrad_ew_old_state": ("denom = (double)eps + sqrt(h);", "denom = (double)eps + sqrt(h - g[d] * g[d]);"),
     "counts_off_by_one": ("counts[u] = seg_offsets[u + 1] - seg_offsets[u];",
                           "counts[u] = seg_offsets[u + 1] - seg_offsets[u] + (u == 0);"),
 }
@@ -71,6 +74,7 @@ def _run_pins(so_path):
             lambda: T.test_sparse_step_equals_dense_step("adagrad"),
             lambda: T.test_rowwise_adagrad_closed_form_constant_row(0.75),
             lambda: T.test_adagrad_accumulates_across_steps(),
+            lambda: T.test_elementwise_adagrad_matches_torch_optim("sum", 0.0),
         ]
         for p in pins:
             try:

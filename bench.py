@@ -52,6 +52,8 @@ def parse():
                          "batch k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
+    ap.add_argument("--route-ranks", type=int, default=8,
+                    help="also time emb_route_ids of the same batches over this many equal row ranges (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for counter calibration)")
@@ -284,6 +286,34 @@ def main():
     copy_gbs = 5 * 2 * (1 << 30) / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del flush, dst
 
+    # routing of the same batches to the owners of equal row ranges: the step
+    # before the forward when the table is sharded over that many devices
+    routing = None
+    if args.route_ranks > 0:
+        Wr = args.route_ranks
+        shard = [w.total_rows * r // Wr for r in range(Wr + 1)]
+        i32 = dict(dtype=torch.int32, device=dev)
+        rcnt = torch.empty(Wr, **i32)
+        rids, rpos, rbag = (torch.empty(nmax, **i32) for _ in range(3))
+        rws = torch.empty(emb.route_workspace_size(nmax, w.num_bags, Wr), dtype=torch.uint8, device=dev)
+        for i in range(args.warmup):
+            emb.route_ids(tables, dev_batches[i][0], shard, rcnt, rids, rpos, rbag, rws, sp)
+        rev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for k, i in enumerate(range(args.warmup, total)):
+            rev[k][0].record(stream)
+            emb.route_ids(tables, dev_batches[i][0], shard, rcnt, rids, rpos, rbag, rws, sp)
+            rev[k][1].record(stream)
+        torch.cuda.synchronize()
+        r_s = float(np.median([e[0].elapsed_time(e[1]) * 1e-3 for e in rev]))
+        r_bytes = 4 * (w.num_bags + 1) + 4 * np.mean([dev_batches[i][2] for i in range(args.warmup, total)]) * 4 \
+            + 4 * Wr
+        routing = {"ranks": Wr, "shard": "equal row ranges", "kernels": "k_route_count, k_route_scan, "
+                   "k_route_scatter (emb_route_ids)", "median_us": r_s * 1e6,
+                   "ids_per_s": float(np.mean([dev_batches[i][2] for i in range(args.warmup, total)])) / r_s,
+                   "bytes_per_launch": float(r_bytes), "achieved_GBs": r_bytes / r_s / 1e9,
+                   "frac": r_bytes / r_s / 1e9 / HBM_PEAK_GBS}
+
     n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
 
     # unique counts of the timed batches (for the byte models)
@@ -337,6 +367,7 @@ def main():
                     "with_phase_events_median": float(np.median(phased_step_s)) * 1e6},
         "cold": None if cold is None else dict(cold, lookups_per_s=N_avg * 1e6 / cold["median_us"]),
         "achievable_copy_GBs": copy_gbs,
+        "routing": routing,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

@@ -60,6 +60,7 @@ typedef enum { EMB_POOL_SUM = 0, EMB_POOL_MEAN = 1 } emb_pool;
 typedef enum { EMB_OPT_SGD = 0, EMB_OPT_ADAGRAD_ROWWISE = 1, EMB_OPT_ADAGRAD_ELEMENTWISE = 2 } emb_opt;
 
 #define EMB_MAX_TABLES 256
+#define EMB_MAX_RANKS 256
 
 /* All tables of one call share dim and dtype and are stacked row-wise in one
  * buffer: the rows of table t are global rows row_offset[t] .. row_offset[t+1]-1. */
@@ -151,6 +152,36 @@ emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int
  * distinct (one owner per row). */
 emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update, const uint32_t* unique_keys,
                              const int32_t* num_unique, int64_t max_unique, const float* grad_rows, void* stream);
+
+/* Bytes of workspace emb_route_ids needs for batches of up to num_indices
+ * ids and num_bags bags over world_size ranks (0 for invalid sizes). */
+size_t emb_route_workspace_size(int64_t num_indices, int64_t num_bags, int32_t world_size);
+
+/* Routing of the batch's ids to the owners of a row-range sharding of the
+ * stacked tables: the step before the forward when the layer is spread over
+ * world_size devices (the paper's distributed sparse lookup layer, its
+ * Introduction), rank r owning global rows [shard_start[r], shard_start[r+1]).
+ * Table-wise placement is the case of bounds at table starts.
+ *   key[j]          = row_offset[t(j)] + indices[j]
+ *   owner(j)        = the r with shard_start[r] <= key[j] < shard_start[r+1]
+ * The send order lists the positions rank by rank, and in position order
+ * within a rank.  Outputs (device, caller-owned):
+ *   send_counts[r]  positions owned by rank r, int32 [world_size]
+ *   send_ids[k]     key - shard_start[owner] of the k-th sent position, int32 [N]
+ *   send_pos[k]     its position j, int32 [N]
+ *   send_bag[k]     the bag holding it, int32 [N]
+ * Rank r's range of the send order starts at the sum of send_counts[< r].
+ * Within it the positions of one bag are consecutive (a bag's positions are),
+ * so the runs of equal send_bag are the bag fragments the owner pools from its
+ * rows (sum pooling); adding the fragments' pooled rows by bag (then scaling
+ * by 1 / bag length for mean pooling) reassembles the forward.
+ * shard_start: host [world_size + 1], shard_start[0] = 0, nondecreasing,
+ * shard_start[world_size] = R; 1 <= world_size <= EMB_MAX_RANKS, else
+ * EMB_EINVAL.  ws: device, ws_bytes >= emb_route_workspace_size(N, M, W).
+ * Device contents are not validated (emb_validate_batch). */
+emb_status emb_route_ids(const emb_tables* tables, const emb_batch* batch, int32_t world_size,
+                         const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids, int32_t* send_pos,
+                         int32_t* send_bag, void* ws, size_t ws_bytes, void* stream);
 
 /* Debug check of device contents (never on the timed path): flag[0] (device
  * int32) is set to 0 if the batch is well formed, else to a bitwise OR of

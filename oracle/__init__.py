@@ -51,6 +51,8 @@ def _lib():
         L.oracle_unique_ids.argtypes = [i32, vp, i32, vp, vp, vp, vp, vp, vp, vp]
         L.oracle_grad_reduce.restype = ctypes.c_int
         L.oracle_grad_reduce.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp, i32, vp, vp]
+        L.oracle_route_ids.restype = ctypes.c_int
+        L.oracle_route_ids.argtypes = [i32, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp]
         L.oracle_sparse_update.restype = ctypes.c_int
         L.oracle_sparse_update.argtypes = [i32, f32, f32, i32, i32, i64, vp, vp, vp, vp, i32, vp]
         _L = L
@@ -156,6 +158,29 @@ def sparse_update(store: RowStore, unique_keys: np.ndarray, grad: np.ndarray, op
     rc = _lib().oracle_sparse_update(OPT[opt], lr, eps, D, store.dtype, store.n, _p(store.keys), _p(store.vals),
                                      _p(store.state), _p(uk), int(uk.shape[0]), _p(g))
     _check(rc, "oracle_sparse_update")
+
+
+@dataclass
+class Route:
+    send_counts: np.ndarray  # int32 [W]
+    send_ids: np.ndarray     # int32 [N], local row ids in send order
+    send_pos: np.ndarray     # int32 [N], position of each sent id
+    send_bag: np.ndarray     # int32 [N], bag of each sent id
+
+
+def route_ids(num_tables: int, row_offset: np.ndarray, bags_per_table: int, offsets: np.ndarray,
+              indices: np.ndarray, shard_start: np.ndarray) -> Route:
+    """Ids of a batch bucketed by the owner rank of a row-range sharding
+    (rank r owns global rows [shard_start[r], shard_start[r+1]))."""
+    N = int(indices.shape[0])
+    W = int(len(shard_start)) - 1
+    ss = np.ascontiguousarray(shard_start, dtype=np.int64)
+    cnt = np.zeros(max(W, 1), np.int32)
+    ids, pos, bag = (np.zeros(max(N, 1), np.int32) for _ in range(3))
+    rc = _lib().oracle_route_ids(num_tables, _p(row_offset), bags_per_table, _p(offsets), _p(indices), W, _p(ss),
+                                 _p(cnt), _p(ids), _p(pos), _p(bag))
+    _check(rc, "oracle_route_ids")
+    return Route(cnt[:W].copy(), ids[:N].copy(), pos[:N].copy(), bag[:N].copy())
 
 
 def step(num_tables: int, row_offset: np.ndarray, bags_per_table: int, offsets: np.ndarray, indices: np.ndarray,

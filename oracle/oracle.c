@@ -258,3 +258,39 @@ int oracle_sparse_update(int32_t opt, float lr, float eps, int32_t D, int32_t dt
   }
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------- routing */
+
+/* Routing of a batch's ids to the owners of a row-range sharding (the step
+ * before the forward when the layer is spread over several devices): rank r
+ * owns global rows [shard_start[r], shard_start[r+1]).  For each position j,
+ * in position order, owner(j) is the rank whose range holds key[j]; the send
+ * order lists the positions rank by rank, in position order within a rank.
+ * send_counts[r] = positions owned by r; for the k-th sent position j:
+ * send_ids[k] = key[j] - shard_start[owner(j)], send_pos[k] = j,
+ * send_bag[k] = the bag holding j. */
+int oracle_route_ids(int32_t T, const int64_t* row_offset, int32_t B, const int32_t* offsets, const int32_t* idx,
+                     int32_t W, const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids,
+                     int32_t* send_pos, int32_t* send_bag) {
+  int rc = validate(T, row_offset, B, offsets, idx);
+  if (rc) return rc;
+  if (W < 1 || shard_start[0] != 0 || shard_start[W] != row_offset[T]) return ORC_BAD_ARG;
+  for (int32_t r = 0; r < W; ++r)
+    if (shard_start[r + 1] < shard_start[r]) return ORC_BAD_ARG;
+  int64_t M = (int64_t)T * B;
+  int64_t k = 0;
+  for (int32_t r = 0; r < W; ++r) {
+    send_counts[r] = 0;
+    for (int64_t m = 0; m < M; ++m)
+      for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {
+        int64_t key = row_offset[m / B] + idx[j];
+        if (key < shard_start[r] || key >= shard_start[r + 1]) continue;
+        send_ids[k] = (int32_t)(key - shard_start[r]);
+        send_pos[k] = j;
+        send_bag[k] = (int32_t)m;
+        ++k;
+        ++send_counts[r];
+      }
+  }
+  return ORC_OK;
+}

@@ -26,7 +26,8 @@ OPT = {"sgd": 0, "adagrad": 1, "adagrad_ew": 2}
 DTYPE = {"fp32": FP32, "bf16": BF16}
 
 EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_grad_reduce",
-            "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_status_string")
+            "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_status_string",
+            "emb_route_workspace_size", "emb_route_ids")
 
 
 class EmbError(RuntimeError):
@@ -75,6 +76,10 @@ def lib():
         L.emb_grad_reduce.argtypes = [T, B, i32, vp, vp, vp, vp, vp, vp, Up, vp, sz, vp]
         L.emb_sparse_update.restype = i32
         L.emb_sparse_update.argtypes = [T, Up, vp, vp, i64, vp, vp]
+        L.emb_route_workspace_size.restype = sz
+        L.emb_route_workspace_size.argtypes = [i64, i64, i32]
+        L.emb_route_ids.restype = i32
+        L.emb_route_ids.argtypes = [T, B, i32, ctypes.POINTER(ctypes.c_int64), vp, vp, vp, vp, vp, sz, vp]
         L.emb_validate_batch.restype = i32
         L.emb_validate_batch.argtypes = [T, B, vp, vp]
         L.emb_workspace_error_offset.restype = sz
@@ -192,6 +197,21 @@ def sparse_update(tables: Tables, opt: str, lr: float, eps: float, state, unique
 def validate_batch(tables: Tables, batch: Batch, flag, stream=None) -> None:
     _check("emb_validate_batch", lib().emb_validate_batch(ctypes.byref(tables.c()), ctypes.byref(batch.c()),
                                                           _ptr(flag), _stream(stream)))
+
+
+def route_workspace_size(num_indices: int, num_bags: int, world_size: int) -> int:
+    return int(lib().emb_route_workspace_size(num_indices, num_bags, world_size))
+
+
+def route_ids(tables: Tables, batch: Batch, shard_start: Sequence[int], send_counts, send_ids, send_pos, send_bag,
+              ws, stream=None) -> None:
+    """Bucket the batch's ids by the owner rank of a row-range sharding
+    (rank r owns global rows [shard_start[r], shard_start[r+1]))."""
+    W = len(shard_start) - 1
+    ss = (ctypes.c_int64 * len(shard_start))(*[int(x) for x in shard_start])
+    _check("emb_route_ids", lib().emb_route_ids(
+        ctypes.byref(tables.c()), ctypes.byref(batch.c()), W, ss, _ptr(send_counts), _ptr(send_ids), _ptr(send_pos),
+        _ptr(send_bag), _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
 
 
 def workspace_error_offset() -> int:

@@ -231,6 +231,53 @@ emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update,
   return hip_status(launch_sparse_update(p, (hipStream_t)stream));
 }
 
+size_t emb_route_workspace_size(int64_t num_indices, int64_t num_bags, int32_t world_size) {
+  if (num_indices < 0 || num_indices >= kMaxIndices || num_bags < 0 || num_bags >= ((int64_t)1 << 31) ||
+      world_size < 1 || world_size > kMaxRanks)
+    return 0;
+  const RoutePlan plan = route_plan(num_indices, num_bags);
+  return align256(sizeof(int32_t) * (size_t)world_size * (size_t)(plan.nblocks > 0 ? plan.nblocks : 1));
+}
+
+emb_status emb_route_ids(const emb_tables* tables, const emb_batch* batch, int32_t world_size,
+                         const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids, int32_t* send_pos,
+                         int32_t* send_bag, void* ws, size_t ws_bytes, void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  st = check_batch(batch, tables->num_tables, &M);
+  if (st != EMB_OK) return st;
+  if (world_size < 1 || world_size > kMaxRanks || shard_start == nullptr || send_counts == nullptr) return EMB_EINVAL;
+  if (shard_start[0] != 0 || shard_start[world_size] != R) return EMB_EINVAL;
+  ShardBounds sb;
+  for (int r = 0; r < world_size; ++r) {
+    if (shard_start[r + 1] < shard_start[r]) return EMB_EINVAL;
+    sb.off[r] = (uint32_t)shard_start[r];
+  }
+  sb.off[world_size] = (uint32_t)R;
+  const int64_t N = batch->num_indices;
+  if (N > 0 && (send_ids == nullptr || send_pos == nullptr || send_bag == nullptr || ws == nullptr))
+    return EMB_EINVAL;
+  if (ws_bytes < emb_route_workspace_size(N, M, world_size)) return EMB_EWORKSPACE;
+  RouteLaunch p{};
+  p.offsets = batch->offsets;
+  p.idx = batch->indices;
+  p.ro = ro;
+  p.sb = sb;
+  p.B = batch->bags_per_table;
+  p.M = M;
+  p.W = world_size;
+  p.N = N;
+  p.ws = ws;
+  p.send_counts = send_counts;
+  p.send_ids = send_ids;
+  p.send_pos = send_pos;
+  p.send_bag = send_bag;
+  return hip_status(launch_route(p, (hipStream_t)stream));
+}
+
 emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, int32_t* flag, void* stream) {
   TableOffsets ro;
   int64_t R = 0;

@@ -166,6 +166,17 @@ struct TableOffsets {
   uint32_t off[EMB_MAX_TABLES + 1];
 };
 
+// Routing: ranks of a sharding, their first global rows (by value in kernel
+// arguments), bags one routing block covers at most, positions it aims at,
+// threads of a per-rank scan block.
+constexpr int kMaxRanks = EMB_MAX_RANKS;
+struct ShardBounds {
+  uint32_t off[kMaxRanks + 1];
+};
+constexpr int kRouteBags = 1024;
+constexpr int kRoutePositions = 256;
+constexpr int kRouteScanThreads = 1024;
+
 // ------------------------------------------------------------ device helpers
 
 // number of set bits of `mask` below this lane

@@ -77,6 +77,26 @@ struct UpdateLaunch {
 hipError_t launch_sparse_update(const UpdateLaunch& p, hipStream_t s);
 int reduce_max_dim();
 
+struct RoutePlan {
+  int32_t bags_per_block, nblocks;
+};
+RoutePlan route_plan(int64_t N, int64_t M);
+
+struct RouteLaunch {
+  const int32_t* offsets;
+  const int32_t* idx;
+  TableOffsets ro;
+  ShardBounds sb;
+  int32_t B, M, W;
+  int64_t N;
+  void* ws;  // [W][nblocks] int32
+  int32_t* send_counts;
+  int32_t* send_ids;
+  int32_t* send_pos;
+  int32_t* send_bag;
+};
+hipError_t launch_route(const RouteLaunch& p, hipStream_t s);
+
 struct ValidateLaunch {
   const int32_t* offsets;
   const int32_t* idx;

@@ -127,6 +127,29 @@ def test_grad_reduce_argument_errors():
     assert call(nbytes=16) == emb.EMB_EWORKSPACE
 
 
+def test_route_argument_errors():
+    L = emb.lib()
+    t, b = _tables(row_offset=(0, 100)), _batch(n=1000)
+    need = emb.route_workspace_size(1000, 4, 4)
+    assert need > 0
+    assert emb.route_workspace_size(1000, 4, 0) == 0
+    assert emb.route_workspace_size(1000, 4, 257) == 0
+
+    def call(bounds=(0, 10, 50, 60, 100), nbytes=None, counts=0x5000, ids=0x6000):
+        W = len(bounds) - 1
+        ss = (ctypes.c_int64 * len(bounds))(*bounds)
+        return L.emb_route_ids(ctypes.byref(t), ctypes.byref(b), W, ss, counts, ids, 0x7000, 0x8000, 0x100000,
+                               need if nbytes is None else nbytes, None)
+
+    assert call(bounds=(1, 50, 100)) == emb.EMB_EINVAL       # first bound not 0
+    assert call(bounds=(0, 50, 99)) == emb.EMB_EINVAL        # last bound not R
+    assert call(bounds=(0, 60, 50, 100)) == emb.EMB_EINVAL   # decreasing
+    assert call(bounds=(0,)) == emb.EMB_EINVAL               # no rank
+    assert call(counts=None) == emb.EMB_EINVAL
+    assert call(ids=None) == emb.EMB_EINVAL
+    assert call(nbytes=need - 1) == emb.EMB_EWORKSPACE
+
+
 def test_sparse_update_argument_errors():
     L = emb.lib()
     t = _tables()

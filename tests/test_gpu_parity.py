@@ -426,3 +426,118 @@ def test_pipelined_schedule_equals_serial(lookahead):
     np.testing.assert_array_equal(s0, s1)
     for a, b in zip(o0, o1):
         np.testing.assert_array_equal(a, b)
+
+
+# ------------------------------------------------------------------ routing
+
+def _route_gpu(row_offset, B, off, idx, shard, W_dev=None):
+    import torch
+    import paper_2112_02752_amd as emb
+    N, M = len(idx), len(off) - 1
+    Wr = len(shard) - 1
+    dev = "cuda"
+    if W_dev is None:
+        W_dev = torch.empty((int(row_offset[-1]), 4), dtype=torch.float32, device=dev)  # never read
+    tables = emb.Tables(W_dev, [int(x) for x in row_offset])
+    b = emb.Batch(torch.from_numpy(np.ascontiguousarray(off, np.int32)).to(dev),
+                  torch.from_numpy(np.ascontiguousarray(idx, np.int32)).to(dev), B)
+    i32 = dict(dtype=torch.int32, device=dev)
+    cnt = torch.full((Wr,), -1, **i32)
+    ids, pos, bag = (torch.full((max(N, 1),), -1, **i32) for _ in range(3))
+    ws = torch.empty(emb.route_workspace_size(N, M, Wr), dtype=torch.uint8, device=dev)
+    emb.route_ids(tables, b, shard, cnt, ids, pos, bag, ws)
+    torch.cuda.synchronize()
+    return cnt.cpu().numpy(), ids[:N].cpu().numpy(), pos[:N].cpu().numpy(), bag[:N].cpu().numpy()
+
+
+def _check_route(row_offset, B, off, idx, shard):
+    import oracle
+    T = len(row_offset) - 1
+    ref = oracle.route_ids(T, np.asarray(row_offset, np.int64), B, np.ascontiguousarray(off, np.int32),
+                           np.ascontiguousarray(idx, np.int32), np.asarray(shard, np.int64))
+    cnt, ids, pos, bag = _route_gpu(row_offset, B, off, idx, shard)
+    np.testing.assert_array_equal(cnt, ref.send_counts)
+    np.testing.assert_array_equal(pos, ref.send_pos)
+    np.testing.assert_array_equal(ids, ref.send_ids)
+    np.testing.assert_array_equal(bag, ref.send_bag)
+
+
+@pytest.mark.parametrize("Wr,seed", [(1, 0), (3, 1), (8, 2), (64, 3), (256, 4)])
+def test_route_small(Wr, seed):
+    """Random bounds (some ranges empty) over three tables, empty bags."""
+    _say(f"case route W={Wr}")
+    rng = np.random.default_rng(100 + seed)
+    rows = [5000, 800, 12000]
+    B = 700
+    off, idx = _rand_batch(rng, rows, B, 40, empty_frac=0.1, zipf=1.2)
+    R = sum(rows)
+    cuts = np.sort(rng.integers(0, R + 1, size=Wr - 1))
+    shard = [0] + [int(x) for x in cuts] + [R]
+    _check_route(_row_offset(rows), B, off, idx, shard)
+
+
+def test_route_tablewise_and_empty_batch():
+    _say("case route table-wise / empty batch")
+    rng = np.random.default_rng(7)
+    rows = [300, 5, 9000, 40]
+    B = 500
+    off, idx = _rand_batch(rng, rows, B, 20, empty_frac=0.3)
+    ro = _row_offset(rows)
+    _check_route(ro, B, off, idx, [int(x) for x in ro])
+    off0 = np.zeros(len(rows) * B + 1, np.int32)
+    cnt, _, _, _ = _route_gpu(ro, B, off0, np.zeros(0, np.int32), [0, 1000, int(ro[-1])])
+    np.testing.assert_array_equal(cnt, [0, 0])
+
+
+@pytest.mark.parametrize("name,Wr", [("c3", 8), ("c5", 8), ("c4", 0)])
+def test_route_full_size(name, Wr):
+    """Full-size batches: equal row ranges over Wr ranks, or (Wr = 0) one rank
+    per table."""
+    w = synth.workload(name)
+    _say(f"case route full size {name} W={Wr or w.num_tables}")
+    b = synth.make_batch(w, 0)
+    R = w.total_rows
+    shard = [int(x) for x in w.row_offset] if Wr == 0 else [R * r // Wr for r in range(Wr + 1)]
+    _check_route(w.row_offset, w.bags_per_table, b.offsets, b.indices, shard)
+
+
+@pytest.mark.parametrize("pool", ["sum", "mean"])
+def test_route_fragments_reassemble_forward_on_gpu(pool):
+    """The sharded forward on one GPU: each rank pools its fragments from its
+    own slice of the table with emb_pool_fwd (sum), the fragments' rows are
+    added by bag (and scaled by 1 / bag length for mean pooling); the result
+    equals the unsharded forward within the fp32 tolerance."""
+    _say(f"case route reassemble pool={pool}")
+    import torch
+    import paper_2112_02752_amd as emb
+    w = synth.scaled(synth.workload("c3"), rows_div=100, bags_div=4, name="c3-small")
+    b = synth.make_batch(w, 0)
+    dl = parity.device_layer_from_workload(w)
+    R = w.total_rows
+    shard = [R * r // 8 for r in range(9)]
+    cnt, ids, pos, bag = _route_gpu(w.row_offset, w.bags_per_table, b.offsets, b.indices, shard, W_dev=dl.W)
+    M = w.num_bags
+    full = torch.empty((M, w.dim), dtype=torch.float32, device="cuda")
+    emb.pool_fwd(dl.tables, emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(),
+                                      w.bags_per_table), pool, full)
+    acc = np.zeros((M, w.dim), np.float64)
+    k0 = 0
+    for r in range(8):
+        k1 = k0 + int(cnt[r])
+        fb = bag[k0:k1]
+        heads = np.concatenate([[True], fb[1:] != fb[:-1]]) if k1 > k0 else np.zeros(0, bool)
+        foff = np.concatenate([np.nonzero(heads)[0], [k1 - k0]]).astype(np.int32)
+        nf = len(foff) - 1
+        if nf > 0:
+            local = emb.Tables(dl.W[shard[r]:shard[r + 1]], [0, shard[r + 1] - shard[r]])
+            part = torch.empty((nf, w.dim), dtype=torch.float32, device="cuda")
+            emb.pool_fwd(local, emb.Batch(torch.from_numpy(foff).cuda(),
+                                          torch.from_numpy(np.ascontiguousarray(ids[k0:k1])).cuda(), nf),
+                         "sum", part)
+            np.add.at(acc, fb[foff[:-1]], part.cpu().numpy())
+        k0 = k1
+    if pool == "mean":
+        L = np.diff(b.offsets)
+        acc[L > 0] /= L[L > 0, None]
+    r = parity.rel_rownorm(acc, full.cpu().numpy())
+    assert r <= parity.TOL_FP32, f"reassembled forward rel err {r}"

@@ -374,6 +374,75 @@ def test_elementwise_adagrad_matches_torch_optim(pool, h0):
     np.testing.assert_array_equal(st.vals[untouched], W0[untouched])
 
 
+# ------------------------------------------------------------ routing
+
+def _shards(rng, R, W):
+    """Row-range boundaries [W+1] over R rows, some ranges empty."""
+    cuts = np.sort(rng.integers(0, R + 1, size=W - 1))
+    return np.concatenate([[0], cuts, [R]]).astype(np.int64)
+
+
+@pytest.mark.parametrize("W,seed", [(1, 0), (4, 1), (8, 2), (13, 3)])
+def test_route_matches_numpy(W, seed):
+    """Owners by np.searchsorted, the send order by a stable argsort of the
+    owners, counts by np.bincount."""
+    rng = np.random.default_rng(seed)
+    ro, B, off, idx, _, _ = random_case(rng, dyadic=False)
+    T = len(ro) - 1
+    ss = _shards(rng, int(ro[-1]), W)
+    r = oracle.route_ids(T, ro, B, off, idx, ss)
+    key = keys_of(ro, B, off, idx).astype(np.int64)
+    owner = np.searchsorted(ss, key, side="right") - 1
+    order = np.argsort(owner, kind="stable")
+    bag = np.repeat(np.arange(len(off) - 1), np.diff(off))
+    np.testing.assert_array_equal(r.send_counts, np.bincount(owner, minlength=W))
+    np.testing.assert_array_equal(r.send_pos, order)
+    np.testing.assert_array_equal(r.send_ids, key[order] - ss[owner[order]])
+    np.testing.assert_array_equal(r.send_bag, bag[order])
+
+
+@pytest.mark.parametrize("pool,tablewise", [("sum", False), ("mean", False), ("sum", True)])
+def test_route_fragments_reassemble_the_forward(pool, tablewise):
+    """Every owner pools its fragments (runs of equal bag in its send range)
+    from its own slice of the table; adding the fragments' rows by bag (then
+    dividing by the bag length for mean pooling) gives the single-device
+    forward exactly (dyadic inputs)."""
+    rng = np.random.default_rng(5)
+    ro, B, off, idx, W, _ = random_case(rng, T=3, rows=(40, 25, 60), D=4, B=12, lmax=9, empty_frac=0.2)
+    T = len(ro) - 1
+    M = len(off) - 1
+    ss = ro.copy() if tablewise else _shards(rng, int(ro[-1]), 5)
+    r = oracle.route_ids(T, ro, B, off, idx, ss)
+    full = oracle.pool_fwd(T, ro, B, off, idx, RowStore(W.copy()), pool)
+    acc = np.zeros((M, W.shape[1]), np.float64)
+    k0 = 0
+    for rank in range(len(ss) - 1):
+        k1 = k0 + int(r.send_counts[rank])
+        bags = r.send_bag[k0:k1]
+        heads = np.concatenate([[True], bags[1:] != bags[:-1]]) if k1 > k0 else np.zeros(0, bool)
+        frag_off = np.concatenate([np.nonzero(heads)[0], [k1 - k0]]).astype(np.int32)
+        local = W[ss[rank]:ss[rank + 1]].copy()
+        if len(frag_off) > 1:
+            part = oracle.pool_fwd(1, np.array([0, local.shape[0]], np.int64), len(frag_off) - 1, frag_off,
+                                   np.ascontiguousarray(r.send_ids[k0:k1]), RowStore(local), "sum")
+            for f in range(len(frag_off) - 1):
+                acc[bags[frag_off[f]]] += part[f]
+        k0 = k1
+    if pool == "mean":
+        L = np.diff(off)
+        acc[L > 0] /= L[L > 0, None]
+    np.testing.assert_array_equal(acc.astype(np.float32), full)
+
+
+def test_route_rejects_bad_shards():
+    ro = np.array([0, 10], np.int64)
+    off = np.array([0, 1], np.int32)
+    idx = np.array([3], np.int32)
+    for bad in ([0, 9], [1, 10], [0, 6, 4, 10]):
+        with pytest.raises(oracle.OracleError):
+            oracle.route_ids(1, ro, 1, off, idx, np.array(bad, np.int64))
+
+
 # ------------------------------------------------------------ sparse store
 
 def test_sparse_row_store_equals_dense():

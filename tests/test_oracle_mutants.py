@@ -34,6 +34,9 @@ MUTANTS = {
     "adagrad_ew_mean_over_D": ("double h = (double)*hp + g[d] * g[d];",
                                "double h = (double)*hp + g[d] * g[d] / (double)D;"),
     "adagrad_ew_old_state": ("denom = (double)eps + sqrt(h);", "denom = (double)eps + sqrt(h - g[d] * g[d]);"),
+    "route_upper_bound_inclusive": ("if (key < shard_start[r] || key >= shard_start[r + 1]) continue;",
+                                    "if (key < shard_start[r] || key > shard_start[r + 1]) continue;"),
+    "route_global_ids": ("send_ids[k] = (int32_t)(key - shard_start[r]);", "send_ids[k] = (int32_t)key;"),
     "counts_off_by_one": ("counts[u] = seg_offsets[u + 1] - seg_offsets[u];",
                           "counts[u] = seg_offsets[u + 1] - seg_offsets[u] + (u == 0);"),
 }
@@ -75,6 +78,8 @@ def _run_pins(so_path):
             lambda: T.test_rowwise_adagrad_closed_form_constant_row(0.75),
             lambda: T.test_adagrad_accumulates_across_steps(),
             lambda: T.test_elementwise_adagrad_matches_torch_optim("sum", 0.0),
+            lambda: T.test_route_matches_numpy(8, 2),
+            lambda: T.test_route_fragments_reassemble_the_forward("sum", False),
         ]
         for p in pins:
             try:

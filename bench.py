@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3")
+    ap.add_argument("--bags", type=int, default=None, help="bags per table instead of the workload's own")
     ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
                     help="optimizer instead of the workload's own (adagrad_ew: element-wise, state [R][D])")
     ap.add_argument("--schedule", choices=("serial", "concurrent", "pipelined"), default="serial",
@@ -144,6 +145,18 @@ def cpu_baseline(w, batches, budget_s: float):
                       f"single thread"}
 
 
+def cost_model_check(w, N, U, t_phase, ms):
+    """The layer's cost model (fitted to earlier MI355X measurements) next to
+    this run's measured phase times."""
+    from paper_2112_02752_amd import cost
+    pr = cost.predict(N, U, w.total_rows, w.dim, w.dtype, w.opt)
+    meas = {k: v * 1e6 for k, v in t_phase.items()}
+    meas["step"] = sum(meas.values())
+    return {"predicted_us": {k: round(v, 2) for k, v in pr.items()},
+            "measured_us": {k: round(v, 2) for k, v in meas.items()},
+            "rel_err": {k: round((pr[k] - meas[k]) / meas[k], 4) for k in meas}}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -163,6 +176,10 @@ def main():
         import dataclasses
         w = dataclasses.replace(w, opt=args.opt, name=f"{w.name}-{args.opt}",
                                 description=f"{w.description}; optimizer {args.opt} instead")
+    if args.bags is not None and args.bags != w.bags_per_table:
+        import dataclasses
+        w = dataclasses.replace(w, bags_per_table=args.bags, name=f"{w.name}-b{args.bags}",
+                                description=f"{w.description}; {args.bags} bags per table instead")
     if args.schedule == "pipelined":
         print("bench.py: the pipelined schedule is switched off (two co-resident dedups in flight together can "
               "wait on each other's blocks); use --schedule serial", file=sys.stderr)
@@ -368,6 +385,7 @@ def main():
         "cold": None if cold is None else dict(cold, lookups_per_s=N_avg * 1e6 / cold["median_us"]),
         "achievable_copy_GBs": copy_gbs,
         "routing": routing,
+        "cost_model": cost_model_check(w, N_avg, U_avg, t_phase, ms),
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

@@ -46,9 +46,10 @@ def parse():
     ap.add_argument("--bags", type=int, default=None, help="bags per table instead of the workload's own")
     ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
                     help="optimizer instead of the workload's own (adagrad_ew: element-wise, state [R][D])")
-    ap.add_argument("--schedule", choices=("serial", "concurrent", "pipelined"), default="serial",
+    ap.add_argument("--schedule", choices=("auto", "serial", "concurrent", "pipelined"), default="auto",
                     help="concurrent: the forward of a batch runs on a side stream at the same time as its id "
                          "dedup; serial: forward, dedup, reduce + update one after another on one stream; "
+                         "auto: concurrent for batches of at least a million lookups, else serial; "
                          "pipelined (switched off): the dedup of batch k+1 alongside the forward and update of "
                          "batch k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -228,9 +229,9 @@ def main():
         if ev:
             ev[3].record(stream)
 
-    if args.schedule == "concurrent":
+    if args.schedule in ("concurrent", "auto"):
         clayer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
-                           concurrent=True)
+                           concurrent=True if args.schedule == "concurrent" else "auto")
 
         def run_step(i):
             clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
@@ -366,7 +367,10 @@ def main():
         "data": "synthetic (seeded Zipf ids, N(0,1) upstream gradients, U(-0.01,0.01) tables)",
         "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
-                   "table_bytes": w.weight_bytes, "schedule": args.schedule},
+                   "table_bytes": w.weight_bytes, "schedule": args.schedule,
+                   "overlapped_steps": sum(1 for i in range(args.warmup, total)
+                                           if args.schedule in ("concurrent", "auto")
+                                           and clayer.overlaps(dev_batches[i][2]))},
         "roofline": {"bound": "hbm", "phase": dom, "kernel": d["kernels"], "model": "logical",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": d["hbm_traffic_bytes"], "bytes_per_launch": d["logical_bytes"],

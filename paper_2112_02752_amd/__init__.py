@@ -222,18 +222,30 @@ class Layer:
     """One GPU's shard of the layer with its buffers: forward, then the
     backward (dedup, segment-reduce, fused optimizer step) of the same batch.
 
-    With ``concurrent=True``, ``step`` runs the id dedup of a batch at the
-    same time as its forward: the dedup reads only the batch's ids and
-    offsets, never the table, so the two are independent; the forward runs on
-    a side stream after every earlier update on the caller's stream, and the
-    segment-reduce with the update waits for both.  The results are those of
-    the serial order bit for bit.  It is off by default: on MI355X the
-    forward's traffic slows the latency-bound sort passes by about as much as
-    the overlap saves, and each cross-stream wait costs the host 15-25 us."""
+    ``concurrent`` picks the schedule of a step.  False: forward, dedup and
+    reduce one after another on the caller's stream.  True: the id dedup
+    runs at the same time as the forward, which goes to a side stream after
+    every earlier update on the caller's stream (the dedup reads only ids and
+    offsets, never the table); the segment-reduce with the update waits for
+    both.  The results are those of the serial order bit for bit.  "auto":
+    concurrent for batches of at least AUTO_MIN_LOOKUPS lookups.  On MI355X
+    the overlap pays for the large batches, whose sort is the look-back kind
+    (26 tables x 8192 bags: 1101 us per step instead of 1160), but not for
+    batches under about a million lookups, whose co-resident sort passes are
+    latency-bound and slowed by the forward's traffic about as much as the
+    overlap saves; each cross-stream wait also costs the host 15-25 us.
+
+    ``step_stale`` is the asynchronous schedule with staleness one: the
+    forward of the next batch reads the table before the current batch's
+    update, as in the paper's asynchronous push-pull executor."""
+
+    AUTO_MIN_LOOKUPS = 1_000_000
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0, concurrent: bool = False):
+                 max_indices: int = 0, max_bags: int = 0, concurrent=False):
         import torch
+        if concurrent not in (False, True, "auto"):
+            raise ValueError("concurrent must be False, True or 'auto'")
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
         dev = tables.weights.device
         n = max(1, max_indices)
@@ -251,11 +263,13 @@ class Layer:
         self.num_unique = torch.zeros(1, **i32)
         self.max_indices = n
         self.concurrent = concurrent
+        self._events = False
         if concurrent:
             self._side_stream = torch.cuda.Stream(device=dev)
             self._side = int(self._side_stream.cuda_stream)
             self._ev_ready = _Hip.event()
             self._ev_fwd = _Hip.event()
+            self._events = True
         # argument values fixed for the layer's life, marshalled once
         self._ct = ctypes.byref(tables.c())
         self._upd = ctypes.byref(_update(opt, lr, eps, state))
@@ -263,7 +277,7 @@ class Layer:
                     _ptr(self.num_unique), _ptr(self.ws), self.ws.numel() * self.ws.element_size())
 
     def __del__(self):
-        if getattr(self, "concurrent", False):
+        if getattr(self, "_events", False):
             try:
                 L = _Hip.lib()
                 L.hipEventDestroy(self._ev_ready)
@@ -283,29 +297,47 @@ class Layer:
                     self.num_unique, self.ws, grad_rows=grad_rows, opt=self.opt, lr=self.lr, eps=self.eps,
                     state=self.state, stream=stream)
 
+    def overlaps(self, num_indices: int) -> bool:
+        """Whether a step of a batch of this many lookups runs concurrently."""
+        if self.concurrent == "auto":
+            return num_indices >= self.AUTO_MIN_LOOKUPS
+        return bool(self.concurrent)
+
     def step(self, batch: Batch, out, grad_out, stream=None) -> None:
         """Forward of ``batch`` into ``out`` and its backward with ``grad_out``
         (fused optimizer step), enqueued on ``stream``; ``out`` is complete
         when ``stream`` reaches the end of the step."""
-        if int(batch.indices.numel()) > self.max_indices:
+        self._enqueue(batch, out, batch, grad_out, stream)
+
+    def step_stale(self, fwd_batch: Batch, out, bwd_batch: Batch, grad_out, stream=None) -> None:
+        """One step of the asynchronous schedule with staleness one: the
+        forward of ``fwd_batch`` (the next batch) into ``out`` reads the table
+        as it is before the update of ``bwd_batch`` (the current batch, whose
+        backward runs with ``grad_out``), i.e. it misses exactly that one
+        update.  With a concurrent layer the forward overlaps the dedup."""
+        self._enqueue(fwd_batch, out, bwd_batch, grad_out, stream)
+
+    def _enqueue(self, fb: Batch, out, bb: Batch, grad_out, stream) -> None:
+        n = int(bb.indices.numel())
+        if n > self.max_indices:
             raise ValueError("batch larger than the layer's buffers")
         L = lib()
         main = _stream(stream)
-        cb = ctypes.byref(batch.c())
+        cf, cb = ctypes.byref(fb.c()), ctypes.byref(bb.c())
         uk, cnt, seg, perm, nu, ws, wsb = self._dd
         pool = POOL[self.pool]
-        if not self.concurrent:
-            _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, pool, _ptr(out), main))
+        if not self.overlaps(max(n, int(fb.indices.numel()))):
+            _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cf, pool, _ptr(out), main))
             _check("emb_unique_ids", L.emb_unique_ids(self._ct, cb, uk, cnt, seg, perm, nu, ws, wsb, main))
             _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, pool, _ptr(grad_out), perm, seg, uk, nu, None,
                                                         self._upd, ws, wsb, main))
             return
         # every earlier update on the caller's stream precedes this forward
         _Hip.record(self._ev_ready, main)
-        _check("emb_unique_ids", L.emb_unique_ids(self._ct, cb, uk, cnt, seg, perm, nu, ws, wsb, main))
         _Hip.wait(self._side, self._ev_ready)
-        _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, pool, _ptr(out), self._side))
+        _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cf, pool, _ptr(out), self._side))
         _Hip.record(self._ev_fwd, self._side)
+        _check("emb_unique_ids", L.emb_unique_ids(self._ct, cb, uk, cnt, seg, perm, nu, ws, wsb, main))
         # the update must not overwrite rows before this forward has read them
         _Hip.wait(main, self._ev_fwd)
         _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, pool, _ptr(grad_out), perm, seg, uk, nu, None,

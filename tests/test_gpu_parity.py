@@ -387,6 +387,64 @@ def test_concurrent_schedule_equals_serial():
         np.testing.assert_array_equal(a, b)
 
 
+def test_auto_schedule_full_size():
+    """The 200M-row workload (3.3M lookups per batch) under the automatic
+    schedule, which overlaps the forward with the dedup for it."""
+    w = synth.workload("c5")
+    _say("case auto schedule c5")
+    parity.run_workload(w, steps=2, concurrent="auto")
+
+
+@pytest.mark.parametrize("name,concurrent", [("c3", False), ("c2", True)])
+def test_stale_schedule_matches_oracle_replay(name, concurrent):
+    """The asynchronous schedule with staleness one (the forward of batch
+    k+1 before the update of batch k) against the oracle replaying exactly
+    that order: pooled outputs of every batch and the final rows."""
+    _say(f"case stale schedule {name} concurrent={concurrent}")
+    import oracle
+    import torch
+    import paper_2112_02752_amd as emb
+    w = synth.scaled(synth.workload(name), rows_div=50, bags_div=4, name=f"{name}-small")
+    K = 4
+    batches = [synth.make_batch(w, s) for s in range(K + 1)]
+    nmax = max(len(b.indices) for b in batches)
+    dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
+              torch.from_numpy(b.grad).cuda()) for b in batches]
+    dl = parity.device_layer_from_workload(w)
+    layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
+                      concurrent=concurrent)
+    outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in range(K + 1)]
+    layer.forward(dev_b[0][0], outs[0])
+    for k in range(K):
+        layer.step_stale(dev_b[k + 1][0], outs[k + 1], dev_b[k][0], dev_b[k][1])
+    layer.backward(dev_b[K][0], dev_b[K][1])
+    torch.cuda.synchronize()
+    # the oracle replays the same order on the rows the batches touch
+    keys = [parity.global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices) for b in batches]
+    touched = np.unique(np.concatenate(keys))
+    store = oracle.RowStore(synth.weight_rows(w, touched), keys=touched.astype(np.uint32),
+                            state=np.zeros(len(touched), np.float32) if w.opt == "adagrad" else None)
+    T, ro, B = w.num_tables, w.row_offset, w.bags_per_table
+
+    def fwd(b):
+        return oracle.pool_fwd(T, ro, B, b.offsets, b.indices, store, w.pool)
+
+    def bwd(b):
+        dd = oracle.unique_ids(T, ro, B, b.offsets, b.indices)
+        _, acc = oracle.grad_reduce(T, B, b.offsets, b.grad, w.pool, dd)
+        oracle.sparse_update(store, dd.unique_keys, acc, w.opt, w.lr, w.eps)
+
+    ref = [fwd(batches[0])]
+    for k in range(K):
+        ref.append(fwd(batches[k + 1]))
+        bwd(batches[k])
+    bwd(batches[K])
+    for k in range(K + 1):
+        r = parity.rel_rownorm(outs[k].cpu().numpy(), ref[k])
+        assert r <= parity.TOL_FP32, f"pooled output of batch {k}: rel err {r}"
+    parity.check_rows(dl, store, touched, w.opt)
+
+
 @pytest.mark.skip(reason="the pipelined schedule is switched off: bench runs of it (two dedups of 204 and 240 "
                          "tiles in flight together) ended in GPU memory faults whose cause is not yet found")
 @pytest.mark.parametrize("lookahead", [1, 2, 3])

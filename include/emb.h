@@ -77,8 +77,10 @@ typedef struct {
 typedef struct {
   int32_t bags_per_table;    /* B >= 0 */
   const int32_t* offsets;    /* device [M+1]; offsets[0] = 0, nondecreasing, offsets[M] = num_indices */
-  const int32_t* indices;    /* device [N]; table-local ids, 0 <= id < rows of the bag's table */
+  const void* indices;       /* device [N] int32 or int64 (index_bytes); table-local ids,
+                                0 <= id < rows of the bag's table */
   int64_t num_indices;       /* N, host value, 0 <= N < 2^30 */
+  int32_t index_bytes;       /* 4 (int32; 0 means 4) or 8 (int64) */
 } emb_batch;
 
 /* Optimizer of one sparse step (the paper's push step applies the sparse

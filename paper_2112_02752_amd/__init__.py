@@ -43,7 +43,7 @@ class CTables(ctypes.Structure):
 
 class CBatch(ctypes.Structure):
     _fields_ = [("bags_per_table", ctypes.c_int32), ("offsets", ctypes.c_void_p), ("indices", ctypes.c_void_p),
-                ("num_indices", ctypes.c_int64)]
+                ("num_indices", ctypes.c_int64), ("index_bytes", ctypes.c_int32)]
 
 
 class CUpdate(ctypes.Structure):
@@ -137,16 +137,18 @@ class Tables:
 
 @dataclass
 class Batch:
-    """A table-major batch in CSR form (device int32 offsets [M+1], indices [N])."""
+    """A table-major batch in CSR form (device int32 offsets [M+1], int32 or
+    int64 indices [N])."""
     offsets: object
     indices: object
     bags_per_table: int
 
     def c(self) -> CBatch:
-        key = (_ptr(self.offsets), _ptr(self.indices), int(self.indices.numel()), self.bags_per_table)
+        key = (_ptr(self.offsets), _ptr(self.indices), int(self.indices.numel()), self.bags_per_table,
+               int(self.indices.element_size()))
         if getattr(self, "_ckey", None) != key:
             n = key[2]
-            self._c = CBatch(self.bags_per_table, key[0], key[1] if n else None, n)
+            self._c = CBatch(self.bags_per_table, key[0], key[1] if n else None, n, key[4])
             self._ckey = key
         return self._c
 

@@ -51,11 +51,12 @@ constexpr uint64_t kFlagAgg = 1, kFlagInc = 2;
 
 struct PrepArgs {
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;
   TableOffsets ro;
   int32_t B, M, bags_per_block, npass, histograms;
   int32_t shift[kMaxPasses], bits[kMaxPasses];
-  uint32_t* keys_out;  // null for one table (the ids are the keys)
+  uint32_t* keys_out;  // null for int32 ids of one table (the ids are the keys)
   int32_t* bag_of;
   uint32_t* totals;    // [kMaxPasses][kMaxDigits], zero on entry (only with histograms)
 };
@@ -84,7 +85,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
       const int j = jb + u * kPrepThreads + tid;
-      id[u] = j < j1 ? a.idx[j] : 0;
+      id[u] = j < j1 ? load_id(a.idx, a.idx64, j) : 0;
     }
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
@@ -137,7 +138,8 @@ struct PassArgs {
   // look-back words
   int32_t search_bags;
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;
   TableOffsets ro;
   int32_t B, M, T;
   uint64_t* uniq_status;
@@ -628,7 +630,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
       const int64_t pos = wbase + i * kWave + lane;
-      key[i] = pos < a.N ? (uint32_t)a.idx[pos] : 0u;
+      key[i] = pos < a.N ? (uint32_t)load_id(a.idx, a.idx64, pos) : 0u;
       val[i] = pos < a.N ? (int32_t)pos : 0;
     }
     // with one table the ids are the keys: the counts go out before the bag search
@@ -1072,6 +1074,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     PrepArgs pa{};
     pa.offsets = p.offsets;
     pa.idx = p.idx;
+    pa.idx64 = p.idx64;
     pa.ro = p.ro;
     pa.B = p.B;
     pa.M = p.M;
@@ -1084,7 +1087,8 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
       pa.shift[i] = p.plan.shift[i];
       pa.bits[i] = p.plan.bits[i];
     }
-    pa.keys_out = p.T > 1 ? keys_built : nullptr;
+    // int32 ids of one table are the keys themselves; otherwise keys are built
+    pa.keys_out = (p.T > 1 || p.idx64) ? keys_built : nullptr;
     pa.bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
     pa.totals = reinterpret_cast<uint32_t*>(ws + L.totals);
     const int prep_blocks = p.M > 0 ? (p.M + pa.bags_per_block - 1) / pa.bags_per_block : 1;
@@ -1093,7 +1097,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
 
-  const uint32_t* kin = p.T > 1 ? keys_built : reinterpret_cast<const uint32_t*>(p.idx);
+  const uint32_t* kin = (p.T > 1 || p.idx64) ? keys_built : static_cast<const uint32_t*>(p.idx);
   const int32_t* vin = nullptr;
   const int32_t* bin = reinterpret_cast<const int32_t*>(ws + L.bag_of);
   uint32_t* keys_a = reinterpret_cast<uint32_t*>(ws + L.keys_a);
@@ -1128,6 +1132,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.search_bags = sort_cores && ps == 0;
     xa.offsets = p.offsets;
     xa.idx = p.idx;
+    xa.idx64 = p.idx64;
     xa.ro = p.ro;
     xa.B = p.B;
     xa.M = p.M;

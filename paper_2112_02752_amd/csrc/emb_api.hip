@@ -37,6 +37,7 @@ emb_status check_batch(const emb_batch* b, int32_t T, int32_t* M) {
   if (b->bags_per_table < 0 || b->num_indices < 0) return EMB_EINVAL;
   if (b->num_indices >= kMaxIndices) return EMB_EUNSUPPORTED;
   if (b->num_indices > 0 && b->indices == nullptr) return EMB_EINVAL;
+  if (b->index_bytes != 0 && b->index_bytes != 4 && b->index_bytes != 8) return EMB_EINVAL;
   const int64_t m = (int64_t)T * b->bags_per_table;
   if (m >= ((int64_t)1 << 31) - 1) return EMB_EUNSUPPORTED;
   *M = (int32_t)m;
@@ -111,6 +112,7 @@ emb_status emb_pool_fwd(const emb_tables* tables, const emb_batch* batch, int32_
   p.W = tables->weights;
   p.offsets = batch->offsets;
   p.idx = batch->indices;
+  p.idx64 = batch->index_bytes == 8;
   p.ro = ro;
   p.B = batch->bags_per_table;
   p.M = M;
@@ -140,6 +142,7 @@ emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint
   DedupLaunch p{};
   p.offsets = batch->offsets;
   p.idx = batch->indices;
+  p.idx64 = batch->index_bytes == 8;
   p.ro = ro;
   p.T = tables->num_tables;
   p.B = batch->bags_per_table;
@@ -264,6 +267,7 @@ emb_status emb_route_ids(const emb_tables* tables, const emb_batch* batch, int32
   RouteLaunch p{};
   p.offsets = batch->offsets;
   p.idx = batch->indices;
+  p.idx64 = batch->index_bytes == 8;
   p.ro = ro;
   p.sb = sb;
   p.B = batch->bags_per_table;
@@ -290,6 +294,7 @@ emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, 
   ValidateLaunch p{};
   p.offsets = batch->offsets;
   p.idx = batch->indices;
+  p.idx64 = batch->index_bytes == 8;
   p.ro = ro;
   p.T = tables->num_tables;
   p.B = batch->bags_per_table;

@@ -179,6 +179,12 @@ constexpr int kRouteScanThreads = 1024;
 
 // ------------------------------------------------------------ device helpers
 
+// id j of a batch whose indices are int32 (idx64 == 0) or int64; a valid id
+// is below 2^31 (rows of a table), so both read the same value
+__device__ __forceinline__ int32_t load_id(const void* idx, int32_t idx64, int64_t j) {
+  return idx64 ? (int32_t) static_cast<const int64_t*>(idx)[j] : static_cast<const int32_t*>(idx)[j];
+}
+
 // number of set bits of `mask` below this lane
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));

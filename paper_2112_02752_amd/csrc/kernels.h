@@ -9,7 +9,8 @@ namespace emb {
 struct FwdLaunch {
   const void* W;
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;  // indices are int64
   TableOffsets ro;
   int32_t B, M, D, dtype, pool;
   float* out;
@@ -27,7 +28,8 @@ SortPlan make_sort_plan(int key_bits);
 
 struct DedupLaunch {
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;
   TableOffsets ro;
   int32_t T, B, M;
   int64_t N;
@@ -84,7 +86,8 @@ RoutePlan route_plan(int64_t N, int64_t M);
 
 struct RouteLaunch {
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;
   TableOffsets ro;
   ShardBounds sb;
   int32_t B, M, W;
@@ -99,7 +102,8 @@ hipError_t launch_route(const RouteLaunch& p, hipStream_t s);
 
 struct ValidateLaunch {
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;
   TableOffsets ro;
   int32_t T, B, M;
   int64_t N;

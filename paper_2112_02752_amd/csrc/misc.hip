@@ -17,8 +17,8 @@ __global__ void k_fill_zero_u32(uint32_t* p, size_t n) {
 }
 
 // flag bits: 1 offsets[0] != 0, 2 decreasing offsets, 4 offsets[M] != N, 8 id out of range
-__global__ void k_validate(const int32_t* offsets, const int32_t* idx, TableOffsets ro, int32_t B, int32_t M,
-                           int64_t N, int32_t* flag) {
+__global__ void k_validate(const int32_t* offsets, const void* idx, int32_t idx64, TableOffsets ro, int32_t B,
+                           int32_t M, int64_t N, int32_t* flag) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   uint32_t bits = 0;
   const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -37,8 +37,8 @@ __global__ void k_validate(const int32_t* offsets, const int32_t* idx, TableOffs
     const int32_t lo = s < 0 ? 0 : s;
     const int64_t hi = (int64_t)e < N ? (int64_t)e : N;
     for (int64_t j = lo; j < hi; ++j) {
-      const int32_t id = idx[j];
-      if (id < 0 || (int64_t)id >= rows) bits |= 8u;
+      const int64_t id = idx64 ? static_cast<const int64_t*>(idx)[j] : (int64_t) static_cast<const int32_t*>(idx)[j];
+      if (id < 0 || id >= rows) bits |= 8u;
     }
   }
   if (bits) atomicOr(reinterpret_cast<uint32_t*>(flag), bits);
@@ -61,7 +61,8 @@ hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s) {
   int64_t blocks = ((int64_t)p.M + 255) / 256;
   if (blocks < 1) blocks = 1;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(k_validate, dim3((unsigned)blocks), dim3(256), 0, s, p.offsets, p.idx, p.ro, p.B, p.M, p.N,
+  hipLaunchKernelGGL(k_validate, dim3((unsigned)blocks), dim3(256), 0, s, p.offsets, p.idx, p.idx64, p.ro, p.B, p.M,
+                     p.N,
                      p.flag);
   return hipGetLastError();
 }

@@ -50,9 +50,9 @@ struct Vec<uint16_t> {
 
 constexpr int unroll_for(int rpi) { return rpi == 1 ? 8 : (rpi == 2 ? 8 : (rpi == 4 ? 8 : 4)); }
 
-template <typename TW, int G, int NV>
+template <typename TW, int G, int NV, typename TI>
 __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, const int32_t* __restrict__ offsets,
-                                                  const int32_t* __restrict__ idx, TableOffsets ro, int32_t B,
+                                                  const TI* __restrict__ idx, TableOffsets ro, int32_t B,
                                                   int32_t M, int32_t D, int32_t pool, float* __restrict__ out) {
   constexpr int RPI = kWave / G;
   constexpr int E = Vec<TW>::kElems;
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
   for (int j0 = start; j0 < end; j0 += kWave) {
     const int n = min(kWave, end - j0);
     const bool valid = lane < n;
-    const int my_id = valid ? idx[j0 + lane] : 0;
+    const int my_id = valid ? (int)idx[j0 + lane] : 0;
     // Skewed ids repeat within a bag: each distinct id of the chunk is loaded
     // once and added with its multiplicity.  Lanes are classed by an 8-bit
     // hash of the id (one ballot per hash bit); a lane whose id equals the
@@ -165,8 +165,13 @@ __global__ __launch_bounds__(256) void k_pool_fwd(const TW* __restrict__ W, cons
 template <typename TW, int G, int NV>
 hipError_t launch_t(const FwdLaunch& p, hipStream_t s) {
   dim3 grid((unsigned)((p.M + 3) / 4)), block(256);
-  hipLaunchKernelGGL((k_pool_fwd<TW, G, NV>), grid, block, 0, s, reinterpret_cast<const TW*>(p.W), p.offsets,
-                     p.idx, p.ro, p.B, p.M, p.D, p.pool, p.out);
+  // the index type (int32 or int64) is a template argument: no per-load branch
+  if (p.idx64)
+    hipLaunchKernelGGL((k_pool_fwd<TW, G, NV, int64_t>), grid, block, 0, s, reinterpret_cast<const TW*>(p.W),
+                       p.offsets, static_cast<const int64_t*>(p.idx), p.ro, p.B, p.M, p.D, p.pool, p.out);
+  else
+    hipLaunchKernelGGL((k_pool_fwd<TW, G, NV, int32_t>), grid, block, 0, s, reinterpret_cast<const TW*>(p.W),
+                       p.offsets, static_cast<const int32_t*>(p.idx), p.ro, p.B, p.M, p.D, p.pool, p.out);
   return hipGetLastError();
 }
 

@@ -19,7 +19,8 @@ namespace {
 
 struct RouteArgs {
   const int32_t* offsets;
-  const int32_t* idx;
+  const void* idx;
+  int32_t idx64;
   TableOffsets ro;
   ShardBounds sb;
   int32_t B, M, W, owner_bits, bags_per_block, nblocks;
@@ -77,7 +78,7 @@ __global__ __launch_bounds__(kWave) void k_route_count(RouteArgs a) {
   const int32_t p0 = s_off[0], p1 = s_off[nb];
   for (int32_t j = p0 + lane; j < p1; j += kWave) {
     const int bl = bag_of(s_off, nb, j);
-    const uint32_t key = a.ro.off[(b0 + bl) / a.B] + (uint32_t)a.idx[j];
+    const uint32_t key = a.ro.off[(b0 + bl) / a.B] + (uint32_t)load_id(a.idx, a.idx64, j);
     atomicAdd(&s_hist[owner_of(s_sb, a.W, key)], 1);
   }
   __syncthreads();
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(kWave) void k_route_scatter(RouteArgs a) {
     uint32_t key = 0;
     if (valid) {
       bl = bag_of(s_off, nb, j);
-      key = a.ro.off[(b0 + bl) / a.B] + (uint32_t)a.idx[j];
+      key = a.ro.off[(b0 + bl) / a.B] + (uint32_t)load_id(a.idx, a.idx64, j);
       o = owner_of(s_sb, a.W, key);
     }
     // lanes with the same owner, by one ballot per owner bit
@@ -173,6 +174,7 @@ hipError_t launch_route(const RouteLaunch& p, hipStream_t s) {
   RouteArgs a{};
   a.offsets = p.offsets;
   a.idx = p.idx;
+  a.idx64 = p.idx64;
   a.ro = p.ro;
   a.sb = p.sb;
   a.B = p.B;

@@ -116,7 +116,7 @@ class StepResult:
 
 def gpu_step(dl: DeviceLayer, offsets: np.ndarray, indices: np.ndarray, grad: np.ndarray, B: int, pool: str,
              opt: str, lr: float, eps: float, fused: bool = True, want_grad_rows: bool = True,
-             layer: Optional[emb.Layer] = None) -> StepResult:
+             layer: Optional[emb.Layer] = None, idx64: bool = False) -> StepResult:
     """One step (fwd on pre-update rows, dedup, reduce, optimizer) on the GPU.
     A layer built with concurrent=True runs the step through Layer.step (the
     forward on a side stream alongside the dedup; no unfused gradient rows)."""
@@ -125,7 +125,7 @@ def gpu_step(dl: DeviceLayer, offsets: np.ndarray, indices: np.ndarray, grad: np
     N = int(indices.shape[0])
     M = int(offsets.shape[0]) - 1
     off = torch.from_numpy(offsets.astype(np.int32)).to(dev)
-    idx = torch.from_numpy(indices.astype(np.int32)).to(dev)
+    idx = torch.from_numpy(indices.astype(np.int64 if idx64 else np.int32)).to(dev)
     G = torch.from_numpy(np.ascontiguousarray(grad, dtype=np.float32)).to(dev)
     if layer is None:
         layer = emb.Layer(dl.tables, pool, opt, lr, eps, dl.state, max_indices=N, max_bags=M, concurrent=False)
@@ -218,7 +218,7 @@ def check_untouched(dl: DeviceLayer, w: synth.Workload, touched: np.ndarray, n: 
 
 
 def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="cuda", concurrent: bool = False,
-                 h0: float = 0.0):
+                 h0: float = 0.0, idx64: bool = False):
     """Full-size parity of `steps` consecutive steps of a workload (serial
     calls, or Layer.step's concurrent schedule); Adagrad state starts at h0."""
     dl = device_layer_from_workload(w, device, h0)
@@ -236,7 +236,7 @@ def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="
                       concurrent=concurrent)
     for s, b in enumerate(batches):
         g = gpu_step(dl, b.offsets, b.indices, b.grad, w.bags_per_table, w.pool, w.opt, w.lr, w.eps, fused=fused,
-                     layer=layer)
+                     layer=layer, idx64=idx64)
         o_out, o_dd, o_gr = oracle.step(w.num_tables, w.row_offset, w.bags_per_table, b.offsets, b.indices, b.grad,
                                         store, w.pool, w.opt, w.lr, w.eps)
         check_against_oracle(g, o_out, o_dd, o_gr)
@@ -246,7 +246,7 @@ def run_workload(w: synth.Workload, steps: int = 1, fused: bool = True, device="
 
 
 def run_case(row_offset, W_host: np.ndarray, offsets, indices, grad, B: int, pool: str, opt: str, lr: float,
-             eps: float, state0=None, fused=True, device="cuda", exact=False):
+             eps: float, state0=None, fused=True, device="cuda", exact=False, idx64=False):
     """Parity of one step on explicit host inputs (dense tables)."""
     offsets = np.ascontiguousarray(offsets, dtype=np.int32)
     indices = np.ascontiguousarray(indices, dtype=np.int32)
@@ -258,7 +258,7 @@ def run_case(row_offset, W_host: np.ndarray, offsets, indices, grad, B: int, poo
         state0 = np.zeros(W_host.shape, np.float32)
     dl = device_layer_from_host(ro, W_host, state0 if opt != "sgd" else None, device)
     store = oracle.RowStore(W_host.copy(), state=state0.copy() if state0 is not None else None)
-    g = gpu_step(dl, offsets, indices, grad, B, pool, opt, lr, eps, fused=fused)
+    g = gpu_step(dl, offsets, indices, grad, B, pool, opt, lr, eps, fused=fused, idx64=idx64)
     o_out, o_dd, o_gr = oracle.step(len(ro) - 1, ro, B, offsets, indices, grad, store, pool, opt, lr, eps)
     check_against_oracle(g, o_out, o_dd, o_gr)
     check_rows(dl, store, o_dd.unique_keys, opt)

@@ -80,6 +80,9 @@ def test_fwd_argument_errors():
     assert call_fwd(_tables(), _batch(n=1 << 30)) == emb.EMB_EUNSUPPORTED
     assert call_fwd(_tables(), _batch(indices=None)) == emb.EMB_EINVAL
     assert call_fwd(_tables(), _batch(), pool=2) == emb.EMB_EINVAL
+    bad_width = _batch()
+    bad_width.index_bytes = 2
+    assert call_fwd(_tables(), bad_width) == emb.EMB_EINVAL
     assert call_fwd(_tables(), _batch(), out=None) == emb.EMB_EINVAL
     t = _tables()
     t.num_tables = 0

@@ -336,6 +336,44 @@ def test_elementwise_adagrad_full_size(name, steps):
     parity.run_workload(w, steps=steps, h0=1.0)
 
 
+# ------------------------------------------------------------- int64 ids
+
+@pytest.mark.parametrize("pool,opt", [("sum", "adagrad"), ("mean", "sgd")])
+def test_int64_indices_small(pool, opt):
+    _say(f"case int64 ids pool={pool} opt={opt}")
+    rng = np.random.default_rng(60)
+    rows = [1000, 37, 5000]
+    B, D = 300, 64
+    off, idx = _rand_batch(rng, rows, B, 40, empty_frac=0.05, zipf=1.3)
+    W = rng.uniform(-0.5, 0.5, size=(sum(rows), D)).astype(np.float32)
+    G = rng.standard_normal(size=(len(off) - 1, D)).astype(np.float32)
+    parity.run_case(_row_offset(rows), W, off, idx, G, B, pool, opt, 0.01, 1e-8, idx64=True)
+
+
+@pytest.mark.parametrize("name", ["c3", "c2", "c5"])
+def test_int64_indices_full_size(name):
+    """int64 ids (PyTorch's index type) at full size: one table with the
+    co-resident sort, several tables, one table with the look-back sort."""
+    w = synth.workload(name)
+    _say(f"case int64 ids full size {name}")
+    parity.run_workload(w, steps=1, idx64=True)
+
+
+def test_int64_validate_flags_ids_beyond_32_bits():
+    _say("case int64 validate")
+    import torch
+    import paper_2112_02752_amd as emb
+    W = torch.zeros((10, 16), dtype=torch.float32, device="cuda")
+    t = emb.Tables(W, [0, 10])
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    off = torch.tensor([0, 2], dtype=torch.int32, device="cuda")
+    for ids, want in (([3, 9], 0), ([3, (1 << 32) + 3], 8), ([-1, 2], 8)):
+        b = emb.Batch(off, torch.tensor(ids, dtype=torch.int64, device="cuda"), 1)
+        emb.validate_batch(t, b, flag)
+        torch.cuda.synchronize()
+        assert int(flag.item()) == want, (ids, int(flag.item()))
+
+
 def test_c5_three_consecutive_steps():
     w = synth.workload("c5")
     _say("case c5 x3 steps")
@@ -488,7 +526,7 @@ def test_pipelined_schedule_equals_serial(lookahead):
 
 # ------------------------------------------------------------------ routing
 
-def _route_gpu(row_offset, B, off, idx, shard, W_dev=None):
+def _route_gpu(row_offset, B, off, idx, shard, W_dev=None, idx64=False):
     import torch
     import paper_2112_02752_amd as emb
     N, M = len(idx), len(off) - 1
@@ -498,7 +536,7 @@ def _route_gpu(row_offset, B, off, idx, shard, W_dev=None):
         W_dev = torch.empty((int(row_offset[-1]), 4), dtype=torch.float32, device=dev)  # never read
     tables = emb.Tables(W_dev, [int(x) for x in row_offset])
     b = emb.Batch(torch.from_numpy(np.ascontiguousarray(off, np.int32)).to(dev),
-                  torch.from_numpy(np.ascontiguousarray(idx, np.int32)).to(dev), B)
+                  torch.from_numpy(np.ascontiguousarray(idx, np.int64 if idx64 else np.int32)).to(dev), B)
     i32 = dict(dtype=torch.int32, device=dev)
     cnt = torch.full((Wr,), -1, **i32)
     ids, pos, bag = (torch.full((max(N, 1),), -1, **i32) for _ in range(3))
@@ -508,12 +546,12 @@ def _route_gpu(row_offset, B, off, idx, shard, W_dev=None):
     return cnt.cpu().numpy(), ids[:N].cpu().numpy(), pos[:N].cpu().numpy(), bag[:N].cpu().numpy()
 
 
-def _check_route(row_offset, B, off, idx, shard):
+def _check_route(row_offset, B, off, idx, shard, idx64=False):
     import oracle
     T = len(row_offset) - 1
     ref = oracle.route_ids(T, np.asarray(row_offset, np.int64), B, np.ascontiguousarray(off, np.int32),
                            np.ascontiguousarray(idx, np.int32), np.asarray(shard, np.int64))
-    cnt, ids, pos, bag = _route_gpu(row_offset, B, off, idx, shard)
+    cnt, ids, pos, bag = _route_gpu(row_offset, B, off, idx, shard, idx64=idx64)
     np.testing.assert_array_equal(cnt, ref.send_counts)
     np.testing.assert_array_equal(pos, ref.send_pos)
     np.testing.assert_array_equal(ids, ref.send_ids)
@@ -532,6 +570,16 @@ def test_route_small(Wr, seed):
     cuts = np.sort(rng.integers(0, R + 1, size=Wr - 1))
     shard = [0] + [int(x) for x in cuts] + [R]
     _check_route(_row_offset(rows), B, off, idx, shard)
+
+
+def test_route_int64_indices():
+    _say("case route int64 ids")
+    rng = np.random.default_rng(9)
+    rows = [5000, 800, 12000]
+    B = 700
+    off, idx = _rand_batch(rng, rows, B, 40, empty_frac=0.1, zipf=1.2)
+    R = sum(rows)
+    _check_route(_row_offset(rows), B, off, idx, [0, 3000, 9000, 15000, R], idx64=True)
 
 
 def test_route_tablewise_and_empty_batch():

@@ -83,6 +83,8 @@ typedef struct {
   int32_t index_bytes;       /* 4 (int32; 0 means 4) or 8 (int64) */
 } emb_batch;
 
+typedef enum { EMB_ROUND_NEAREST_EVEN = 0, EMB_ROUND_STOCHASTIC = 1 } emb_rounding;
+
 /* Optimizer of one sparse step (the paper's push step applies the sparse
  * gradient to the touched rows; it does not fix the optimizer).
  *   SGD:                   W_r <- W_r - lr * g_r
@@ -98,6 +100,13 @@ typedef struct {
   float eps;      /* Adagrad only */
   float* state;   /* device fp32 accumulators h: [R] (row-wise), [R][D] row-major
                      (element-wise); NULL for SGD */
+  int32_t rounding; /* emb_rounding of bf16 table stores (fp32 tables ignore it).
+                       Stochastic: the 16 bits below the bf16 mantissa are added to
+                       16 random bits and cut off (unbiased); the bits of element
+                       (row r, column d) are the top 16 of
+                       splitmix64(seed ^ splitmix64(r * D + d)) (Steele, Lea and
+                       Flood 2014), so a caller passes a fresh seed every step */
+  uint64_t seed;
 } emb_update;
 
 /* Forward: out[m][d] = scale_m * sum over bag m of W[key(j)][d], fp32

@@ -54,7 +54,12 @@ def _lib():
         L.oracle_route_ids.restype = ctypes.c_int
         L.oracle_route_ids.argtypes = [i32, vp, i32, vp, vp, i32, vp, vp, vp, vp, vp]
         L.oracle_sparse_update.restype = ctypes.c_int
-        L.oracle_sparse_update.argtypes = [i32, f32, f32, i32, i32, i64, vp, vp, vp, vp, i32, vp]
+        L.oracle_sparse_update.argtypes = [i32, f32, f32, i32, i32, i64, vp, vp, vp, vp, i32, vp, i32,
+                                           ctypes.c_uint64]
+        L.oracle_sr_bits.restype = ctypes.c_uint32
+        L.oracle_sr_bits.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.oracle_bf16_stochastic.restype = ctypes.c_uint16
+        L.oracle_bf16_stochastic.argtypes = [f32, ctypes.c_uint32]
         _L = L
     return _L
 
@@ -143,8 +148,21 @@ def grad_reduce(num_tables: int, bags_per_table: int, offsets: np.ndarray, grad:
     return gr[:U], acc[:U]
 
 
+ROUNDING = {"nearest": 0, "stochastic": 1}
+
+
+def sr_bits(seed: int, counter: int) -> int:
+    """The 16 random bits of stochastic rounding for element counter row * D + column."""
+    return int(_lib().oracle_sr_bits(seed, counter))
+
+
+def bf16_stochastic(x: float, r16: int) -> int:
+    """Stochastic rounding of an fp32 value to bf16 bits with 16 random bits."""
+    return int(_lib().oracle_bf16_stochastic(x, r16))
+
+
 def sparse_update(store: RowStore, unique_keys: np.ndarray, grad: np.ndarray, opt: str, lr: float,
-                  eps: float) -> None:
+                  eps: float, rounding: str = "nearest", seed: int = 0) -> None:
     """In-place optimizer step on ``store`` (grad: float64 [U][D] or float32, widened)."""
     D = store.vals.shape[1]
     g = np.ascontiguousarray(grad, dtype=np.float64)
@@ -156,7 +174,7 @@ def sparse_update(store: RowStore, unique_keys: np.ndarray, grad: np.ndarray, op
     if OPT[opt] == 2:
         assert store.state.shape == (store.n, D) and store.state.flags["C_CONTIGUOUS"]
     rc = _lib().oracle_sparse_update(OPT[opt], lr, eps, D, store.dtype, store.n, _p(store.keys), _p(store.vals),
-                                     _p(store.state), _p(uk), int(uk.shape[0]), _p(g))
+                                     _p(store.state), _p(uk), int(uk.shape[0]), _p(g), ROUNDING[rounding], seed)
     _check(rc, "oracle_sparse_update")
 
 
@@ -184,12 +202,13 @@ def route_ids(num_tables: int, row_offset: np.ndarray, bags_per_table: int, offs
 
 
 def step(num_tables: int, row_offset: np.ndarray, bags_per_table: int, offsets: np.ndarray, indices: np.ndarray,
-         grad: np.ndarray, store: RowStore, pool: str, opt: str, lr: float, eps: float):
+         grad: np.ndarray, store: RowStore, pool: str, opt: str, lr: float, eps: float, rounding: str = "nearest",
+         seed: int = 0):
     """One whole step in the layer's order: forward on the pre-update rows,
     dedup, gradient reduce, optimizer step (in place on ``store``).
     Returns (out, dedup, grad_rows)."""
     out = pool_fwd(num_tables, row_offset, bags_per_table, offsets, indices, store, pool)
     dd = unique_ids(num_tables, row_offset, bags_per_table, offsets, indices)
     gr, acc = grad_reduce(num_tables, bags_per_table, offsets, grad, pool, dd)
-    sparse_update(store, dd.unique_keys, acc, opt, lr, eps)
+    sparse_update(store, dd.unique_keys, acc, opt, lr, eps, rounding, seed)
     return out, dd, gr

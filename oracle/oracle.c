@@ -70,6 +70,29 @@ static uint16_t float_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+/* splitmix64 (Steele, Lea and Flood 2014): the output for generator state x */
+static uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9e3779b97f4a7c15ULL;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+  return z ^ (z >> 31);
+}
+
+/* The 16 random bits of stochastic rounding for element counter c (row * D +
+ * column) under seed: the top 16 bits of splitmix64(seed ^ splitmix64(c)). */
+uint32_t oracle_sr_bits(uint64_t seed, uint64_t c) { return (uint32_t)(splitmix64(seed ^ splitmix64(c)) >> 48); }
+
+/* Stochastic rounding of an fp32 value to bf16: the 16 bits below the bf16
+ * mantissa are added to 16 random bits and cut off, so the magnitude rounds
+ * up with probability (dropped bits) / 2^16 -- unbiased.  Non-finite values
+ * round to nearest even. */
+uint16_t oracle_bf16_stochastic(float f, uint32_t r16) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) return float_to_bf16_rne(f);
+  return (uint16_t)((u + (r16 & 0xffffu)) >> 16);
+}
+
 static double store_get(const store_t* s, const void* vals, int64_t slot, int32_t d) {
   if (s->dtype == 0) return (double)((const float*)vals)[slot * s->dim + d];
   return bf16_to_double(((const uint16_t*)vals)[slot * s->dim + d]);
@@ -80,6 +103,16 @@ static void store_put(const store_t* s, void* vals, int64_t slot, int32_t d, dou
   float f = (float)v;
   if (s->dtype == 0) ((float*)vals)[slot * s->dim + d] = f;
   else ((uint16_t*)vals)[slot * s->dim + d] = float_to_bf16_rne(f);
+}
+
+/* the same, stochastic rounding to bf16 with the bits of element (row, d) */
+static void store_put_sr(const store_t* s, void* vals, int64_t slot, int32_t d, double v, uint64_t seed,
+                         uint32_t row) {
+  float f = (float)v;
+  if (s->dtype == 0) ((float*)vals)[slot * s->dim + d] = f;
+  else
+    ((uint16_t*)vals)[slot * s->dim + d] =
+        oracle_bf16_stochastic(f, oracle_sr_bits(seed, (uint64_t)row * (uint64_t)s->dim + (uint64_t)d));
 }
 
 /* ------------------------------------------------------------- validate */
@@ -217,7 +250,9 @@ int oracle_grad_reduce(int32_t T, int32_t B, const int32_t* offsets, int32_t D, 
 
 /* ------------------------------------------------------------ optimizer */
 
-/* One step on the rows unique_keys[0..U) with gradient rows grad[u][.]:
+/* One step on the rows unique_keys[0..U) with gradient rows grad[u][.]
+ * (rounding 1: bf16 rows round stochastically, element (r, d) with the bits
+ * oracle_sr_bits(seed, r * D + d)):
  *   opt 0, SGD:                     W[r] <- W[r] - lr * g
  *   opt 1, row-wise Adagrad:        h_r <- h_r + (1/D) sum_d g[d]^2
  *                                   W[r] <- W[r] - lr * g / (sqrt(h_r) + eps)
@@ -229,8 +264,8 @@ int oracle_grad_reduce(int32_t T, int32_t B, const int32_t* offsets, int32_t D, 
  * W. */
 int oracle_sparse_update(int32_t opt, float lr, float eps, int32_t D, int32_t dtype, int64_t store_n,
                          const uint32_t* store_keys, void* store_vals, float* state, const uint32_t* unique_keys,
-                         int32_t U, const double* grad) {
-  if (opt < 0 || opt > 2 || D < 1 || U < 0) return ORC_BAD_ARG;
+                         int32_t U, const double* grad, int32_t rounding, uint64_t seed) {
+  if (opt < 0 || opt > 2 || D < 1 || U < 0 || rounding < 0 || rounding > 1) return ORC_BAD_ARG;
   if (opt != 0 && state == NULL) return ORC_BAD_ARG;
   store_t s = {store_n, store_keys, D, dtype};
   for (int32_t u = 0; u < U; ++u) {
@@ -253,7 +288,8 @@ int oracle_sparse_update(int32_t opt, float lr, float eps, int32_t D, int32_t dt
         denom = (double)eps + sqrt(h);
       }
       double w = store_get(&s, store_vals, slot, d);
-      store_put(&s, store_vals, slot, d, w - (double)lr * g[d] / denom);
+      if (rounding == 1) store_put_sr(&s, store_vals, slot, d, w - (double)lr * g[d] / denom, seed, unique_keys[u]);
+      else store_put(&s, store_vals, slot, d, w - (double)lr * g[d] / denom);
     }
   }
   return ORC_OK;

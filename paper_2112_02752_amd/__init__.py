@@ -48,7 +48,10 @@ class CBatch(ctypes.Structure):
 
 class CUpdate(ctypes.Structure):
     _fields_ = [("opt", ctypes.c_int32), ("lr", ctypes.c_float), ("eps", ctypes.c_float),
-                ("state", ctypes.c_void_p)]
+                ("state", ctypes.c_void_p), ("rounding", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+
+
+ROUNDING = {"nearest": 0, "stochastic": 1}
 
 
 _lib = None
@@ -174,15 +177,15 @@ def unique_ids(tables: Tables, batch: Batch, unique_keys, counts, seg_offsets, s
         _ptr(sort_perm), _ptr(num_unique), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def _update(opt: str, lr: float, eps: float, state) -> CUpdate:
-    return CUpdate(OPT[opt], lr, eps, _ptr(state))
+def _update(opt: str, lr: float, eps: float, state, rounding: str = "nearest", seed: int = 0) -> CUpdate:
+    return CUpdate(OPT[opt], lr, eps, _ptr(state), ROUNDING[rounding], seed)
 
 
 def grad_reduce(tables: Tables, batch: Batch, pool: str, grad_out, sort_perm, seg_offsets, unique_keys,
                 num_unique, ws, grad_rows=None, opt: Optional[str] = None, lr: float = 0.0, eps: float = 0.0,
-                state=None, stream=None) -> None:
+                state=None, stream=None, rounding: str = "nearest", seed: int = 0) -> None:
     """Segment-reduce the upstream gradient; with ``opt`` also apply the fused optimizer step."""
-    upd = ctypes.byref(_update(opt, lr, eps, state)) if opt is not None else None
+    upd = ctypes.byref(_update(opt, lr, eps, state, rounding, seed)) if opt is not None else None
     _check("emb_grad_reduce", lib().emb_grad_reduce(
         ctypes.byref(tables.c()), ctypes.byref(batch.c()), POOL[pool], _ptr(grad_out), _ptr(sort_perm),
         _ptr(seg_offsets), _ptr(unique_keys), _ptr(num_unique), _ptr(grad_rows), upd, _ptr(ws),
@@ -190,9 +193,9 @@ def grad_reduce(tables: Tables, batch: Batch, pool: str, grad_out, sort_perm, se
 
 
 def sparse_update(tables: Tables, opt: str, lr: float, eps: float, state, unique_keys, num_unique,
-                  max_unique: int, grad_rows, stream=None) -> None:
+                  max_unique: int, grad_rows, stream=None, rounding: str = "nearest", seed: int = 0) -> None:
     _check("emb_sparse_update", lib().emb_sparse_update(
-        ctypes.byref(tables.c()), ctypes.byref(_update(opt, lr, eps, state)), _ptr(unique_keys),
+        ctypes.byref(tables.c()), ctypes.byref(_update(opt, lr, eps, state, rounding, seed)), _ptr(unique_keys),
         _ptr(num_unique), max_unique, _ptr(grad_rows), _stream(stream)))
 
 
@@ -244,7 +247,8 @@ class Layer:
     AUTO_MIN_LOOKUPS = 1_000_000
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0, concurrent=False):
+                 max_indices: int = 0, max_bags: int = 0, concurrent=False, rounding: str = "nearest",
+                 seed: int = 0):
         import torch
         if concurrent not in (False, True, "auto"):
             raise ValueError("concurrent must be False, True or 'auto'")
@@ -274,7 +278,10 @@ class Layer:
             self._events = True
         # argument values fixed for the layer's life, marshalled once
         self._ct = ctypes.byref(tables.c())
-        self._upd = ctypes.byref(_update(opt, lr, eps, state))
+        # bf16 stochastic rounding draws fresh bits every step: seed, seed + 1, ...
+        self.rounding, self.seed, self.steps_done = rounding, seed, 0
+        self._updc = _update(opt, lr, eps, state, rounding, seed)
+        self._upd = ctypes.byref(self._updc)
         self._dd = (_ptr(self.unique_keys), _ptr(self.counts), _ptr(self.seg_offsets), _ptr(self.sort_perm),
                     _ptr(self.num_unique), _ptr(self.ws), self.ws.numel() * self.ws.element_size())
 
@@ -297,7 +304,8 @@ class Layer:
                    self.num_unique, self.ws, stream)
         grad_reduce(self.tables, batch, self.pool, grad_out, self.sort_perm, self.seg_offsets, self.unique_keys,
                     self.num_unique, self.ws, grad_rows=grad_rows, opt=self.opt, lr=self.lr, eps=self.eps,
-                    state=self.state, stream=stream)
+                    state=self.state, stream=stream, rounding=self.rounding, seed=self.seed + self.steps_done)
+        self.steps_done += 1
 
     def overlaps(self, num_indices: int) -> bool:
         """Whether a step of a batch of this many lookups runs concurrently."""
@@ -328,6 +336,8 @@ class Layer:
         cf, cb = ctypes.byref(fb.c()), ctypes.byref(bb.c())
         uk, cnt, seg, perm, nu, ws, wsb = self._dd
         pool = POOL[self.pool]
+        self._updc.seed = self.seed + self.steps_done
+        self.steps_done += 1
         if not self.overlaps(max(n, int(fb.indices.numel()))):
             _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cf, pool, _ptr(out), main))
             _check("emb_unique_ids", L.emb_unique_ids(self._ct, cb, uk, cnt, seg, perm, nu, ws, wsb, main))

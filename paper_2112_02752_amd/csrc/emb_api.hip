@@ -63,6 +63,7 @@ emb_status check_update(const emb_update* u) {
   if (u->opt != EMB_OPT_SGD && u->opt != EMB_OPT_ADAGRAD_ROWWISE && u->opt != EMB_OPT_ADAGRAD_ELEMENTWISE)
     return EMB_EINVAL;
   if (u->opt != EMB_OPT_SGD && u->state == nullptr) return EMB_EINVAL;
+  if (u->rounding != EMB_ROUND_NEAREST_EVEN && u->rounding != EMB_ROUND_STOCHASTIC) return EMB_EINVAL;
   return EMB_OK;
 }
 
@@ -202,6 +203,8 @@ emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int
   p.dtype = tables->dtype;
   p.lr = fuse ? fuse->lr : 0.f;
   p.eps = fuse ? fuse->eps : 0.f;
+  p.rounding = fuse ? fuse->rounding : 0;
+  p.seed = fuse ? fuse->seed : 0;
   p.W = tables->weights;
   p.state = fuse ? fuse->state : nullptr;
   return hip_status(launch_grad_reduce(p, (hipStream_t)stream));
@@ -229,6 +232,8 @@ emb_status emb_sparse_update(const emb_tables* tables, const emb_update* update,
   p.dtype = tables->dtype;
   p.lr = update->lr;
   p.eps = update->eps;
+  p.rounding = update->rounding;
+  p.seed = update->seed;
   p.W = tables->weights;
   p.state = update->state;
   return hip_status(launch_sparse_update(p, (hipStream_t)stream));

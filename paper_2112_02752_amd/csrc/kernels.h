@@ -60,6 +60,8 @@ struct ReduceLaunch {
   // fused optimizer (fuse = 0: reduce only)
   int32_t fuse, opt, dtype;
   float lr, eps;
+  int32_t rounding;  // bf16 stores: 0 nearest even, 1 stochastic
+  uint64_t seed;
   void* W;
   float* state;
 };
@@ -73,6 +75,8 @@ struct UpdateLaunch {
   uint32_t rows;  // R: keys at or above it are skipped
   int32_t D, opt, dtype;
   float lr, eps;
+  int32_t rounding;  // bf16 stores: 0 nearest even, 1 stochastic
+  uint64_t seed;
   void* W;
   float* state;
 };

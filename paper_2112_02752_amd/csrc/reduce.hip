@@ -26,6 +26,8 @@ struct Upd {
   float* state;
   int32_t D, opt, fuse;
   float lr, eps;
+  int32_t rounding;  // bf16 stores: 0 nearest even, 1 stochastic
+  uint64_t seed;
 };
 
 struct RArgs {
@@ -79,6 +81,45 @@ struct Row4<uint16_t> {
     *reinterpret_cast<uint2*>(p) = v;
   }
 };
+
+// splitmix64 (Steele, Lea and Flood 2014): the output for generator state x
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9e3779b97f4a7c15ull;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+// Row of four stored values with stochastic rounding to bf16: element e of
+// counter c0 + e gets the top 16 bits of splitmix64(seed ^ splitmix64(c)),
+// added to the 16 bits below the bf16 mantissa, which are then cut off (the
+// magnitude rounds up with probability dropped / 2^16); non-finite values
+// round to nearest even.
+__device__ __forceinline__ void store_bf16_stochastic(uint16_t* p, const float (&o)[4], uint64_t seed, uint64_t c0) {
+  uint16_t b[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t u = __float_as_uint(o[e]);
+    const uint32_t r16 = (uint32_t)(splitmix64(seed ^ splitmix64(c0 + (uint64_t)e)) >> 48);
+    b[e] = (u & 0x7f800000u) == 0x7f800000u ? f32_to_bf16_rne(o[e]) : (uint16_t)((u + r16) >> 16);
+  }
+  uint2 v;
+  v.x = (uint32_t)b[0] | ((uint32_t)b[1] << 16);
+  v.y = (uint32_t)b[2] | ((uint32_t)b[3] << 16);
+  *reinterpret_cast<uint2*>(p) = v;
+}
+
+template <typename TW>
+__device__ __forceinline__ void store_w(const Upd& up, TW* p, const float (&o)[4], uint64_t c0);
+template <>
+__device__ __forceinline__ void store_w<float>(const Upd&, float* p, const float (&o)[4], uint64_t) {
+  Row4<float>::store(p, o);
+}
+template <>
+__device__ __forceinline__ void store_w<uint16_t>(const Upd& up, uint16_t* p, const float (&o)[4], uint64_t c0) {
+  if (up.rounding) store_bf16_stochastic(p, o, up.seed, c0);
+  else Row4<uint16_t>::store(p, o);
+}
 
 template <int G, int NV>
 __device__ __forceinline__ void zero(float (&acc)[NV][4]) {
@@ -207,7 +248,7 @@ __device__ __forceinline__ void apply_row(const Upd& up, float* grad_rows, int64
           w[e] = pre.w[v][e] - up.lr * acc[v][e] / (sqrtf(hv[v][e]) + up.eps);
         }
         Row4<float>::store(hp + c0, hv[v]);
-        Row4<TW>::store(wp + c0, w);
+        store_w<TW>(up, wp + c0, w, (uint64_t)r * (uint64_t)D + (uint64_t)c0);
       }
     }
     return;
@@ -219,7 +260,7 @@ __device__ __forceinline__ void apply_row(const Upd& up, float* grad_rows, int64
       float w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) w[e] = pre.w[v][e] - step * acc[v][e];
-      Row4<TW>::store(wp + c0, w);
+      store_w<TW>(up, wp + c0, w, (uint64_t)r * (uint64_t)D + (uint64_t)c0);
     }
   }
 }
@@ -742,6 +783,8 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.up.fuse = p.fuse;
   ra.up.lr = p.lr;
   ra.up.eps = p.eps;
+  ra.up.rounding = p.rounding;
+  ra.up.seed = p.seed;
   // main: two wavefronts per chunk of sorted positions (one for its heavy
   // pieces, one for a batch of light segments), up to two full devices
   const int bm = clamp_blocks(((int64_t)ra.nchunks + 1) / 2, 1, 4096);
@@ -764,6 +807,8 @@ hipError_t launch_sparse_update(const UpdateLaunch& p, hipStream_t s) {
   ua.up.fuse = 1;
   ua.up.lr = p.lr;
   ua.up.eps = p.eps;
+  ua.up.rounding = p.rounding;
+  ua.up.seed = p.seed;
   const int blocks = clamp_blocks((p.max_unique + 15) / 16, 1, 2048);
   return p.dtype == EMB_FP32 ? launch_update_dt<float>(ua, blocks, s) : launch_update_dt<uint16_t>(ua, blocks, s);
 }

@@ -336,6 +336,32 @@ def test_elementwise_adagrad_full_size(name, steps):
     parity.run_workload(w, steps=steps, h0=1.0)
 
 
+# ------------------------------------------------- bf16 stochastic rounding
+
+@pytest.mark.parametrize("opt,fused", [("adagrad", True), ("sgd", False), ("adagrad_ew", True)])
+def test_stochastic_rounding_small(opt, fused):
+    """bf16 tables with stochastic rounding: rows within the bf16 tolerance of
+    the oracle and, element by element, the same stored value almost
+    everywhere (both draw the same bits for every element)."""
+    _say(f"case stochastic rounding opt={opt} fused={fused}")
+    rng = np.random.default_rng(70)
+    rows = [3000, 2000]
+    B, D = 200, 64
+    off, idx = _rand_batch(rng, rows, B, 60, zipf=1.2)
+    W = _bf16_bits(rng.uniform(-0.5, 0.5, size=(sum(rows), D)).astype(np.float32))
+    G = rng.standard_normal((len(off) - 1, D)).astype(np.float32)
+    state0 = np.ones((sum(rows), D), np.float32) if opt == "adagrad_ew" else None
+    parity.run_case(_row_offset(rows), W, off, idx, G, B, "sum", opt, 0.05, 1e-8, state0=state0, fused=fused,
+                    rounding="stochastic", seed=0x1234)
+
+
+def test_stochastic_rounding_full_size():
+    """The 26-table bf16 workload, two steps with fresh seeds."""
+    w = synth.workload("c4")
+    _say("case stochastic rounding c4 x2")
+    parity.run_workload(w, steps=2, rounding="stochastic", seed=77)
+
+
 # ------------------------------------------------------------- int64 ids
 
 @pytest.mark.parametrize("pool,opt", [("sum", "adagrad"), ("mean", "sgd")])

@@ -443,6 +443,63 @@ def test_route_rejects_bad_shards():
             oracle.route_ids(1, ro, 1, off, idx, np.array(bad, np.int64))
 
 
+# ------------------------------------------------- bf16 stochastic rounding
+
+def test_sr_bits_match_the_input_generators_splitmix64():
+    """The oracle's random bits are the top 16 bits of the counter hash the
+    seeded input generator implements separately (splitmix64 of the seed xor
+    splitmix64 of the counter)."""
+    import synth
+    L = synth._lib()
+    for seed in (0, 1, 0x5EED0004, 2 ** 63 + 12345):
+        for c in (0, 1, 63, 64, 10 ** 9, 2 ** 40 + 7):
+            assert oracle.sr_bits(seed, c) == int(L.synth_hash(seed, c)) >> 48, (seed, c)
+
+
+def _bf16_neighbours(x: np.float32):
+    u = int(np.array([x], np.float32).view(np.uint32)[0])
+    down = u >> 16
+    return down, down + (1 if (u & 0xFFFF) else 0)
+
+
+def test_bf16_stochastic_rounding_is_exactly_unbiased_over_all_random_bits():
+    """Over all 2^16 values of the random bits, rounding up happens for
+    exactly (dropped bits) of them, so the mean of the rounded values is the
+    fp32 value exactly; every result is one of its two bf16 neighbours, and a
+    value bf16 holds exactly never moves."""
+    rng = np.random.default_rng(8)
+    xs = np.concatenate([rng.uniform(-2, 2, 6), rng.standard_normal(3) * 1e-3, [1.5, -0.25, 3.0]]).astype(np.float32)
+    for x in xs:
+        down, up = _bf16_neighbours(x)
+        outs = np.array([oracle.bf16_stochastic(float(x), r) for r in range(1 << 16)], np.uint32)
+        assert set(np.unique(outs)) <= {down, up}
+        vals = (outs << 16).view(np.float32).astype(np.float64)
+        assert vals.mean() == np.float64(x), (x, vals.mean())
+
+
+def test_stochastic_step_rounds_to_a_neighbour_with_the_elements_bits():
+    """A bf16 step with stochastic rounding stores, for every element, one of
+    the two bf16 neighbours of the fp32 result the nearest-even step would
+    round, and it depends on the seed."""
+    rng = np.random.default_rng(12)
+    ro, B, off, idx, Wf, G = random_case(rng, T=2, rows=(30, 20), D=8, B=10, dyadic=False)
+    T = len(ro) - 1
+    Wb = ((Wf.view(np.uint32).astype(np.uint64) + 0x7FFF + ((Wf.view(np.uint32) >> 16) & 1)) >> 16).astype(np.uint16)
+    ref = RowStore(Wf.copy())  # fp32 table with the same starting values
+    ref.vals[:] = (Wb.astype(np.uint32) << 16).view(np.float32)
+    oracle.step(T, ro, B, off, idx, G, ref, "sum", "sgd", 0.5, 0.0)
+    stores = []
+    for seed in (1, 2):
+        st = RowStore(Wb.copy())
+        oracle.step(T, ro, B, off, idx, G, st, "sum", "sgd", 0.5, 0.0, rounding="stochastic", seed=seed)
+        stores.append(st.vals.copy())
+        for r in np.unique(keys_of(ro, B, off, idx)):
+            for d in range(8):
+                down, up = _bf16_neighbours(ref.vals[r, d])
+                assert int(st.vals[r, d]) in (down, up)
+    assert (stores[0] != stores[1]).any()
+
+
 # ------------------------------------------------------------ sparse store
 
 def test_sparse_row_store_equals_dense():

@@ -37,6 +37,9 @@ MUTANTS = {
     "route_upper_bound_inclusive": ("if (key < shard_start[r] || key >= shard_start[r + 1]) continue;",
                                     "if (key < shard_start[r] || key > shard_start[r + 1]) continue;"),
     "route_global_ids": ("send_ids[k] = (int32_t)(key - shard_start[r]);", "send_ids[k] = (int32_t)key;"),
+    "sr_truncate": ("return (uint16_t)((u + (r16 & 0xffffu)) >> 16);", "return (uint16_t)(u >> 16);"),
+    "sr_low_bits": ("return (uint32_t)(splitmix64(seed ^ splitmix64(c)) >> 48);",
+                    "return (uint32_t)(splitmix64(seed ^ splitmix64(c)) & 0xffffu);"),
     "counts_off_by_one": ("counts[u] = seg_offsets[u + 1] - seg_offsets[u];",
                           "counts[u] = seg_offsets[u + 1] - seg_offsets[u] + (u == 0);"),
 }
@@ -80,6 +83,8 @@ def _run_pins(so_path):
             lambda: T.test_elementwise_adagrad_matches_torch_optim("sum", 0.0),
             lambda: T.test_route_matches_numpy(8, 2),
             lambda: T.test_route_fragments_reassemble_the_forward("sum", False),
+            lambda: T.test_sr_bits_match_the_input_generators_splitmix64(),
+            lambda: T.test_bf16_stochastic_rounding_is_exactly_unbiased_over_all_random_bits(),
         ]
         for p in pins:
             try:

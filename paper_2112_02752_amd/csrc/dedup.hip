@@ -47,6 +47,18 @@ namespace {
 
 constexpr uint64_t kFlagAgg = 1, kFlagInc = 2;
 
+// One wavefront's digits added to an LDS histogram.  The lanes that share
+// lane 0's digit add once, through lane 0: skewed batches put most of a
+// wavefront's keys on one digit (the later passes see the high bits of
+// mostly small ids), and lane-by-lane atomics on one LDS word serialise.
+// Valid lanes are the low ones, so lane 0 is valid whenever any lane is.
+__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t d, bool valid, int lane) {
+  const uint32_t d0 = (uint32_t)__shfl((int)d, 0, kWave);
+  const uint64_t same = __ballot(valid && d == d0);
+  if (valid && d != d0) atomicAdd(&hist[d], 1u);
+  if (lane == 0 && same) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+}
+
 // ------------------------------------------------------------------ prepare
 
 struct PrepArgs {
@@ -586,8 +598,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   uint32_t my_cnt[DPT];
   auto publish_counts = [&]() {
 #pragma unroll
-    for (int i = 0; i < IT; ++i)
-      if (wbase + i * kWave + lane < a.N) atomicAdd(&s_hist[dig[i]], 1u);
+    for (int i = 0; i < IT; ++i) hist_add(s_hist, dig[i], wbase + i * kWave + lane < a.N, lane);
     __syncthreads();
     uint64_t* row = a.coresident ? a.rows + (size_t)tile * a.status_stride
                                  : a.status + (size_t)tile * a.status_stride;
@@ -608,7 +619,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
         const uint32_t pm = (1u << a.pass_bits[p]) - 1u;
 #pragma unroll
         for (int i = 0; i < IT; ++i)
-          if (wbase + i * kWave + lane < a.N) atomicAdd(&s_cnt[p - 1][(key[i] >> a.pass_shift[p]) & pm], 1u);
+          hist_add(s_cnt[p - 1], (key[i] >> a.pass_shift[p]) & pm, wbase + i * kWave + lane < a.N, lane);
       }
       __syncthreads();
       for (int p = 1; p < a.npass; ++p) {

@@ -277,15 +277,47 @@ def test_workload_full_size_one_step(name):
     parity.run_workload(w, steps=1)
 
 
-@pytest.mark.parametrize("bags,concurrent", [(16384, True), (17000, False), (23000, True), (40000, False)])
-def test_sort_tile_modes(bags, concurrent):
+@pytest.mark.parametrize("rows_div,bags,concurrent", [(1, 16384, True), (1, 17000, False), (1, 23000, True),
+                                                     (1, 40000, False), (50, 16384, False), (50, 23000, True)])
+def test_sort_tile_modes(rows_div, bags, concurrent):
     """Batches of the 50M-row workload's shape whose sizes select each sort
     mode: co-resident passes with 2048-, 2560- and 4096-key tiles (at most
-    one block per compute unit), and the ticket look-back beyond that."""
+    one block per compute unit) and the ticket look-back beyond that, for
+    26-bit keys (three passes) and 20-bit keys (rows / 50: two passes)."""
     import dataclasses
-    w = dataclasses.replace(synth.workload("c3"), bags_per_table=bags, name=f"c3-b{bags}")
-    _say(f"case sort tile modes bags={bags} concurrent={concurrent}")
+    w = dataclasses.replace(synth.scaled(synth.workload("c3"), rows_div=rows_div), bags_per_table=bags,
+                            name=f"c3/r{rows_div}-b{bags}")
+    _say(f"case sort tile modes rows/{rows_div} bags={bags} concurrent={concurrent}")
     parity.run_workload(w, steps=1, concurrent=concurrent)
+
+
+@pytest.mark.parametrize("rows_div", [1, 2, 4, 8, 16, 32])
+def test_sort_key_widths_21_to_26_bits(rows_div):
+    """Every key width from 26 down to 21 bits (rows of the 50M-row table
+    divided by 1..32: three radix passes of 7 to 9 bits), 1024 bags."""
+    w = synth.scaled(synth.workload("c3"), rows_div=rows_div, bags_div=16)
+    _say(f"case sort key bits={w.key_bits} bags={w.bags_per_table}")
+    assert 21 <= w.key_bits <= 26
+    parity.run_workload(w, steps=1)
+
+
+@pytest.mark.parametrize("name,bags", [("c3", 1), ("c3", 137), ("c3", 3000), ("c2", 2), ("c2", 500)])
+def test_sort_small_batches(name, bags):
+    """One tile, a ragged second tile, and several tiles, two steps on one
+    workspace; one table (the ids are the keys) and eight (keys built from
+    the bags)."""
+    import dataclasses
+    w = dataclasses.replace(synth.workload(name), bags_per_table=bags, name=f"{name}-b{bags}")
+    _say(f"case sort small {name} bags={bags}")
+    parity.run_workload(w, steps=2)
+
+
+def test_sort_three_passes_coresident():
+    """28-bit keys (the 200M-row table) in a batch small enough for
+    co-resident 10-bit passes: three passes with digit-range prefix blocks."""
+    w = synth.scaled(synth.workload("c5"), bags_div=8)
+    _say(f"case three co-resident passes bags={w.bags_per_table}")
+    parity.run_workload(w, steps=1)
 
 
 # ------------------------------------------------ element-wise Adagrad variant

@@ -47,18 +47,6 @@ namespace {
 
 constexpr uint64_t kFlagAgg = 1, kFlagInc = 2;
 
-// One wavefront's digits added to an LDS histogram.  The lanes that share
-// lane 0's digit add once, through lane 0: skewed batches put most of a
-// wavefront's keys on one digit (the later passes see the high bits of
-// mostly small ids), and lane-by-lane atomics on one LDS word serialise.
-// Valid lanes are the low ones, so lane 0 is valid whenever any lane is.
-__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t d, bool valid, int lane) {
-  const uint32_t d0 = (uint32_t)__shfl((int)d, 0, kWave);
-  const uint64_t same = __ballot(valid && d == d0);
-  if (valid && d != d0) atomicAdd(&hist[d], 1u);
-  if (lane == 0 && same) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
-}
-
 // ------------------------------------------------------------------ prepare
 
 struct PrepArgs {

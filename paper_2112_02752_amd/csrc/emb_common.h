@@ -185,6 +185,19 @@ __device__ __forceinline__ int32_t load_id(const void* idx, int32_t idx64, int64
   return idx64 ? (int32_t) static_cast<const int64_t*>(idx)[j] : static_cast<const int32_t*>(idx)[j];
 }
 
+// One wavefront's values added to an LDS histogram.  The lanes that share
+// lane 0's value add once, through lane 0: skewed batches put most of a
+// wavefront's keys in one bin (a radix sort's high digits of mostly small
+// ids, the owner of the hot rows), and lane-by-lane atomics on one LDS word
+// serialise.  Valid lanes are the low ones, so lane 0 is valid whenever any
+// lane is.  Called by every lane of the wavefront.
+__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t d, bool valid, int lane) {
+  const uint32_t d0 = (uint32_t)__shfl((int)d, 0, kWave);
+  const uint64_t same = __ballot(valid && d == d0);
+  if (valid && d != d0) atomicAdd(&hist[d], 1u);
+  if (lane == 0 && same) atomicAdd(&hist[d0], (uint32_t)__popcll(same));
+}
+
 // number of set bits of `mask` below this lane
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));

@@ -186,11 +186,11 @@ __device__ __forceinline__ int32_t load_id(const void* idx, int32_t idx64, int64
 }
 
 // One wavefront's values added to an LDS histogram.  The lanes that share
-// lane 0's value add once, through lane 0: skewed batches put most of a
-// wavefront's keys in one bin (a radix sort's high digits of mostly small
-// ids, the owner of the hot rows), and lane-by-lane atomics on one LDS word
-// serialise.  Valid lanes are the low ones, so lane 0 is valid whenever any
-// lane is.  Called by every lane of the wavefront.
+// lane 0's value add once, through lane 0: in a skewed batch many of a
+// wavefront's keys are the hottest id (a fifth of them in the 50M-row
+// workload), whose digit is one bin in every radix pass, and lane-by-lane
+// atomics on one LDS word serialise.  Valid lanes are the low ones, so lane 0
+// is valid whenever any lane is.  Called by every lane of the wavefront.
 __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t d, bool valid, int lane) {
   const uint32_t d0 = (uint32_t)__shfl((int)d, 0, kWave);
   const uint64_t same = __ballot(valid && d == d0);

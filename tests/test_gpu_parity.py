@@ -438,6 +438,57 @@ def test_c5_three_consecutive_steps():
     parity.run_workload(w, steps=3)
 
 
+def test_c5_hundred_steps_sampled_rows():
+    """All 100 steps of the 200M-row workload on the device, then a sample of
+    rows (the first batch's 1000 hottest ids, 4000 more of its ids, the last
+    row) against the oracle replaying every step's update of just those rows,
+    and rows that no step touched against their initial values.  With sum
+    pooling a row's gradient sums the upstream rows of its own id's positions
+    only, so each batch is cut down to the positions of the sampled ids (bags
+    kept, shortened) before the oracle's dedup, reduce and SGD step."""
+    import oracle
+    import paper_2112_02752_amd as emb
+    torch = parity.torch_mod()
+    w = synth.workload("c5")
+    assert w.steps == 100 and w.pool == "sum" and w.num_tables == 1
+    _say(f"case c5 x{w.steps} steps, sampled rows")
+    dl = parity.device_layer_from_workload(w)
+    b0 = synth.make_batch(w, 0, with_grad=False)
+    ids, cnt = np.unique(b0.indices, return_counts=True)
+    rng = np.random.default_rng(100)
+    hot = ids[np.argsort(-cnt, kind="stable")[:1000]]
+    sample = np.unique(np.concatenate([hot, rng.choice(ids, 4000, replace=False),
+                                       [w.total_rows - 1]])).astype(np.uint32)
+    untouched = np.setdiff1d(np.unique(rng.integers(0, w.total_rows, 2000)), sample)
+    store = oracle.RowStore(synth.weight_rows(w, sample), keys=sample)
+    B, M = w.bags_per_table, w.num_bags
+    layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state,
+                      max_indices=M * max(t.lmax for t in w.tables), max_bags=M)
+    out = torch.empty((M, w.dim), dtype=torch.float32, device=dl.W.device)
+    for s in range(w.steps):
+        b = synth.make_batch(w, s)
+        off = torch.from_numpy(b.offsets).to(dl.W.device)
+        idx = torch.from_numpy(b.indices).to(dl.W.device)
+        G = torch.from_numpy(b.grad).to(dl.W.device)
+        layer.step(emb.Batch(off, idx, B), out, G)
+        keep = np.isin(b.indices, sample)
+        bag = np.repeat(np.arange(M), np.diff(b.offsets))
+        off_f = np.concatenate([[0], np.cumsum(np.bincount(bag[keep], minlength=M))]).astype(np.int32)
+        idx_f = np.ascontiguousarray(b.indices[keep])
+        dd = oracle.unique_ids(1, w.row_offset, B, off_f, idx_f)
+        _, acc = oracle.grad_reduce(1, B, off_f, b.grad, w.pool, dd)
+        oracle.sparse_update(store, dd.unique_keys, acc, w.opt, w.lr, w.eps)
+        untouched = untouched[~np.isin(untouched, b.indices)]
+        if s % 20 == 19:
+            _say(f"  step {s + 1} done")
+    torch.cuda.synchronize()
+    eo = emb.workspace_error_offset()
+    assert int(layer.ws[eo:eo + 4].cpu().numpy().view(np.uint32)[0]) == 0
+    parity.check_rows(dl, store, sample, w.opt)
+    assert untouched.size > 0
+    np.testing.assert_array_equal(dl.rows(untouched.astype(np.uint32)), synth.weight_rows(w, untouched))
+
+
 def test_c2_unfused_path():
     w = synth.workload("c2")
     _say("case c2 unfused")

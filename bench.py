@@ -145,7 +145,19 @@ def cpu_baseline(w, batches, budget_s: float):
     return {"value": done_n / elapsed, "unit": "lookups/s", "cores": 1, "kind": "oracle",
             "sample": f"{steps} whole steps of {w.name} (fwd+dedup+reduce+update; rows the batch touches "
                       f"regenerated from the seed, untimed), {done_n} lookups, {elapsed:.1f} s of oracle time, "
-                      f"single thread"}
+                      f"single thread",
+            "host": {"cpu_model": host_cpu_model(), "nproc": os.cpu_count()}}
+
+
+def host_cpu_model() -> str:
+    """The host CPU's model name (the oracle's machine), from /proc/cpuinfo."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cost_model_check(w, N, U, t_phase, ms):

@@ -709,10 +709,11 @@ hipError_t launch_reduce_t(const RArgs& ra, int blocks_main, int blocks_comb, hi
   return hipGetLastError();
 }
 
-// Rows of more than 32 values are held two vectors per lane (half as many
-// lanes per row, twice as many rows per wavefront): a wavefront then carries
-// twice the light segments, which outweighs the lower occupancy (measured on
-// rows of 64 fp32 and 128 bf16 values); narrower rows keep one vector.
+// Rows of 33 to 64 values are held two vectors per lane (half as many lanes
+// per row, twice as many rows per wavefront): a wavefront then carries twice
+// the light segments, which outweighs the lower occupancy (measured on rows
+// of 64 fp32 values).  Narrower rows, and wider ones (128 bf16 values lost on
+// small batches), keep one vector.
 template <typename TW>
 hipError_t launch_reduce_dt(const RArgs& ra, int bm, int bc, hipStream_t s) {
   const int vecs = (ra.D + 3) / 4;
@@ -721,8 +722,8 @@ hipError_t launch_reduce_dt(const RArgs& ra, int bm, int bc, hipStream_t s) {
   if (vecs <= 4) return launch_reduce_t<TW, 4, 1>(ra, bm, bc, s);
   if (vecs <= 8) return launch_reduce_t<TW, 8, 1>(ra, bm, bc, s);
   if (vecs <= 16) return launch_reduce_t<TW, 8, 2>(ra, bm, bc, s);
-  if (vecs <= 32) return launch_reduce_t<TW, 16, 2>(ra, bm, bc, s);
-  if (vecs <= 64) return launch_reduce_t<TW, 32, 2>(ra, bm, bc, s);
+  if (vecs <= 32) return launch_reduce_t<TW, 32, 1>(ra, bm, bc, s);
+  if (vecs <= 64) return launch_reduce_t<TW, 64, 1>(ra, bm, bc, s);
   if (vecs <= 128) return launch_reduce_t<TW, 64, 2>(ra, bm, bc, s);
   if (vecs <= 256) return launch_reduce_t<TW, 64, 4>(ra, bm, bc, s);
   return hipErrorInvalidValue;
@@ -744,8 +745,8 @@ hipError_t launch_update_dt(const UArgs& ua, int blocks, hipStream_t s) {
   if (vecs <= 4) return launch_update_t<TW, 4, 1>(ua, blocks, s);
   if (vecs <= 8) return launch_update_t<TW, 8, 1>(ua, blocks, s);
   if (vecs <= 16) return launch_update_t<TW, 8, 2>(ua, blocks, s);
-  if (vecs <= 32) return launch_update_t<TW, 16, 2>(ua, blocks, s);
-  if (vecs <= 64) return launch_update_t<TW, 32, 2>(ua, blocks, s);
+  if (vecs <= 32) return launch_update_t<TW, 32, 1>(ua, blocks, s);
+  if (vecs <= 64) return launch_update_t<TW, 64, 1>(ua, blocks, s);
   if (vecs <= 128) return launch_update_t<TW, 64, 2>(ua, blocks, s);
   if (vecs <= 256) return launch_update_t<TW, 64, 4>(ua, blocks, s);
   return hipErrorInvalidValue;

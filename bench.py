@@ -56,6 +56,7 @@ def parse():
                          "batch k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
     ap.add_argument("--route-ranks", type=int, default=8,
                     help="also time emb_route_ids of the same batches over this many equal row ranges (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
@@ -357,6 +358,37 @@ def main():
                    "bytes_per_launch": float(r_bytes), "achieved_GBs": r_bytes / r_s / 1e9,
                    "frac": r_bytes / r_s / 1e9 / HBM_PEAK_GBS}
 
+    # the serial step captured in a HIP graph: one batch, replayed back to back,
+    # against the same batch's eager steps (the step launches only kernels)
+    graph = None
+    if not args.no_graph:
+        i0 = args.warmup
+        reps = 20
+        ge = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        torch.cuda.synchronize()
+        ge[0].record(stream)
+        for _ in range(reps):
+            layer.step(dev_batches[i0][0], out, dev_batches[i0][1], sp)
+        ge[1].record(stream)
+        torch.cuda.synchronize()
+        try:
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                layer.step(dev_batches[i0][0], out, dev_batches[i0][1])
+            gr.replay()
+            torch.cuda.synchronize()
+            ge[2].record(stream)
+            for _ in range(reps):
+                gr.replay()
+            ge[3].record(stream)
+            torch.cuda.synchronize()
+            graph = {"note": f"serial steps of batch {i0} ({dev_batches[i0][2]} lookups), {reps} back to back "
+                             f"each way", "eager_us_per_step": ge[0].elapsed_time(ge[1]) * 1e3 / reps,
+                     "graph_replay_us_per_step": ge[2].elapsed_time(ge[3]) * 1e3 / reps}
+            del gr
+        except RuntimeError as e:  # reported, not fatal: the headline does not depend on it
+            graph = {"error": str(e)[:200]}
+
     n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
 
     # unique counts of the timed batches (for the byte models)
@@ -415,6 +447,7 @@ def main():
         "cold": None if cold is None else dict(cold, lookups_per_s=N_avg * 1e6 / cold["median_us"]),
         "achievable_copy_GBs": copy_gbs,
         "routing": routing,
+        "graph": graph,
         "cost_model": cost_model_check(w, N_avg, U_avg, t_phase, ms),
     }
     if not args.no_cpu_baseline:

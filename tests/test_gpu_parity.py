@@ -489,6 +489,61 @@ def test_c5_hundred_steps_sampled_rows():
     np.testing.assert_array_equal(dl.rows(untouched.astype(np.uint32)), synth.weight_rows(w, untouched))
 
 
+def test_graph_replay_matches_eager():
+    """The serial step captured once in a HIP graph (torch.cuda.graph) and
+    replayed on four batches of one size, each copied into the captured input
+    buffers, with eager steps of a twin layer and host synchronisations
+    between the replays: every replay's pooled output, table and Adagrad
+    state equal the eager twin's bit for bit (the step launches kernels
+    only, with no memset nodes)."""
+    import paper_2112_02752_amd as emb
+    torch = parity.torch_mod()
+    _say("case graph replay vs eager")
+    rows, B, D, N = 200_000, 2048, 64, 2048 * 30
+    rng = np.random.default_rng(11)
+
+    def batch():
+        cuts = np.sort(rng.integers(0, N + 1, size=B - 1))
+        off = np.concatenate([[0], cuts, [N]]).astype(np.int32)
+        idx = ((rng.zipf(1.2, size=N) - 1) % rows).astype(np.int32)
+        return off, idx, rng.standard_normal((B, D)).astype(np.float32)
+
+    dev = "cuda"
+    W0 = torch.from_numpy(rng.uniform(-0.01, 0.01, size=(rows, D)).astype(np.float32)).to(dev)
+    Wa, Wb = W0.clone(), W0.clone()
+    ha, hb = torch.zeros(rows, device=dev), torch.zeros(rows, device=dev)
+    la = emb.Layer(emb.Tables(Wa, [0, rows]), "sum", "adagrad", 0.01, 1e-8, ha, max_indices=N, max_bags=B)
+    lb = emb.Layer(emb.Tables(Wb, [0, rows]), "sum", "adagrad", 0.01, 1e-8, hb, max_indices=N, max_bags=B)
+    off_s = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    idx_s = torch.empty(N, dtype=torch.int32, device=dev)
+    G_s = torch.empty((B, D), device=dev)
+    out_s = torch.empty((B, D), device=dev)
+    out_a = torch.empty((B, D), device=dev)
+
+    def step_both(b, replay=None):
+        off_s.copy_(torch.from_numpy(b[0]))
+        idx_s.copy_(torch.from_numpy(b[1]))
+        G_s.copy_(torch.from_numpy(b[2]))
+        if replay is None:
+            lb.step(emb.Batch(off_s, idx_s, B), out_s, G_s)
+        else:
+            replay.replay()
+        torch.cuda.synchronize()
+        off_a, idx_a, G_a = (torch.from_numpy(x).to(dev) for x in b)
+        la.step(emb.Batch(off_a, idx_a, B), out_a, G_a)
+        torch.cuda.synchronize()
+        assert torch.equal(out_s, out_a)
+        assert torch.equal(Wb, Wa) and torch.equal(hb, ha)
+
+    step_both(batch())  # eager warm-up on both layers
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lb.step(emb.Batch(off_s, idx_s, B), out_s, G_s)
+    for _ in range(4):
+        step_both(batch(), replay=g)
+    assert not torch.equal(Wb, W0)
+
+
 def test_c2_unfused_path():
     w = synth.workload("c2")
     _say("case c2 unfused")

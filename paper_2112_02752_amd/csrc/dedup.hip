@@ -5,21 +5,22 @@
 //   unique_keys / seg_offsets / counts = the runs of equal sorted keys
 //
 // Kernels, in stream order:
-//  1. k_prepare: one wavefront per bag writes the bag id of every position
-//     (and the key, for several tables), and counts the digits of every
-//     radix pass into LDS histograms that are added to global totals.
-//  2. k_sort_pass (once per digit): a tile publishes its per-digit counts
-//     (an LDS histogram) as soon as its keys are loaded, then ranks its keys
-//     with wavefront ballots (the lanes sharing a digit are found with one
-//     ballot per digit bit, the rank is a masked popcount) and reorders them
-//     in LDS by digit.  Each digit's offset among earlier tiles comes either
-//     from prefix blocks (when every tile is resident at once: one block per
-//     group of tiles sums the published counts and publishes final offsets)
-//     or from a decoupled look-back over tile status words.  The tile is then
-//     written out in digit runs.  Ranks follow position order within a tile
-//     and tiles follow position order, so every pass is stable and so is the
-//     whole sort.
-//  3. k_unique: head flags key[k] != key[k-1], a block scan plus a look-back
+//  1. k_sort_pass (once per digit): a tile ranks its keys with wavefront
+//     ballots (the lanes sharing a digit are found with one ballot per digit
+//     bit, the rank is a masked popcount), reorders them in LDS by digit and
+//     writes them out in digit runs.  Each digit's offset among earlier tiles
+//     comes from one of two schemes.  When every tile of a pass is resident
+//     at once, the tile publishes its digit counts (an LDS histogram) as soon
+//     as its keys are loaded, and prefix blocks launched after the tiles sum
+//     the published counts and publish final offsets while the tiles rank;
+//     the first pass also finds each position's bag.  Otherwise k_prepare
+//     first writes every position's bag id (and key, for several tables), and
+//     each pass is preceded by k_tile_counts (every tile's digit counts) and
+//     k_column_scan (per digit, the prefix of those counts over the tiles,
+//     and the digit's total), so that the pass reads its offsets with no
+//     wait.  Ranks follow position order within a tile and tiles follow
+//     position order, so every pass is stable and so is the whole sort.
+//  2. k_unique: head flags key[k] != key[k-1], a block scan plus a look-back
 //     of (number of heads, last head position) gives every head its segment
 //     index and the length of the previous segment.
 #include "emb_common.h"
@@ -45,6 +46,7 @@ SortPlan make_sort_plan(int key_bits) {
 
 namespace {
 
+// status word flags of the unique scan's look-back: aggregate, inclusive prefix
 constexpr uint64_t kFlagAgg = 1, kFlagInc = 2;
 
 // ------------------------------------------------------------------ prepare
@@ -54,27 +56,20 @@ struct PrepArgs {
   const void* idx;
   int32_t idx64;
   TableOffsets ro;
-  int32_t B, M, bags_per_block, npass, histograms;
-  int32_t shift[kMaxPasses], bits[kMaxPasses];
+  int32_t B, M, bags_per_block;
   uint32_t* keys_out;  // null for int32 ids of one table (the ids are the keys)
   int32_t* bag_of;
-  uint32_t* totals;    // [kMaxPasses][kMaxDigits], zero on entry (only with histograms)
 };
 
-// Used when the tiles of a pass are not all resident at once (the look-back
-// needs every pass's digit totals up front).  A block owns a contiguous range
-// of bags and therefore of positions.  The bags' offsets are staged in LDS;
-// every thread takes positions of the range in strides, finds each one's bag
-// by a binary search in LDS, and writes the bag id (and the key for several
-// tables); the digits of every radix pass are counted in LDS and added to the
-// global totals.
+// Used when the tiles of a pass are not all resident at once.  A block owns a
+// contiguous range of bags and therefore of positions.  The bags' offsets are
+// staged in LDS; every thread takes positions of the range in strides, finds
+// each one's bag by a binary search in LDS, and writes the bag id (and the key
+// for several tables).
 __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
   constexpr int UN = 8;
-  __shared__ uint32_t hist[kMaxPasses * kMaxDigits];
   __shared__ int32_t s_off[kPrepMaxBags + 1];
   const int tid = threadIdx.x;
-  if (a.histograms)
-    for (int i = tid; i < a.npass * kMaxDigits; i += kPrepThreads) hist[i] = 0;
   const int m0 = blockIdx.x * a.bags_per_block;
   const int nb = min(a.M - m0, a.bags_per_block);
   for (int i = tid; i <= nb; i += kPrepThreads) s_off[i] = a.offsets[m0 + i];
@@ -101,19 +96,7 @@ __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
         const uint32_t key = a.ro.off[m / a.B] + (uint32_t)id[u];
         a.bag_of[j] = m;
         if (a.keys_out) a.keys_out[j] = key;
-        if (a.histograms)
-          for (int p = 0; p < a.npass; ++p)
-            atomicAdd(&hist[p * kMaxDigits + ((key >> a.shift[p]) & ((1u << a.bits[p]) - 1u))], 1u);
       }
-    }
-  }
-  if (!a.histograms) return;
-  __syncthreads();
-  for (int p = 0; p < a.npass; ++p) {
-    const int nd = 1 << a.bits[p];
-    for (int d = tid; d < nd; d += kPrepThreads) {
-      const uint32_t v = hist[p * kMaxDigits + d];
-      if (v) atomic_add_u32(&a.totals[p * kMaxDigits + d], v);
     }
   }
 }
@@ -129,7 +112,7 @@ struct PassArgs {
   int32_t* bags_out;
   uint32_t* totals;        // this pass's digit totals (global histogram)
   uint32_t* prev_totals;   // the previous pass's totals, cleared here (null for the first pass)
-  uint64_t* status;        // look-back: [tiles][status_stride], zeroed by k_prepare of the same call
+  uint64_t* status;        // co-resident: each tile's final digit offsets (tag << 32 | offset): [tiles][status_stride]
   uint64_t* rows;          // published tile counts (tag << 32 | count): [tiles][status_stride]
   uint64_t* grp;           // published group sums, same form: [groups][status_stride]
   WsHeader* hdr;
@@ -145,6 +128,8 @@ struct PassArgs {
   uint64_t* uniq_status;
   int32_t uniq_tiles;
   int32_t N, ntiles, shift, bits, pass, status_stride;
+  const uint32_t* prefix;  // reduce-then-scan (tiles not co-resident): [tiles][status_stride], each digit's
+                           // count in the tiles before this one, from k_tile_counts and k_column_scan
   int32_t coresident;      // 1: every tile is resident at once (tile = block index, prefix blocks
                            //    after the tiles publish each tile's final digit offsets)
   int32_t prefix_mode;     // co-resident: kPrefixGroups or kPrefixRanges
@@ -191,50 +176,6 @@ __device__ __forceinline__ void block_excl_scan(uint32_t* arr, uint32_t* s_wsum)
     }
   }
   __syncthreads();
-}
-
-// Count of digit d in all tiles before `tile`: walks back over the tiles'
-// status words, kLookbackWindow of them per round (loaded together), adding
-// aggregates until it reaches an inclusive prefix.  A word that is not yet
-// published (wrong tag or no flag) ends the round; the next round starts
-// there.  The wait is bounded in time (kWaitTicks).
-__device__ __forceinline__ uint32_t lookback_digit(const uint64_t* status, int stride, int tile, int d,
-                                                   uint32_t tag, WsHeader* h, uint32_t site) {
-  uint32_t excl = 0;
-  int j = tile - 1;
-  uint32_t spins = 0;
-  const uint64_t t0 = wait_clock();
-  while (j >= 0) {
-    uint64_t sv[kLookbackWindow];
-#pragma unroll
-    for (int k = 0; k < kLookbackWindow; ++k)
-      sv[k] = (j - k >= 0) ? ld_acquire_u64(status + (size_t)(j - k) * stride + d) : 0;
-    int consumed = 0;
-    bool stop = false, inc = false;
-#pragma unroll
-    for (int k = 0; k < kLookbackWindow; ++k) {
-      if (!stop) {
-        const uint64_t flag = (sv[k] >> 30) & 3u;
-        if (j - k >= 0 && (uint32_t)(sv[k] >> 32) == tag && flag != 0) {
-          excl += (uint32_t)(sv[k] & 0x3fffffffu);
-          consumed = k + 1;
-          if (flag == kFlagInc) inc = stop = true;
-        } else {
-          stop = true;
-        }
-      }
-    }
-    if (inc) break;
-    j -= consumed;
-    if (consumed == 0) {
-      if (wait_over(h, t0, ++spins)) {
-        flag_timeout(h, site);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  return excl;
 }
 
 // Two-level prefix of a co-resident pass, for digit d.  Published words are
@@ -539,28 +480,20 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   __shared__ int32_t s_vals[TILE];
   __shared__ int32_t s_bags[TILE];
   __shared__ uint32_t s_wsum[NW];
-  __shared__ int s_tile;
   __shared__ int32_t s_boff[kBagStage + 1];
   __shared__ int s_lohi[2];
   __shared__ uint32_t s_toff[EMB_MAX_TABLES];
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  if (a.coresident) {
-    if (tid == 0) s_tile = blockIdx.x;
-  } else if (tid == 0) {
-    s_tile = (int)atomic_add_u32(&a.hdr->ticket[a.pass], 1u);
-  }
   for (int i = tid; i < NW * ND; i += kSortThreads) (&s_cnt[0][0])[i] = 0u;
   for (int i = tid; i < ND; i += kSortThreads) s_hist[i] = 0u;
   if (a.search_bags && a.T > 1)
     for (int t = tid; t < a.T; t += kSortThreads) s_toff[t] = a.ro.off[t];
-  // the previous pass is complete: clear its totals and ticket for the next call
-  if (blockIdx.x == 0 && a.prev_totals) {
+  // the previous pass is complete: clear its totals for the next call
+  if (blockIdx.x == 0 && a.prev_totals)
     for (int d = tid; d < kMaxDigits; d += kSortThreads) a.prev_totals[d] = 0u;
-    if (tid == 0) a.hdr->ticket[a.pass - 1] = 0u;
-  }
   __syncthreads();
-  const int tile = s_tile;
+  const int tile = blockIdx.x;
   const uint32_t mask = (1u << a.bits) - 1u;
   // the call's tag: the header's generation advances once per call, at its end
   const uint32_t tag = 0x80000000u | ((a.hdr->gen + 1u) * 8u + (uint32_t)a.pass);
@@ -583,22 +516,16 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   // (from an LDS histogram), so that the other tiles' prefixes advance while
   // this tile finds its bags, ranks and reorders its keys.
   const uint64_t tag_hi = (uint64_t)tag << 32;
-  uint32_t my_cnt[DPT];
   auto publish_counts = [&]() {
+    if (!a.coresident) return;  // the offsets were computed before the pass
 #pragma unroll
     for (int i = 0; i < IT; ++i) hist_add(s_hist, dig[i], wbase + i * kWave + lane < a.N, lane);
     __syncthreads();
-    uint64_t* row = a.coresident ? a.rows + (size_t)tile * a.status_stride
-                                 : a.status + (size_t)tile * a.status_stride;
-    const uint64_t flag = a.coresident ? 0 : ((tile == 0 ? kFlagInc : kFlagAgg) << 30);
+    uint64_t* row = a.rows + (size_t)tile * a.status_stride;
 #pragma unroll
     for (int k = 0; k < DPT; ++k) {
       const int d = tid + k * kSortThreads;
-      my_cnt[k] = 0;
-      if (d < ND) {
-        my_cnt[k] = s_hist[d];
-        st_u64(row + d, tag_hi | flag | my_cnt[k]);
-      }
+      if (d < ND) st_u64(row + d, tag_hi | s_hist[d]);
     }
     if (a.later) {
       // then the later passes' digits (counted in s_cnt, which stays zero
@@ -736,15 +663,10 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       if (d < ND) s_gbase[d] = 0;
     }
   } else {
-    uint64_t* st = a.status + (size_t)tile * a.status_stride;
 #pragma unroll
     for (int k = 0; k < DPT; ++k) {
       const int d = tid + k * kSortThreads;
-      excl[k] = 0;
-      if (d < ND && tile > 0) {
-        excl[k] = lookback_digit(a.status, a.status_stride, tile, d, tag, a.hdr, kSiteLookback | ((uint32_t)a.pass << 4));
-        st_u64(st + d, tag_hi | (kFlagInc << 30) | (excl[k] + my_cnt[k]));
-      }
+      excl[k] = d < ND ? a.prefix[(size_t)tile * a.status_stride + d] : 0u;
     }
   }
 #pragma unroll
@@ -771,6 +693,89 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   }
 }
 
+// ------------------------------------------------- reduce-then-scan passes
+//
+// When the tiles of a pass cannot all be resident at once, a pass takes three
+// kernels instead of a look-back: each tile's digit counts, then per digit the
+// exclusive prefix of those counts over the tiles (and the digit's total), and
+// the pass itself, which reads its tile's offsets with no wait.
+
+struct CountArgs {
+  const uint32_t* keys;
+  int32_t N, shift, bits, stride;
+  uint32_t* counts;  // [tiles][stride]
+};
+
+template <int IT>
+__global__ __launch_bounds__(kSortThreads) void k_tile_counts(CountArgs a) {
+  __shared__ uint32_t s_hist[kMaxDigits];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  const int nd = 1 << a.bits;
+  const uint32_t mask = (uint32_t)nd - 1u;
+  for (int i = tid; i < nd; i += kSortThreads) s_hist[i] = 0u;
+  __syncthreads();
+  const int64_t wbase = (int64_t)blockIdx.x * (kSortThreads * IT) + w * (kWave * IT);
+  uint32_t key[IT];
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    const int64_t pos = wbase + i * kWave + lane;
+    key[i] = pos < a.N ? a.keys[pos] : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < IT; ++i) hist_add(s_hist, (key[i] >> a.shift) & mask, wbase + i * kWave + lane < a.N, lane);
+  __syncthreads();
+  for (int d = tid; d < nd; d += kSortThreads) a.counts[(size_t)blockIdx.x * a.stride + d] = s_hist[d];
+}
+
+struct ColScanArgs {
+  uint32_t* counts;  // in: counts, out: exclusive prefixes over the tiles
+  uint32_t* totals;  // out: each digit's total
+  int32_t tiles, nd, stride;
+};
+
+// One block per kColDigits digits; thread (digit, chunk of consecutive
+// tiles): the chunk's counts are loaded kColBatch at a time, the chunk sums
+// scanned in LDS, and the chunk rewritten with running prefixes.
+constexpr int kColDigits = 16;
+constexpr int kColChunks = 32;
+constexpr int kColBatch = 16;
+__global__ __launch_bounds__(kColDigits * kColChunks) void k_column_scan(ColScanArgs a) {
+  __shared__ uint32_t s_cs[kColChunks][kColDigits];
+  const int tid = threadIdx.x, dl = tid % kColDigits, c = tid / kColDigits;
+  const int d = blockIdx.x * kColDigits + dl;
+  const int ct = (a.tiles + kColChunks - 1) / kColChunks;
+  const int t0 = min(a.tiles, c * ct), t1 = min(a.tiles, t0 + ct);
+  const bool ok = d < a.nd;
+  uint32_t sum = 0;
+  for (int tb = t0; tb < t1; tb += kColBatch) {
+    uint32_t v[kColBatch];
+#pragma unroll
+    for (int i = 0; i < kColBatch; ++i) v[i] = ok && tb + i < t1 ? a.counts[(size_t)(tb + i) * a.stride + d] : 0u;
+#pragma unroll
+    for (int i = 0; i < kColBatch; ++i) sum += v[i];
+  }
+  s_cs[c][dl] = sum;
+  __syncthreads();
+  uint32_t run = 0, total = 0;
+  for (int cc = 0; cc < kColChunks; ++cc) {
+    if (cc < c) run += s_cs[cc][dl];
+    total += s_cs[cc][dl];
+  }
+  if (ok && c == 0) a.totals[d] = total;
+  for (int tb = t0; tb < t1; tb += kColBatch) {
+    uint32_t v[kColBatch];
+#pragma unroll
+    for (int i = 0; i < kColBatch; ++i) v[i] = ok && tb + i < t1 ? a.counts[(size_t)(tb + i) * a.stride + d] : 0u;
+#pragma unroll
+    for (int i = 0; i < kColBatch; ++i) {
+      if (ok && tb + i < t1) {
+        a.counts[(size_t)(tb + i) * a.stride + d] = run;
+        run += v[i];
+      }
+    }
+  }
+}
+
 // ----------------------------------------------------------------- unique
 
 struct UniqArgs {
@@ -783,7 +788,6 @@ struct UniqArgs {
   int32_t* chunk_seg;  // [nchunks+1]: segment of position c*kChunk; [nchunks] = U
   uint64_t* status;    // [tiles], zeroed by k_prepare of the same call
   uint32_t* prev_totals;  // the last sort pass's totals, cleared here
-  int32_t last_pass;
   int32_t coresident;  // 1: tile = block index
   WsHeader* hdr;
 };
@@ -807,12 +811,11 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   } else if (tid == 0) {
     s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
   }
-  // the sort is complete: clear the last pass's totals and ticket and advance
-  // the generation that tags the next call's coordination words
+  // the sort is complete: clear the last pass's totals and advance the
+  // generation that tags the next call's coordination words
   if (blockIdx.x == 0) {
     for (int d = tid; d < kMaxDigits; d += kUniqThreads) a.prev_totals[d] = 0u;
     if (tid == 0) {
-      a.hdr->ticket[a.last_pass] = 0u;
       a.hdr->gen = a.hdr->gen + 1u;
     }
   }
@@ -1032,8 +1035,8 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   // Co-resident passes, when every tile of a pass and its prefix blocks fit
   // one block per compute unit (coresident_limit): tile = block index, bags
   // found by the first pass, two-level published-count prefix, with the
-  // smallest tiles that fit.  Otherwise a prepare kernel (bags, keys, digit
-  // totals), tickets and a look-back.
+  // smallest tiles that fit.  Otherwise a prepare kernel (bags, keys) and
+  // 4096-key tiles, each pass preceded by its tile counts and column scan.
   // A co-resident pass also runs its prefix blocks after the tiles: one per
   // group of kPrefixGroup tiles for the first pass, one per kRangeDigits
   // digits for the later ones (their digit totals are counted during the
@@ -1077,19 +1080,12 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     pa.ro = p.ro;
     pa.B = p.B;
     pa.M = p.M;
-    // about 4 * kPrepPositions positions per block: fewer global histogram atomics
+    // about 4 * kPrepPositions positions per block
     const int64_t want = (int64_t)4 * kPrepPositions * p.M / N;
     pa.bags_per_block = (int)(want < 1 ? 1 : (want > kPrepMaxBags ? kPrepMaxBags : want));
-    pa.npass = p.plan.passes;
-    pa.histograms = 1;
-    for (int i = 0; i < kMaxPasses; ++i) {
-      pa.shift[i] = p.plan.shift[i];
-      pa.bits[i] = p.plan.bits[i];
-    }
     // int32 ids of one table are the keys themselves; otherwise keys are built
     pa.keys_out = (p.T > 1 || p.idx64) ? keys_built : nullptr;
     pa.bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
-    pa.totals = reinterpret_cast<uint32_t*>(ws + L.totals);
     const int prep_blocks = p.M > 0 ? (p.M + pa.bags_per_block - 1) / pa.bags_per_block : 1;
     hipLaunchKernelGGL(k_prepare, dim3((unsigned)prep_blocks), dim3(kPrepThreads), 0, s, pa);
     e = hipGetLastError();
@@ -1145,6 +1141,30 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     xa.bits = p.plan.bits[ps];
     xa.pass = ps;
     xa.status_stride = status_stride;
+    if (!sort_cores) {
+      // reduce-then-scan: the tiles' digit counts, then their prefixes over
+      // the tiles and the digit totals
+      uint32_t* counts = reinterpret_cast<uint32_t*>(back + L.rows);
+      CountArgs ca{};
+      ca.keys = kin;
+      ca.N = N;
+      ca.shift = xa.shift;
+      ca.bits = xa.bits;
+      ca.stride = status_stride;
+      ca.counts = counts;
+      hipLaunchKernelGGL(k_tile_counts<kSortItemsWide>, dim3((unsigned)sort_tiles), dim3(kSortThreads), 0, s, ca);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      ColScanArgs sa{};
+      sa.counts = counts;
+      sa.totals = xa.totals;
+      sa.tiles = sort_tiles;
+      sa.nd = 1 << xa.bits;
+      sa.stride = status_stride;
+      hipLaunchKernelGGL(k_column_scan, dim3((unsigned)((sa.nd + kColDigits - 1) / kColDigits)),
+                         dim3(kColDigits * kColChunks), 0, s, sa);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      xa.prefix = counts;
+    }
     switch (sort_cores ? sort_it : kSortItemsWide) {
       case kSortItemsCore: e = launch_pass_bits<kSortItemsCore>(xa, sort_tiles + prefix_blocks(ps), s); break;
       case kSortItemsMid: e = launch_pass_bits<kSortItemsMid>(xa, sort_tiles + prefix_blocks(ps), s); break;
@@ -1168,7 +1188,6 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   ua.chunk_seg = reinterpret_cast<int32_t*>(ws + L.chunk_seg);
   ua.status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
   ua.prev_totals = reinterpret_cast<uint32_t*>(ws + L.totals) + (p.plan.passes - 1) * kMaxDigits;
-  ua.last_pass = p.plan.passes - 1;
   ua.coresident = uniq_cores;
   ua.hdr = hdr;
   hipLaunchKernelGGL(k_unique, dim3((unsigned)uniq_tiles), dim3(kUniqThreads), 0, s, ua);

@@ -13,13 +13,14 @@ namespace emb {
 constexpr int kWave = 64;
 
 // ---------------------------------------------------------------- dedup sort
-// LSD radix sort, one kernel per digit with a decoupled look-back over tiles.
+// LSD radix sort, one kernel per digit (co-resident tiles with prefix blocks,
+// or reduce-then-scan: tile counts and a column scan before each pass).
 constexpr int kMaxPasses = 4;
 constexpr int kMaxDigitBits = 10;
 constexpr int kMaxDigits = 1 << kMaxDigitBits;
 constexpr int kSortThreads = 512;
 // keys per thread: tiles of 2048 when every tile of a pass is resident at
-// once (more blocks, shorter ranking), 4096 otherwise (fewer look-back steps)
+// once (more blocks, shorter ranking), 4096 otherwise (fewer tiles per pass)
 constexpr int kSortItemsCore = 4;
 constexpr int kSortItemsMid = 5;
 constexpr int kSortItemsWide = 8;
@@ -30,8 +31,6 @@ constexpr int kUniqThreads = 256;
 constexpr int kUniqItems = 8;
 constexpr int kUniqTile = kUniqThreads * kUniqItems;
 
-// tile status words a look-back round loads together
-constexpr int kLookbackWindow = 8;
 // tiles per group of the two-level prefix used when all tiles are resident
 constexpr int kPrefixGroup = 16;
 // digit-range prefix blocks (passes after the first, co-resident): digits per
@@ -239,7 +238,6 @@ constexpr uint32_t kDedupErrors = 3u;
 // Site codes of the waits: (kernel << 8) | (sort pass << 4) | wait.
 enum WaitSite : uint32_t {
   kSiteTileOffsets = 0x100,  // co-resident tile: its final digit offsets
-  kSiteLookback = 0x101,     // windowed look-back tile: earlier tiles' counts
   kSiteGroupCounts = 0x102,  // first-pass prefix block: its group's counts
   kSiteGroupSums = 0x103,    // first-pass prefix block: every group's sum
   kSiteLaterCounts = 0x104,  // first-pass prefix block: later passes' counts

@@ -8,14 +8,14 @@ models of the phases and a small set of coefficients fitted (non-negative
 least squares) to measured phase times, `cost_table.json`.
 
   forward        t = a0 + a1 * N*rowbytes + a2 * U*rowbytes
-  dedup          t = b0 + b1 * passes + b2 * N (co-resident sort) + b3 * N (look-back sort)
+  dedup          t = b0 + b1 * passes + b2 * N (co-resident sort) + b3 * N (reduce-then-scan sort)
   reduce+update  t = c0 + c1 * N*D*4 + c2 * U*(2*rowbytes + 2*statebytes)
 
 N lookups, U distinct rows, rowbytes = D * (4 fp32 | 2 bf16), passes = the
 number of 10-bit radix passes for the table's key width, statebytes = 0
 (SGD), 4 (row-wise Adagrad) or 4*D (element-wise).  The co-resident sort
 holds every tile of a pass on the device at once (up to about a million
-keys); larger batches take the look-back sort.  Host logic only: nothing
+keys); larger batches take the reduce-then-scan sort.  Host logic only: nothing
 here runs on the device.
 """
 from __future__ import annotations

@@ -1080,8 +1080,8 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     pa.ro = p.ro;
     pa.B = p.B;
     pa.M = p.M;
-    // about 4 * kPrepPositions positions per block
-    const int64_t want = (int64_t)4 * kPrepPositions * p.M / N;
+    // about kPrepPositions positions per block
+    const int64_t want = (int64_t)kPrepPositions * p.M / N;
     pa.bags_per_block = (int)(want < 1 ? 1 : (want > kPrepMaxBags ? kPrepMaxBags : want));
     // int32 ids of one table are the keys themselves; otherwise keys are built
     pa.keys_out = (p.T > 1 || p.idx64) ? keys_built : nullptr;

@@ -788,6 +788,8 @@ struct UniqArgs {
   int32_t* chunk_seg;  // [nchunks+1]: segment of position c*kChunk; [nchunks] = U
   uint64_t* status;    // [tiles], zeroed by k_prepare of the same call
   uint32_t* prev_totals;  // the last sort pass's totals, cleared here
+  const uint64_t* prefix;  // reduce-then-scan: each tile's (heads, last head position + 1) over the
+                           // tiles before it, from k_uniq_counts and k_uniq_scan; null: look-back
   int32_t coresident;  // 1: tile = block index
   WsHeader* hdr;
 };
@@ -799,6 +801,90 @@ __device__ __forceinline__ uint64_t pack_uniq(uint64_t flag, uint32_t c, uint32_
 
 constexpr int kUniqWindows = 4;  // look-back words per lane and round
 
+// Reduce-then-scan unique (the tiles are not all resident at once): each
+// tile's number of heads and last head position + 1, then their exclusive
+// (sum, max) scan over the tiles by one block.
+struct UniqCountArgs {
+  const uint32_t* skeys;
+  int32_t N;
+  uint64_t* out;  // [tiles]: pack_uniq(0, heads, last head position + 1)
+};
+
+__global__ __launch_bounds__(kUniqThreads) void k_uniq_counts(UniqCountArgs a) {
+  constexpr int NW = kUniqThreads / kWave;
+  __shared__ uint32_t s_c[NW], s_q[NW];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  const int64_t tbase = (int64_t)blockIdx.x * kUniqTile;
+  uint32_t cur[kUniqItems], prv[kUniqItems];
+#pragma unroll
+  for (int i = 0; i < kUniqItems; ++i) {
+    const int64_t pos = tbase + tid + i * kUniqThreads;
+    cur[i] = pos < a.N ? a.skeys[pos] : 0u;
+    prv[i] = pos > 0 && pos < a.N ? a.skeys[pos - 1] : 0u;
+  }
+  uint32_t c = 0, q = 0;
+#pragma unroll
+  for (int i = 0; i < kUniqItems; ++i) {
+    const int64_t pos = tbase + tid + i * kUniqThreads;
+    if (pos < a.N && (pos == 0 || cur[i] != prv[i])) {
+      ++c;
+      q = max(q, (uint32_t)pos + 1u);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    c += __shfl_xor(c, o, kWave);
+    q = max(q, (uint32_t)__shfl_xor((int)q, o, kWave));
+  }
+  if (lane == 0) {
+    s_c[w] = c;
+    s_q[w] = q;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t tc = 0, tq = 0;
+    for (int ww = 0; ww < NW; ++ww) {
+      tc += s_c[ww];
+      tq = max(tq, s_q[ww]);
+    }
+    a.out[blockIdx.x] = pack_uniq(0, tc, tq);
+  }
+}
+
+constexpr int kUniqScanThreads = 1024;
+__global__ __launch_bounds__(kUniqScanThreads) void k_uniq_scan(uint64_t* words, int32_t tiles) {
+  constexpr int NW = kUniqScanThreads / kWave;
+  __shared__ uint32_t s_c[NW], s_q[NW];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  const int per = (tiles + kUniqScanThreads - 1) / kUniqScanThreads;
+  const int t0 = min(tiles, tid * per), t1 = min(tiles, t0 + per);
+  uint32_t c = 0, q = 0;
+  for (int t = t0; t < t1; ++t) {
+    const uint64_t v = words[t];
+    c += (uint32_t)(v >> 31) & 0x7fffffffu;
+    q = max(q, (uint32_t)v & 0x7fffffffu);
+  }
+  const uint32_t ci = wave_incl_sum(c), qi = wave_incl_max(q);
+  if (lane == kWave - 1) {
+    s_c[w] = ci;
+    s_q[w] = qi;
+  }
+  uint32_t qb = (uint32_t)__shfl_up((int)qi, 1, kWave);
+  if (lane == 0) qb = 0;
+  __syncthreads();
+  uint32_t rc = ci - c, rq = qb;
+  for (int ww = 0; ww < w; ++ww) {
+    rc += s_c[ww];
+    rq = max(rq, s_q[ww]);
+  }
+  for (int t = t0; t < t1; ++t) {
+    const uint64_t v = words[t];
+    words[t] = pack_uniq(0, rc, rq);
+    rc += (uint32_t)(v >> 31) & 0x7fffffffu;
+    rq = max(rq, (uint32_t)v & 0x7fffffffu);
+  }
+}
+
 __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   constexpr int NW = kUniqThreads / kWave;
   __shared__ uint32_t s_keys[kUniqTile];
@@ -806,7 +892,7 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   __shared__ uint32_t s_pc, s_pq, s_prev;
   __shared__ int s_tile;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  if (a.coresident) {
+  if (a.coresident || a.prefix) {
     if (tid == 0) s_tile = blockIdx.x;
   } else if (tid == 0) {
     s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
@@ -868,7 +954,13 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     tile_c += s_wc[ww];
     tile_q = max(tile_q, s_wq[ww]);
   }
-  if (w == 0) {
+  if (a.prefix) {
+    if (tid == 0) {
+      const uint64_t v = a.prefix[tile];
+      s_pc = (uint32_t)(v >> 31) & 0x7fffffffu;
+      s_pq = (uint32_t)v & 0x7fffffffu;
+    }
+  } else if (w == 0) {
     // wave-parallel look-back: in a round, lane k reads the status of tiles
     // j - k - 64 i for i < kUniqWindows (one round trip for all of them); the
     // windows are then taken in order up to the first word not yet published
@@ -1189,6 +1281,18 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   ua.status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
   ua.prev_totals = reinterpret_cast<uint32_t*>(ws + L.totals) + (p.plan.passes - 1) * kMaxDigits;
   ua.coresident = uniq_cores;
+  if (!uniq_cores) {
+    // reduce-then-scan: tile head counts, then their scan over the tiles
+    UniqCountArgs uc{};
+    uc.skeys = kin;
+    uc.N = N;
+    uc.out = ua.status;
+    hipLaunchKernelGGL(k_uniq_counts, dim3((unsigned)uniq_tiles), dim3(kUniqThreads), 0, s, uc);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_uniq_scan, dim3(1), dim3(kUniqScanThreads), 0, s, ua.status, uniq_tiles);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    ua.prefix = ua.status;
+  }
   ua.hdr = hdr;
   hipLaunchKernelGGL(k_unique, dim3((unsigned)uniq_tiles), dim3(kUniqThreads), 0, s, ua);
   return hipGetLastError();

@@ -22,7 +22,9 @@
 //     position order, so every pass is stable and so is the whole sort.
 //  2. k_unique: head flags key[k] != key[k-1], a block scan plus a look-back
 //     of (number of heads, last head position) gives every head its segment
-//     index and the length of the previous segment.
+//     index and the length of the previous segment; when its tiles are not
+//     all resident at once, k_uniq_counts and k_uniq_scan compute each
+//     tile's (heads, last head) prefix first instead of the look-back.
 #include "emb_common.h"
 #include "kernels.h"
 

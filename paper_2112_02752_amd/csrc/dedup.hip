@@ -512,7 +512,6 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
     // the unique scan of this call starts from cleared look-back words
     for (int i = blockIdx.x * kSortThreads + tid; i < a.uniq_tiles; i += a.ntiles * kSortThreads)
       a.uniq_status[i] = 0;
-    if (blockIdx.x == 0 && tid == 0) a.hdr->ticket[kSlotUnique] = 0u;
   }
   // The tile's digit counts are published as soon as its digits are known
   // (from an LDS histogram), so that the other tiles' prefixes advance while
@@ -792,7 +791,6 @@ struct UniqArgs {
   uint32_t* prev_totals;  // the last sort pass's totals, cleared here
   const uint64_t* prefix;  // reduce-then-scan: each tile's (heads, last head position + 1) over the
                            // tiles before it, from k_uniq_counts and k_uniq_scan; null: look-back
-  int32_t coresident;  // 1: tile = block index
   WsHeader* hdr;
 };
 
@@ -892,13 +890,7 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   __shared__ uint32_t s_keys[kUniqTile];
   __shared__ uint32_t s_wc[NW], s_wq[NW];
   __shared__ uint32_t s_pc, s_pq, s_prev;
-  __shared__ int s_tile;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  if (a.coresident || a.prefix) {
-    if (tid == 0) s_tile = blockIdx.x;
-  } else if (tid == 0) {
-    s_tile = (int)atomic_add_u32(&a.hdr->ticket[kSlotUnique], 1u);
-  }
   // the sort is complete: clear the last pass's totals and advance the
   // generation that tags the next call's coordination words
   if (blockIdx.x == 0) {
@@ -908,7 +900,7 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     }
   }
   __syncthreads();
-  const int tile = s_tile;
+  const int tile = blockIdx.x;
   const int64_t tbase = (int64_t)tile * kUniqTile;
   // every load of the tile is issued before the first LDS store
   uint32_t kv[kUniqItems];
@@ -1282,7 +1274,6 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   ua.chunk_seg = reinterpret_cast<int32_t*>(ws + L.chunk_seg);
   ua.status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
   ua.prev_totals = reinterpret_cast<uint32_t*>(ws + L.totals) + (p.plan.passes - 1) * kMaxDigits;
-  ua.coresident = uniq_cores;
   if (!uniq_cores) {
     // reduce-then-scan: tile head counts, then their scan over the tiles
     UniqCountArgs uc{};

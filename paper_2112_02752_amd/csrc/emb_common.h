@@ -58,16 +58,12 @@ constexpr int kTinySeg = 16;
 constexpr int kCombineThreads = 1024;
 constexpr int kCombineChunks = 64;
 
-// ticket / done counter slots in the workspace header
-constexpr int kSlotUnique = kMaxPasses;
-
 // Workspace header (device).  gen counts emb_unique_ids calls; it tags the
-// sort's published counts so they never need clearing.  A tile ticket is
-// cleared by the kernel that runs after the one that used it.
+// sort's published counts so they never need clearing.
 struct WsHeader {
   uint32_t gen;
   uint32_t error;
-  uint32_t ticket[8];
+  uint32_t reserved[8];
   // first wait that ran out: its site code, block index and the number of
   // waits that ran out in all (kept until the workspace is initialised again)
   uint32_t timeout_site, timeout_block, timeouts;

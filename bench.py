@@ -7,13 +7,18 @@ upstream gradients) are resident in HBM before the timed region starts.
 
 Prints ONE JSON line.  `value` is pooled lookups per second of the K timed
 steps, run back to back (wall clock; `step_us.timed_region_gpu_per_step` is
-one HIP event pair around all of them on the launch stream).  The same
-batches then run again with an event pair around each step (`step_us`:
-median, p10, p90) and with events between the phases: `roofline` prices the
-phase that takes the most time against HBM bandwidth and `phases` lists all
-three; `cold` repeats them after flushing
-the caches.  `cpu_baseline` is the CPU oracle timed on this host's cores on a
-bounded sample of the same workload.
+one HIP event pair around all of them on the launch stream).  The default
+schedule is pipelined: the dedups of the next group of batches run on a side
+stream while the main stream runs the forward and update of the current
+group (results identical to serial steps bit for bit).  After the timed
+region the workspaces' status is read: a step that failed on the device
+ends the run with exit status 3.  The same batches then run again as serial
+steps with an event pair around each step (`step_us`: median, p10, p90) and
+with events between the phases: `roofline` prices the phase that takes the
+most time against HBM bandwidth and `phases` lists all three; `cold` repeats
+them after flushing the caches.  `cpu_baseline` is the CPU oracle timed on
+this host on a bounded sample of the same workload, on all its cores and on
+one.
 """
 from __future__ import annotations
 
@@ -48,12 +53,13 @@ def parse():
     ap.add_argument("--bags", type=int, default=None, help="bags per table instead of the workload's own")
     ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
                     help="optimizer instead of the workload's own (adagrad_ew: element-wise, state [R][D])")
-    ap.add_argument("--schedule", choices=("auto", "serial", "concurrent", "pipelined"), default="auto",
-                    help="concurrent: the forward of a batch runs on a side stream at the same time as its id "
-                         "dedup; serial: forward, dedup, reduce + update one after another on one stream; "
-                         "auto: concurrent for batches of at least a million lookups, else serial; "
-                         "pipelined (switched off): the dedup of batch k+1 alongside the forward and update of "
-                         "batch k")
+    ap.add_argument("--schedule", choices=("pipelined", "auto", "serial", "concurrent"), default="pipelined",
+                    help="pipelined: the dedups of the next group of batches on a side stream while the main "
+                         "stream runs the forward and update of the current group; concurrent: the forward of a "
+                         "batch on a side stream at the same time as its id dedup; serial: forward, dedup, "
+                         "reduce + update one after another on one stream; auto: concurrent for batches of at "
+                         "least a million lookups, else serial")
+    ap.add_argument("--group", type=int, default=4, help="batches per group of the pipelined schedule")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
@@ -123,14 +129,13 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 3}), flush=True)
 
 
-def cpu_baseline(w, batches, budget_s: float):
-    """The oracle, untuned, single-threaded, on whole steps of the same workload:
-    the benchmark's batches, then further seeded batches of the same workload
-    until about `budget_s` seconds of oracle time."""
+def _oracle_rate(w, batches, budget_s: float):
+    """Oracle whole steps on the benchmark's batches, then further seeded
+    batches of the same workload, until about `budget_s` seconds of oracle
+    time: (lookups per second, steps, lookups, seconds)."""
     import oracle
     import synth
-    done_n, elapsed, steps = 0, 0.0, 0
-    s = 0
+    done_n, elapsed, steps, s = 0, 0.0, 0, 0
     while elapsed < budget_s and s < 400:
         b = batches[s] if s < len(batches) else synth.make_batch(w, s)
         keys = np.unique(global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices))
@@ -143,11 +148,31 @@ def cpu_baseline(w, batches, budget_s: float):
         done_n += len(b.indices)
         steps += 1
         s += 1
-    return {"value": done_n / elapsed, "unit": "lookups/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} whole steps of {w.name} (fwd+dedup+reduce+update; rows the batch touches "
-                      f"regenerated from the seed, untimed), {done_n} lookups, {elapsed:.1f} s of oracle time, "
-                      f"single thread",
-            "host": {"cpu_model": host_cpu_model(), "nproc": os.cpu_count()}}
+    return done_n / elapsed, steps, done_n, elapsed
+
+
+def cpu_baseline(w, batches, budget_s: float):
+    """The oracle, untuned, on whole steps of the same workload: on all the
+    host's cores (its loops over bags and segments in parallel, the sort on
+    one thread; the results do not depend on the thread count), then on one."""
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    what = (f"whole steps of {w.name} (fwd+dedup+reduce+update; the rows a batch touches regenerated from the "
+            f"seed, untimed)")
+    try:
+        oracle.set_threads(threads)
+        used = oracle.get_threads()
+        rate, steps, n, t = _oracle_rate(w, batches, budget_s)
+        oracle.set_threads(1)
+        rate1, steps1, n1, t1 = _oracle_rate(w, batches, budget_s)
+    finally:
+        oracle.set_threads(0)
+    return {"value": rate, "unit": "lookups/s", "cores": used, "kind": "oracle",
+            "sample": f"{steps} {what}, {n} lookups, {t:.1f} s of oracle time on {used} threads",
+            "single_thread": {"value": rate1, "unit": "lookups/s", "cores": 1,
+                              "sample": f"{steps1} {what}, {n1} lookups, {t1:.1f} s of oracle time"},
+            "host": {"cpu_model": host_cpu_model(), "nproc": os.cpu_count(),
+                     "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}}
 
 
 def host_cpu_model() -> str:
@@ -196,10 +221,6 @@ def main():
         import dataclasses
         w = dataclasses.replace(w, bags_per_table=args.bags, name=f"{w.name}-b{args.bags}",
                                 description=f"{w.description}; {args.bags} bags per table instead")
-    if args.schedule == "pipelined":
-        print("bench.py: the pipelined schedule is switched off (two co-resident dedups in flight together can "
-              "wait on each other's blocks); use --schedule serial", file=sys.stderr)
-        sys.exit(2)
     dev = "cuda"
     total = args.warmup + args.steps
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
@@ -244,19 +265,40 @@ def main():
         if ev:
             ev[3].record(stream)
 
+    clayer = pipe = None
     if args.schedule in ("concurrent", "auto"):
         clayer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
                            concurrent=True if args.schedule == "concurrent" else "auto")
 
-        def run_step(i):
-            clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
-    else:
-        def run_step(i):
-            layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
+        def run_steps(lo, hi):
+            for i in range(lo, hi):
+                clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
+    elif args.schedule == "pipelined":
+        pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
+                            group=args.group)
 
-    for i in range(args.warmup):
-        run_step(i)
+        def run_steps(lo, hi):
+            pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in range(lo, hi)], sp)
+    else:
+        def run_steps(lo, hi):
+            for i in range(lo, hi):
+                layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
+
+    def check_status(where):
+        """A step that failed on the device (a bounded wait of its dedup ran
+        out) wrote no table row: its time would not be a step's, so the run
+        ends here with the reason."""
+        try:
+            for obj in (layer, clayer, pipe):
+                if obj is not None:
+                    obj.check(sp)
+        except emb.StepFailed as e:
+            print(f"bench.py: {where}: {e}", file=sys.stderr, flush=True)
+            sys.exit(3)
+
+    run_steps(0, args.warmup)
     torch.cuda.synchronize()
+    check_status("warm-up")
 
     # timed region: K whole steps back to back, one fresh batch each, one HIP
     # event pair around all of them on the launch stream
@@ -264,20 +306,20 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     e_all[0].record(stream)
-    for i in range(args.warmup, total):
-        run_step(i)
+    run_steps(args.warmup, total)
     e_all[1].record(stream)
     t_enq = time.perf_counter() - t_start
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     gpu_all_s = e_all[0].elapsed_time(e_all[1]) * 1e-3
+    check_status("timed region")
 
-    # the same batches again with an event pair around each step: the
-    # distribution of step times
+    # the same batches again as serial steps with an event pair around each
+    # step: the distribution of serial step times
     sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     for k, i in enumerate(range(args.warmup, total)):
         sev[k][0].record(stream)
-        run_step(i)
+        layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
         sev[k][1].record(stream)
     torch.cuda.synchronize()
     step_s = [e[0].elapsed_time(e[1]) * 1e-3 for e in sev]
@@ -389,6 +431,7 @@ def main():
         except RuntimeError as e:  # reported, not fatal: the headline does not depend on it
             graph = {"error": str(e)[:200]}
 
+    check_status("after the serial, phase-timed and cold steps")
     n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
 
     # unique counts of the timed batches (for the byte models)
@@ -425,9 +468,10 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
                    "table_bytes": w.weight_bytes, "schedule": args.schedule,
-                   "overlapped_steps": sum(1 for i in range(args.warmup, total)
-                                           if args.schedule in ("concurrent", "auto")
-                                           and clayer.overlaps(dev_batches[i][2]))},
+                   "group": args.group if args.schedule == "pipelined" else None,
+                   "overlapped_steps": args.steps if args.schedule == "pipelined" else
+                   sum(1 for i in range(args.warmup, total)
+                       if clayer is not None and clayer.overlaps(dev_batches[i][2]))},
         "roofline": {"bound": "hbm", "phase": dom, "kernel": d["kernels"], "model": "logical",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": d["hbm_traffic_bytes"], "bytes_per_launch": d["logical_bytes"],
@@ -438,6 +482,8 @@ def main():
                        "compulsory_GBs": step_comp / (ms * 1e-3) / 1e9,
                        "logical_frac": step_log / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
         "step_us": {"schedule": args.schedule, "timed_region_gpu_per_step": gpu_all_s / args.steps * 1e6,
+                    "serial_note": "mean / median / p10 / p90: serial steps of the same batches, one event pair "
+                                   "around each",
                     "mean": gpu_step_s * 1e6,
                     "median": float(np.median(step_s)) * 1e6,
                     "p10": float(np.percentile(step_s, 10)) * 1e6,

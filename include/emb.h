@@ -200,18 +200,40 @@ emb_status emb_route_ids(const emb_tables* tables, const emb_batch* batch, int32
  * 8 (an id out of range of its table). */
 emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, int32_t* flag, void* stream);
 
-/* Device-side error word of a workspace (host-readable after a copy): bit 0 is
- * set if a wait for a word another workgroup publishes ran out (every such
- * wait is bounded to 20 ms, far beyond any wait of a healthy call), bit 1 if
- * a sort pass found digit totals inconsistent with its keys (a workspace that
- * was not initialised), bit 2 if a wait of the gradient combine ran out.  The
- * results of that call are then undefined, but every write stays inside the
- * caller's buffers: while bit 0 or 1 is set, emb_grad_reduce with this
- * workspace forms no gradient row and writes no table row, and
- * emb_sparse_update skips keys >= R.  The word stays set until the workspace
- * is initialised again.  The three 32-bit words after it record the first
- * wait that ran out (a site code, its block index) and how many ran out.
- * Offset in bytes from the workspace base. */
+/* Failures a kernel finds on the device are recorded per call in the
+ * workspace.  Every wait of a workgroup for a word another workgroup
+ * publishes is bounded to 20 ms, far beyond any wait of a healthy call.  A
+ * wait that runs out makes the call fail: its waits all give up within
+ * microseconds, every write stays inside the caller's buffers, its
+ * emb_unique_ids outputs are undefined except num_unique[0] = 0 when the sort
+ * failed, and the emb_grad_reduce that follows it writes no table or state
+ * row (unfused, it writes zero gradient rows, so an emb_sparse_update of
+ * them leaves every row as it is for SGD and for Adagrad with eps > 0).  The
+ * next emb_unique_ids on the workspace starts afresh.
+ *
+ * emb_workspace_status enqueues on stream a kernel that writes the status of
+ * the last emb_unique_ids call on ws, and of the emb_grad_reduce that
+ * followed it, to status (device int32 [4]):
+ *   status[0]  error bits of that call, 0 if it completed normally:
+ *              1 a wait of the dedup ran out, 2 a sort pass found digit
+ *              totals inconsistent with its keys (a workspace that was not
+ *              initialised), 4 a wait of the gradient combine ran out
+ *   status[1]  site code of the first wait that ran out since the workspace
+ *              was initialised (0: none): 0x1p0 / 0x1p2-0x1p5 a sort pass
+ *              (pass p), 0x200 the unique scan, 0x300 the gradient combine
+ *   status[2]  the workgroup of that wait
+ *   status[3]  number of waits that ran out since the workspace was
+ *              initialised
+ * emb_workspace_init clears everything.  Returns EMB_EWORKSPACE if ws is
+ * misaligned or ws_bytes is smaller than a workspace header (256 bytes). */
+emb_status emb_workspace_status(const void* ws, size_t ws_bytes, int32_t* status, void* stream);
+
+/* Layout of the workspace header, for callers that read or set it directly:
+ * the uint32 at offset 0 is the generation g of the last dedup call (the
+ * next call has generation g + 1, or 1 after 0xffffffff), and the uint64 at
+ * the offset returned here holds (generation << 32) | error bits of the last
+ * call that set any; its bits belong to a call only while its generation is
+ * that call's. */
 size_t emb_workspace_error_offset(void);
 
 const char* emb_status_string(int32_t status);

@@ -1,8 +1,9 @@
 """ORACLE -- test infrastructure only.
 
-Python wrapper over ``oracle.c``: a plain single-threaded CPU statement of
-one step of the pooled sparse embedding layer (forward, dedup, gradient
-reduce, optimizer step), accumulated in double.  Only ``tests/``, the smoke
+Python wrapper over ``oracle.c``: a plain CPU statement of one step of the
+pooled sparse embedding layer (forward, dedup, gradient reduce, optimizer
+step), accumulated in double; its bag and segment loops may run on several
+threads with results that do not depend on the thread count.  Only ``tests/``, the smoke
 check and the benchmark's CPU-baseline leg may import this package; the
 product library never does.  It shares no code with the HIP path.
 
@@ -30,7 +31,7 @@ DTYPE = {"fp32": 0, "bf16": 1}
 
 def build() -> None:
     src = os.path.join(_HERE, "oracle.c")
-    subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-ffp-contract=off", "-std=c11",
+    subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-std=c11",
                            src, "-o", _SO + ".tmp", "-lm"])
     os.replace(_SO + ".tmp", _SO)
 
@@ -60,8 +61,22 @@ def _lib():
         L.oracle_sr_bits.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         L.oracle_bf16_stochastic.restype = ctypes.c_uint16
         L.oracle_bf16_stochastic.argtypes = [f32, ctypes.c_uint32]
+        L.oracle_set_threads.restype = None
+        L.oracle_set_threads.argtypes = [i32]
+        L.oracle_get_threads.restype = i32
+        L.oracle_get_threads.argtypes = []
         _L = L
     return _L
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (n < 1: one per processor).
+    Results do not depend on it: every output is computed by one thread."""
+    _lib().oracle_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(_lib().oracle_get_threads())
 
 
 class OracleError(RuntimeError):

@@ -1,7 +1,7 @@
 /*
  * ORACLE -- test infrastructure only.
  *
- * A plain, slow, single-threaded CPU statement of one training step of a
+ * A plain, slow CPU statement of one training step of a
  * pooled sparse embedding layer: the layer the paper's introduction names as
  * the part of a recommendation model that turns massive high-dimensional
  * sparse ids into dense features at a high data-access cost (Introduction;
@@ -19,7 +19,11 @@
  * it is the plain definition: a stable ascending sort by key, then the runs
  * of equal keys.
  *
- * Accumulation is in double, with one rounding at each output.  Only the
+ * Accumulation is in double, with one rounding at each output.  The loops
+ * over bags (forward) and over segments and rows (reduce, optimizer) may run
+ * on several threads (OpenMP, oracle_set_threads); every output is computed
+ * by one thread in the same order whatever the thread count, so the results
+ * do not depend on it.  The sort is single-threaded.  Only the
  * tests, the smoke check and the CPU-baseline leg of the benchmark load this
  * file; the product library never links or calls it.
  *
@@ -31,11 +35,16 @@
  * step-1 validation below).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 enum { ORC_OK = 0, ORC_BAD_OFFSETS = -1, ORC_BAD_ID = -2, ORC_MISSING_ROW = -3, ORC_BAD_ARG = -4, ORC_NOMEM = -5 };
+
+/* Threads of the parallel loops (n < 1: the OpenMP default); the number in use. */
+void oracle_set_threads(int32_t n) { omp_set_num_threads(n > 0 ? n : omp_get_num_procs()); }
+int32_t oracle_get_threads(void) { return omp_get_max_threads(); }
 
 /* ------------------------------------------------------------ row store */
 
@@ -142,26 +151,44 @@ int oracle_pool_fwd(int32_t T, const int64_t* row_offset, int32_t B, const int32
   int rc = validate(T, row_offset, B, offsets, idx);
   if (rc) return rc;
   store_t s = {store_n, store_keys, D, dtype};
-  double* acc = (double*)malloc(sizeof(double) * (size_t)D);
-  if (!acc) return ORC_NOMEM;
   int64_t M = (int64_t)T * B;
-  for (int64_t m = 0; m < M; ++m) {
-    int64_t t = m / B;
-    for (int32_t d = 0; d < D; ++d) acc[d] = 0.0;
-    for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {
-      int64_t slot = store_slot(&s, (uint32_t)(row_offset[t] + idx[j]));
-      if (slot < 0) { free(acc); return ORC_MISSING_ROW; }
-      for (int32_t d = 0; d < D; ++d) acc[d] += store_get(&s, store_vals, slot, d);
+  int err = ORC_OK;
+#pragma omp parallel
+  {
+    double* acc = (double*)malloc(sizeof(double) * (size_t)D);
+    if (!acc) {
+#pragma omp atomic write
+      err = ORC_NOMEM;
     }
-    int32_t L = offsets[m + 1] - offsets[m];
-    for (int32_t d = 0; d < D; ++d) {
-      double v = acc[d];
-      if (pool == 1 && L > 0) v = v / (double)L;
-      out[m * D + d] = (float)v;
+#pragma omp for schedule(static)
+    for (int64_t m = 0; m < M; ++m) {
+      if (!acc) continue;
+      int64_t t = m / B;
+      for (int32_t d = 0; d < D; ++d) acc[d] = 0.0;
+      int missing = 0;
+      for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {
+        int64_t slot = store_slot(&s, (uint32_t)(row_offset[t] + idx[j]));
+        if (slot < 0) {
+          missing = 1;
+          break;
+        }
+        for (int32_t d = 0; d < D; ++d) acc[d] += store_get(&s, store_vals, slot, d);
+      }
+      if (missing) {
+#pragma omp atomic write
+        err = ORC_MISSING_ROW;
+        continue;
+      }
+      int32_t L = offsets[m + 1] - offsets[m];
+      for (int32_t d = 0; d < D; ++d) {
+        double v = acc[d];
+        if (pool == 1 && L > 0) v = v / (double)L;
+        out[m * D + d] = (float)v;
+      }
     }
+    free(acc);
   }
-  free(acc);
-  return ORC_OK;
+  return err;
 }
 
 /* --------------------------------------------------------------- dedup */
@@ -192,6 +219,7 @@ int oracle_unique_ids(int32_t T, const int64_t* row_offset, int32_t B, const int
   int64_t N = offsets[M];
   kp_t* a = (kp_t*)malloc(sizeof(kp_t) * (size_t)(N > 0 ? N : 1));
   if (!a) return ORC_NOMEM;
+#pragma omp parallel for schedule(static)
   for (int64_t m = 0; m < M; ++m)
     for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {
       a[j].key = (uint32_t)(row_offset[m / B] + idx[j]);
@@ -226,26 +254,37 @@ int oracle_grad_reduce(int32_t T, int32_t B, const int32_t* offsets, int32_t D, 
   int64_t M = (int64_t)T * B;
   int64_t N = offsets[M];
   int32_t* bag = (int32_t*)malloc(sizeof(int32_t) * (size_t)(N > 0 ? N : 1));
-  double* sum = (double*)malloc(sizeof(double) * (size_t)D);
-  if (!bag || !sum) { free(bag); free(sum); return ORC_NOMEM; }
+  if (!bag) return ORC_NOMEM;
+#pragma omp parallel for schedule(static)
   for (int64_t m = 0; m < M; ++m)
     for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) bag[j] = (int32_t)m;
-  for (int32_t u = 0; u < U; ++u) {
-    for (int32_t d = 0; d < D; ++d) sum[d] = 0.0;
-    for (int32_t k = seg_offsets[u]; k < seg_offsets[u + 1]; ++k) {
-      int32_t m = bag[perm[k]];
-      int32_t L = offsets[m + 1] - offsets[m];
-      double scale = pool == 1 ? 1.0 / (double)L : 1.0;
-      for (int32_t d = 0; d < D; ++d) sum[d] += scale * (double)G[(int64_t)m * D + d];
+  int err = ORC_OK;
+#pragma omp parallel
+  {
+    double* sum = (double*)malloc(sizeof(double) * (size_t)D);
+    if (!sum) {
+#pragma omp atomic write
+      err = ORC_NOMEM;
     }
-    for (int32_t d = 0; d < D; ++d) {
-      if (grad_rows) grad_rows[(int64_t)u * D + d] = (float)sum[d];
-      if (acc) acc[(int64_t)u * D + d] = sum[d];
+#pragma omp for schedule(dynamic, 64)
+    for (int32_t u = 0; u < U; ++u) {
+      if (!sum) continue;
+      for (int32_t d = 0; d < D; ++d) sum[d] = 0.0;
+      for (int32_t k = seg_offsets[u]; k < seg_offsets[u + 1]; ++k) {
+        int32_t m = bag[perm[k]];
+        int32_t L = offsets[m + 1] - offsets[m];
+        double scale = pool == 1 ? 1.0 / (double)L : 1.0;
+        for (int32_t d = 0; d < D; ++d) sum[d] += scale * (double)G[(int64_t)m * D + d];
+      }
+      for (int32_t d = 0; d < D; ++d) {
+        if (grad_rows) grad_rows[(int64_t)u * D + d] = (float)sum[d];
+        if (acc) acc[(int64_t)u * D + d] = sum[d];
+      }
     }
+    free(sum);
   }
   free(bag);
-  free(sum);
-  return ORC_OK;
+  return err;
 }
 
 /* ------------------------------------------------------------ optimizer */
@@ -268,9 +307,15 @@ int oracle_sparse_update(int32_t opt, float lr, float eps, int32_t D, int32_t dt
   if (opt < 0 || opt > 2 || D < 1 || U < 0 || rounding < 0 || rounding > 1) return ORC_BAD_ARG;
   if (opt != 0 && state == NULL) return ORC_BAD_ARG;
   store_t s = {store_n, store_keys, D, dtype};
+  for (int32_t u = 0; u < U; ++u)
+    if (store_slot(&s, unique_keys[u]) < 0) return ORC_MISSING_ROW;
+  /* distinct keys (strictly ascending, as a dedup gives them) touch distinct
+   * rows, so their rows may be updated on several threads; otherwise in order */
+  int distinct = 1;
+  for (int32_t u = 1; u < U && distinct; ++u) distinct = unique_keys[u] > unique_keys[u - 1];
+#pragma omp parallel for schedule(static) if (distinct)
   for (int32_t u = 0; u < U; ++u) {
     int64_t slot = store_slot(&s, unique_keys[u]);
-    if (slot < 0) return ORC_MISSING_ROW;
     const double* g = grad + (int64_t)u * D;
     double denom = 1.0;
     if (opt == 1) {

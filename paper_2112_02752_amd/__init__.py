@@ -26,14 +26,42 @@ OPT = {"sgd": 0, "adagrad": 1, "adagrad_ew": 2}
 DTYPE = {"fp32": FP32, "bf16": BF16}
 
 EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_grad_reduce",
-            "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_status_string",
-            "emb_route_workspace_size", "emb_route_ids")
+            "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_workspace_status",
+            "emb_status_string", "emb_route_workspace_size", "emb_route_ids")
 
 
 class EmbError(RuntimeError):
     def __init__(self, fn: str, status: int):
         self.status = status
         super().__init__(f"{fn}: {_status_string(status)} (status {status})")
+
+
+class StepFailed(RuntimeError):
+    """A dedup (and the reduce after it) failed on the device: one of its
+    bounded waits for a word another workgroup publishes ran out, or a sort
+    pass found inconsistent digit totals.  No table or state row was written
+    by that step."""
+
+    SITES = {0x100: "sort pass {p}: tile waiting for its digit offsets",
+             0x102: "sort pass {p}: prefix block waiting for its group's counts",
+             0x103: "sort pass {p}: prefix block waiting for the group sums",
+             0x104: "sort pass {p}: prefix block waiting for the later passes' counts",
+             0x105: "sort pass {p}: range block waiting for its tiles' counts",
+             0x200: "unique scan look-back", 0x300: "gradient combine"}
+
+    def __init__(self, bits: int, site: int, block: int, timeouts: int):
+        self.bits, self.site, self.block, self.timeouts = bits, site, block, timeouts
+        what = []
+        if bits & 1:
+            what.append("a dedup wait ran out")
+        if bits & 2:
+            what.append("a sort pass found digit totals inconsistent with its keys (workspace not initialised?)")
+        if bits & 4:
+            what.append("a gradient-combine wait ran out")
+        desc = self.SITES.get(site & ~0xf0, "none").format(p=(site >> 4) & 0xf) if site else "none"
+        super().__init__(f"embedding step failed on the device: {'; '.join(what)} (error bits {bits}); first wait "
+                         f"that ran out since the workspace was initialised: {desc}, workgroup {block}; "
+                         f"{timeouts} waits ran out in all")
 
 
 class CTables(ctypes.Structure):
@@ -87,6 +115,8 @@ def lib():
         L.emb_validate_batch.argtypes = [T, B, vp, vp]
         L.emb_workspace_error_offset.restype = sz
         L.emb_workspace_error_offset.argtypes = []
+        L.emb_workspace_status.restype = i32
+        L.emb_workspace_status.argtypes = [vp, sz, vp, vp]
         L.emb_status_string.restype = ctypes.c_char_p
         L.emb_status_string.argtypes = [i32]
         _lib = L
@@ -223,6 +253,22 @@ def workspace_error_offset() -> int:
     return int(lib().emb_workspace_error_offset())
 
 
+def workspace_status(ws, status, stream=None) -> None:
+    """Enqueue the write of the workspace's last-call status to ``status``
+    (device int32 [4]): error bits, first timed-out wait's site, its
+    workgroup, waits that ran out since the workspace was initialised."""
+    _check("emb_workspace_status", lib().emb_workspace_status(_ptr(ws), ws.numel() * ws.element_size(),
+                                                              _ptr(status), _stream(stream)))
+
+
+def read_status(ws, stream=None):
+    """The workspace's last-call status as host ints (synchronises)."""
+    import torch
+    st = torch.zeros(4, dtype=torch.int32, device=ws.device)
+    workspace_status(ws, st, stream)
+    return tuple(int(x) for x in st.cpu())
+
+
 class Layer:
     """One GPU's shard of the layer with its buffers: forward, then the
     backward (dedup, segment-reduce, fused optimizer step) of the same batch.
@@ -267,6 +313,7 @@ class Layer:
         self.seg_offsets = torch.empty(n + 1, **i32)
         self.sort_perm = torch.empty(n, **i32)
         self.num_unique = torch.zeros(1, **i32)
+        self._status = torch.zeros(4, **i32)
         self.max_indices = n
         self.concurrent = concurrent
         self._events = False
@@ -293,6 +340,20 @@ class Layer:
                 L.hipEventDestroy(self._ev_fwd)
             except Exception:
                 pass
+
+    def status(self, stream=None):
+        """Status of the last step (emb_workspace_status): (error bits,
+        first timed-out wait's site, its workgroup, waits that ran out since
+        the workspace was initialised); synchronises."""
+        workspace_status(self.ws, self._status, stream)
+        return tuple(int(x) for x in self._status.cpu())
+
+    def check(self, stream=None) -> None:
+        """Raise StepFailed if the last step failed on the device (it then
+        wrote no table or state row)."""
+        st = self.status(stream)
+        if st[0]:
+            raise StepFailed(*st)
 
     def forward(self, batch: Batch, out, stream=None) -> None:
         pool_fwd(self.tables, batch, self.pool, out, stream)
@@ -417,54 +478,49 @@ class _Hip:
             raise RuntimeError(f"hipStreamWaitEvent: {rc}")
 
 
-# The pipelined schedule stays off until the cause of the GPU memory faults
-# seen with it is found (it is kept, unused, for that work).
-PIPELINE_ENABLED = False
-
-
 class Pipeline:
-    """Training steps of the layer with the id dedup of later batches
-    overlapped with the forward and update of the current one.
+    """Training steps of the layer with the id dedups of the next group of
+    batches running on a side stream while the main stream runs the forward
+    and the fused update of the current group.
 
-    The dedup of a batch reads only its ids, never the table, so it can run
-    ahead: the dedups of the next `lookahead` batches run on their own side
-    streams while the main stream runs forward k then the update of k, so the
-    forward of batch k+1 still follows the update of batch k and every step
-    sees exactly the weights a serial execution would.  lookahead + 2 dedup
-    buffer sets rotate; a set is reused only after the update that read it has
-    completed (events)."""
+    The dedup reads only a batch's ids and offsets, never the table, so
+    running it ahead changes no result: every forward still follows the
+    previous update on the main stream, and tables, state and pooled outputs
+    equal those of serial steps bit for bit.  The dedups are serialised on
+    the side stream, so at most one runs at a time, next to forward and
+    reduce kernels that never wait for other workgroups: every workgroup of a
+    sort pass is dispatched once the main stream's workgroups retire, which
+    they do without waiting on the dedup.  Two sets of ``group`` dedup
+    buffers alternate; the side stream overwrites a set only after the main
+    stream's group that read it, so each direction takes one cross-stream
+    wait per group (each costs the host 15-25 us on ROCm when the event is
+    still pending, hence groups rather than single steps).
+
+    This is the paper's embedding stage run ahead of the dense stage
+    (Section "Multi-mode Execution", heterogeneous pipeline) with no
+    staleness: only the dedup, which the table never feeds, runs early."""
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0, lookahead: int = 2):
-        if not PIPELINE_ENABLED:
-            raise RuntimeError("the pipelined schedule is switched off: runs of it on MI355X ended in GPU memory "
-                               "faults (two dedups of many tiles in flight together) whose cause is not yet found; "
-                               "use Layer.step")
+                 max_indices: int = 0, max_bags: int = 0, group: int = 4, rounding: str = "nearest", seed: int = 0):
         import torch
-        if lookahead < 1:
-            raise ValueError("lookahead must be >= 1")
+        if group < 1:
+            raise ValueError("group must be >= 1")
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
         dev = tables.weights.device
         D = int(tables.weights.shape[1])
-        self.L = lookahead
-        # one set more than in flight: the update a dedup waits for was enqueued
-        # a whole step earlier, which keeps the host-side cost of the
-        # cross-stream wait small
-        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(lookahead + 2)]
-        self._main = torch.cuda.current_stream(dev)
-        self._sides = [torch.cuda.Stream(device=dev) for _ in range(lookahead)]
-        self.main = int(self._main.cuda_stream)
-        self.sides = [int(x.cuda_stream) for x in self._sides]
-        self.dedup_done = [_Hip.event() for _ in self.sets]
-        self.update_done = [_Hip.event() for _ in self.sets]
-        for e in self.update_done:
-            _Hip.record(e, self.main)
+        self.K = group
+        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(2 * group)]
         self.max_indices = max(1, max_indices)
-        self.k = 0               # index of the next step
-        self.enqueued = {}       # step index -> batch whose dedup is enqueued
-        # argument values that stay fixed across steps, marshalled once
+        self._side_stream = torch.cuda.Stream(device=dev)
+        self.side = int(self._side_stream.cuda_stream)
+        self._ev_start = _Hip.event()
+        self._ev_side = [_Hip.event(), _Hip.event()]   # a group's dedups are done (per set parity)
+        self._ev_main = [_Hip.event(), _Hip.event()]   # the main stream's group that read a set is done
+        self._status = torch.zeros(4, dtype=torch.int32, device=dev)
         self._ct = ctypes.byref(tables.c())
-        self._upd = _update(opt, lr, eps, state)
+        self.rounding, self.seed, self.steps_done = rounding, seed, 0
+        self._updc = _update(opt, lr, eps, state, rounding, seed)
+        self._upd = ctypes.byref(self._updc)
         self._pool = POOL[pool]
         self._set_args = [(_ptr(b.unique_keys), _ptr(b.counts), _ptr(b.seg_offsets), _ptr(b.sort_perm),
                            _ptr(b.num_unique), _ptr(b.ws), b.ws.numel() * b.ws.element_size()) for b in self.sets]
@@ -472,43 +528,69 @@ class Pipeline:
     def __del__(self):
         try:
             L = _Hip.lib()
-            for e in self.dedup_done + self.update_done:
+            for e in [self._ev_start] + self._ev_side + self._ev_main:
                 L.hipEventDestroy(e)
         except Exception:
             pass
 
-    def _dedup(self, j: int, batch: Batch) -> None:
-        if int(batch.indices.numel()) > self.max_indices:
-            raise ValueError("batch larger than the pipeline's buffers")
-        si = j % len(self.sets)
-        uk, cnt, seg, perm, nu, ws, wsb = self._set_args[si]
-        side = self.sides[j % self.L]
-        _Hip.wait(side, self.update_done[si])
-        _check("emb_unique_ids", lib().emb_unique_ids(self._ct, ctypes.byref(batch.c()), uk, cnt, seg, perm, nu, ws,
-                                                      wsb, side))
-        _Hip.record(self.dedup_done[si], side)
-        self.enqueued[j] = batch
-
-    def step(self, batch: Batch, out, grad_out, upcoming=(), grad_rows=None) -> None:
-        """Forward of `batch` into `out`, then its backward with `grad_out`.
-        `upcoming`: the next batches in order (up to `lookahead` are used),
-        whose dedups are started now."""
-        k = self.k
-        if self.enqueued.get(k) is not batch:
-            self._dedup(k, batch)
-        for i, nb in enumerate(upcoming):
-            if i >= self.L:
-                break
-            if k + 1 + i not in self.enqueued:
-                self._dedup(k + 1 + i, nb)
-        si = k % len(self.sets)
+    def run(self, steps, stream=None) -> None:
+        """Enqueue one training step per ``(batch, out, grad_out)`` of
+        ``steps``, in order, on ``stream`` (the forward of each batch into its
+        ``out``, then its backward with ``grad_out`` and the optimizer step).
+        Every step's results are complete when ``stream`` reaches the end of
+        the enqueued work; the side stream's work all precedes it."""
+        steps = list(steps)
+        for b, _, _ in steps:
+            if int(b.indices.numel()) > self.max_indices:
+                raise ValueError("batch larger than the pipeline's buffers")
+        if not steps:
+            return
         L = lib()
-        cb = ctypes.byref(batch.c())
-        _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, self._pool, _ptr(out), self.main))
-        _Hip.wait(self.main, self.dedup_done[si])
-        uk, cnt, seg, perm, nu, ws, wsb = self._set_args[si]
-        _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, self._pool, _ptr(grad_out), perm, seg, uk, nu,
-                                                    _ptr(grad_rows), ctypes.byref(self._upd), ws, wsb, self.main))
-        _Hip.record(self.update_done[si], self.main)
-        del self.enqueued[k]
-        self.k = k + 1
+        main = _stream(stream)
+        K = self.K
+        ngroups = (len(steps) + K - 1) // K
+        # the side stream starts after everything already on the main stream
+        _Hip.record(self._ev_start, main)
+        _Hip.wait(self.side, self._ev_start)
+
+        def dedups(g):
+            par = g % 2
+            for i, (b, _, _) in enumerate(steps[g * K:(g + 1) * K]):
+                uk, cnt, seg, perm, nu, ws, wsb = self._set_args[par * K + i]
+                _check("emb_unique_ids", L.emb_unique_ids(self._ct, ctypes.byref(b.c()), uk, cnt, seg, perm, nu, ws,
+                                                          wsb, self.side))
+            _Hip.record(self._ev_side[par], self.side)
+
+        dedups(0)
+        for g in range(ngroups):
+            if g + 1 < ngroups:
+                if g >= 1:
+                    # the sets of group g + 1 were read by the main stream's group g - 1
+                    _Hip.wait(self.side, self._ev_main[(g + 1) % 2])
+                dedups(g + 1)
+            _Hip.wait(main, self._ev_side[g % 2])
+            for i, (b, out, grad_out) in enumerate(steps[g * K:(g + 1) * K]):
+                uk, cnt, seg, perm, nu, ws, wsb = self._set_args[(g % 2) * K + i]
+                cb = ctypes.byref(b.c())
+                self._updc.seed = self.seed + self.steps_done
+                self.steps_done += 1
+                _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, self._pool, _ptr(out), main))
+                _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, self._pool, _ptr(grad_out), perm, seg, uk,
+                                                            nu, None, self._upd, ws, wsb, main))
+            _Hip.record(self._ev_main[g % 2], main)
+
+    def status(self, stream=None):
+        """Per buffer set, the status of its last step (emb_workspace_status);
+        synchronises."""
+        out = []
+        for b in self.sets:
+            workspace_status(b.ws, self._status, stream)
+            out.append(tuple(int(x) for x in self._status.cpu()))
+        return out
+
+    def check(self, stream=None) -> None:
+        """Raise StepFailed if the last step of any buffer set failed on the
+        device (that step wrote no table row)."""
+        for st in self.status(stream):
+            if st[0]:
+                raise StepFailed(*st)

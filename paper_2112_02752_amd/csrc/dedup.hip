@@ -186,27 +186,27 @@ __device__ __forceinline__ void block_excl_scan(uint32_t* arr, uint32_t* s_wsum)
 // sleep, so every retry round costs one memory round trip however many words
 // are stale.  The wait is bounded in time (kWaitTicks).
 template <int K>
-__device__ __forceinline__ void poll_batch(const uint64_t* base, int stride, int lo, int n, int d, uint32_t tag,
-                                           WsHeader* h, uint32_t site, uint64_t (&v)[K]) {
+__device__ __forceinline__ void poll_batch(const uint64_t* base, int stride, int lo, int n, int d, uint64_t tag,
+                                           WsHeader* h, uint32_t g, uint32_t site, uint64_t (&v)[K]) {
   // words past n stand in as ready
   uint32_t stale = 0;
 #pragma unroll
-  for (int i = 0; i < K; ++i) stale |= (i < n && (uint32_t)(v[i] >> 32) != tag) ? (1u << i) : 0u;
+  for (int i = 0; i < K; ++i) stale |= (i < n && !word_current(v[i], tag)) ? (1u << i) : 0u;
   uint32_t spins = 0;
   const uint64_t t0 = stale ? wait_clock() : 0;
   while (stale) {
-    if (wait_over(h, t0, ++spins)) {
-      flag_timeout(h, site);
+    if (wait_over(h, g, t0, ++spins)) {
+      flag_timeout(h, g, site);
       break;
     }
     __builtin_amdgcn_s_sleep(1);
     const uint64_t* p = base + (size_t)lo * stride + d;
 #pragma unroll
     for (int i = 0; i < K; ++i)
-      if (stale & (1u << i)) v[i] = ld_acquire_u64(p + (size_t)i * stride);
+      if (stale & (1u << i)) v[i] = ld_relaxed_u64(p + (size_t)i * stride);
     stale = 0;
 #pragma unroll
-    for (int i = 0; i < K; ++i) stale |= (i < n && (uint32_t)(v[i] >> 32) != tag) ? (1u << i) : 0u;
+    for (int i = 0; i < K; ++i) stale |= (i < n && !word_current(v[i], tag)) ? (1u << i) : 0u;
   }
 }
 
@@ -217,14 +217,14 @@ __device__ __forceinline__ void poll_batch(const uint64_t* base, int stride, int
 // its own.
 static_assert((kPrefixGroup - 1) * kSortThreads * kSortItemsWide < 65536, "in-group prefixes fit 16 bits");
 __device__ __forceinline__ void group_counts(const uint64_t* rows, uint64_t* grp, int stride, int g, int g0, int g1,
-                                             int d, uint32_t tag, WsHeader* h, uint32_t site,
+                                             int d, uint64_t tag, WsHeader* h, uint32_t gcall, uint32_t site,
                                              uint32_t (&pk)[kPrefixGroup / 2],
                                              uint32_t& last_pre) {
   uint64_t v[kPrefixGroup];
   const int n = g1 - g0;
 #pragma unroll
-  for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(rows + (size_t)(g0 + i) * stride + d) : 0;
-  poll_batch<kPrefixGroup>(rows, stride, g0, n, d, tag, h, site, v);
+  for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_relaxed_u64(rows + (size_t)(g0 + i) * stride + d) : 0;
+  poll_batch<kPrefixGroup>(rows, stride, g0, n, d, tag, h, gcall, site, v);
   uint32_t run = 0;
   last_pre = 0;
 #pragma unroll
@@ -232,26 +232,27 @@ __device__ __forceinline__ void group_counts(const uint64_t* rows, uint64_t* grp
     if (i % 2 == 0) pk[i / 2] = run;
     else pk[i / 2] |= run << 16;
     if (i == n - 1) last_pre = run;
-    if (i < n) run += (uint32_t)v[i];
+    if (i < n) run += word_count(v[i]);
   }
-  st_u64(grp + (size_t)g * stride + d, ((uint64_t)tag << 32) | run);
+  st_u64(grp + (size_t)g * stride + d, word_make(tag, run));
 }
 
 // Sum of the published group sums of digit d before group g, and of all of
 // them (the digit's total), loaded in batches of kPrefixGroup.
-__device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int g, int ngroups, int d, uint32_t tag,
-                                           WsHeader* h, uint32_t site, uint32_t& before, uint32_t& total) {
+__device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int g, int ngroups, int d, uint64_t tag,
+                                           WsHeader* h, uint32_t gcall, uint32_t site, uint32_t& before,
+                                           uint32_t& total) {
   before = total = 0;
   for (int base = 0; base < ngroups; base += kPrefixGroup) {
     const int n = min(kPrefixGroup, ngroups - base);
     uint64_t gv[kPrefixGroup];
 #pragma unroll
-    for (int i = 0; i < kPrefixGroup; ++i) gv[i] = i < n ? ld_acquire_u64(grp + (size_t)(base + i) * stride + d) : 0;
-    poll_batch<kPrefixGroup>(grp, stride, base, n, d, tag, h, site, gv);
+    for (int i = 0; i < kPrefixGroup; ++i) gv[i] = i < n ? ld_relaxed_u64(grp + (size_t)(base + i) * stride + d) : 0;
+    poll_batch<kPrefixGroup>(grp, stride, base, n, d, tag, h, gcall, site, gv);
 #pragma unroll
     for (int i = 0; i < kPrefixGroup; ++i) {
       if (i < n) {
-        const uint32_t c = (uint32_t)gv[i];
+        const uint32_t c = word_count(gv[i]);
         total += c;
         if (base + i < g) before += c;
       }
@@ -267,7 +268,7 @@ __device__ __forceinline__ void group_sums(const uint64_t* grp, int stride, int 
 // publishes for every tile of its group the final output offset of digit d in
 // that tile's status word.  The tiles rank and reorder their keys meanwhile.
 template <int RB>
-__device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t tag, uint32_t* s_base,
+__device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t gcall, uint64_t tag, uint32_t* s_base,
                                                   uint32_t* s_wsum, uint32_t* s_pre) {
   constexpr int ND = 1 << RB;
   constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
@@ -282,8 +283,8 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
     const int d = tid + k * kSortThreads;
     if (d < ND) {
       uint32_t pk[kPrefixGroup / 2], unused;
-      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, a.hdr, kSiteGroupCounts | ((uint32_t)a.pass << 4), pk,
-                   unused);
+      group_counts(a.rows, a.grp, a.status_stride, g, g0, g1, d, tag, a.hdr, gcall,
+                   kSiteGroupCounts | ((uint32_t)a.pass << 4), pk, unused);
 #pragma unroll
       for (int j = 0; j < kPrefixGroup / 2; ++j) s_pre[j * ND + d] = pk[j];
     }
@@ -294,13 +295,13 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
     excl[k] = 0;
     if (d < ND) {
       uint32_t total = 0;
-      group_sums(a.grp, a.status_stride, g, ngroups, d, tag, a.hdr, kSiteGroupSums | ((uint32_t)a.pass << 4), excl[k], total);
+      group_sums(a.grp, a.status_stride, g, ngroups, d, tag, a.hdr, gcall, kSiteGroupSums | ((uint32_t)a.pass << 4),
+                 excl[k], total);
       s_base[d] = total;
     }
   }
   __syncthreads();
   block_excl_scan<RB>(s_base, s_wsum);
-  const uint64_t tag_hi = (uint64_t)tag << 32;
 #pragma unroll
   for (int k = 0; k < DPT; ++k) {
     const int d = tid + k * kSortThreads;
@@ -309,7 +310,7 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
 #pragma unroll
       for (int i = 0; i < kPrefixGroup; ++i) {
         const uint32_t pre = (s_pre[(i / 2) * ND + d] >> (16 * (i % 2))) & 0xffffu;
-        if (g0 + i < g1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, tag_hi | (gb + pre));
+        if (g0 + i < g1) st_u64(a.status + (size_t)(g0 + i) * a.status_stride + d, word_make(tag, gb + pre));
       }
     }
   }
@@ -326,11 +327,12 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
           const uint64_t* lb = a.later + (size_t)(p - 1) * a.status_stride;
           uint64_t v[kPrefixGroup];
 #pragma unroll
-          for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_acquire_u64(lb + (size_t)(g0 + i) * lstride + d) : 0;
-          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, a.hdr, kSiteLaterCounts | ((uint32_t)a.pass << 4), v);
+          for (int i = 0; i < kPrefixGroup; ++i) v[i] = i < n ? ld_relaxed_u64(lb + (size_t)(g0 + i) * lstride + d) : 0;
+          poll_batch<kPrefixGroup>(lb, (int)lstride, g0, n, d, tag, a.hdr, gcall,
+                                   kSiteLaterCounts | ((uint32_t)a.pass << 4), v);
           uint32_t sum = 0;
 #pragma unroll
-          for (int i = 0; i < kPrefixGroup; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
+          for (int i = 0; i < kPrefixGroup; ++i) sum += i < n ? word_count(v[i]) : 0u;
           if (sum) atomic_add_u32(&a.totals_all[p * kMaxDigits + d], sum);
         }
       }
@@ -345,7 +347,7 @@ __device__ __forceinline__ void sort_prefix_block(const PassArgs& a, uint32_t ta
 // and the thread publishes the final offset of its digit for each tile of its
 // chunk.
 template <int RB>
-__device__ __forceinline__ void sort_prefix_range(const PassArgs& a, uint32_t tag, uint32_t* s_base,
+__device__ __forceinline__ void sort_prefix_range(const PassArgs& a, uint32_t gcall, uint64_t tag, uint32_t* s_base,
                                                   uint32_t* s_wsum, uint32_t* s_cs) {
   constexpr int ND = 1 << RB;
   constexpr int DPT = (ND + kSortThreads - 1) / kSortThreads;
@@ -367,21 +369,22 @@ __device__ __forceinline__ void sort_prefix_range(const PassArgs& a, uint32_t ta
   // this digit's counts in the chunk's tiles
   uint64_t v[kRangeTiles];
 #pragma unroll
-  for (int i = 0; i < kRangeTiles; ++i) v[i] = i < n ? ld_acquire_u64(a.rows + (size_t)(t0 + i) * a.status_stride + d) : 0;
-  poll_batch<kRangeTiles>(a.rows, a.status_stride, t0, n, d, tag, a.hdr, kSiteRangeCounts | ((uint32_t)a.pass << 4), v);
+  for (int i = 0; i < kRangeTiles; ++i)
+    v[i] = i < n ? ld_relaxed_u64(a.rows + (size_t)(t0 + i) * a.status_stride + d) : 0;
+  poll_batch<kRangeTiles>(a.rows, a.status_stride, t0, n, d, tag, a.hdr, gcall,
+                          kSiteRangeCounts | ((uint32_t)a.pass << 4), v);
   uint32_t sum = 0;
 #pragma unroll
-  for (int i = 0; i < kRangeTiles; ++i) sum += i < n ? (uint32_t)v[i] : 0u;
+  for (int i = 0; i < kRangeTiles; ++i) sum += i < n ? word_count(v[i]) : 0u;
   s_cs[c * DB + dl] = sum;
   __syncthreads();
   uint32_t run = s_base[d];
   for (int cc = 0; cc < c; ++cc) run += s_cs[cc * DB + dl];
-  const uint64_t tag_hi = (uint64_t)tag << 32;
 #pragma unroll
   for (int i = 0; i < kRangeTiles; ++i) {
     if (i < n) {
-      st_u64(a.status + (size_t)(t0 + i) * a.status_stride + d, tag_hi | run);
-      run += (uint32_t)v[i];
+      st_u64(a.status + (size_t)(t0 + i) * a.status_stride + d, word_make(tag, run));
+      run += word_count(v[i]);
     }
   }
 }
@@ -497,11 +500,14 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   __syncthreads();
   const int tile = blockIdx.x;
   const uint32_t mask = (1u << a.bits) - 1u;
-  // the call's tag: the header's generation advances once per call, at its end
-  const uint32_t tag = 0x80000000u | ((a.hdr->gen + 1u) * 8u + (uint32_t)a.pass);
+  // the call's generation (the header's advances once per call, in the
+  // unique scan) and this pass's tag
+  const uint32_t gcall = next_gen(a.hdr->gen);
+  const uint64_t tag = word_tag(gcall, (uint32_t)a.pass);
+  if (a.pass == 0 && blockIdx.x == 0 && tid == 0) a.hdr->cur = gcall;
   if (a.coresident && (int)blockIdx.x >= a.ntiles) {
-    if (a.prefix_mode == kPrefixRanges) sort_prefix_range<RB>(a, tag, s_gbase, s_wsum, s_keys);
-    else sort_prefix_block<RB>(a, tag, s_gbase, s_wsum, &s_cnt[0][0]);
+    if (a.prefix_mode == kPrefixRanges) sort_prefix_range<RB>(a, gcall, tag, s_gbase, s_wsum, s_keys);
+    else sort_prefix_block<RB>(a, gcall, tag, s_gbase, s_wsum, &s_cnt[0][0]);
     return;
   }
   const int64_t wbase = (int64_t)tile * TILE + w * (kWave * IT);
@@ -516,7 +522,6 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   // The tile's digit counts are published as soon as its digits are known
   // (from an LDS histogram), so that the other tiles' prefixes advance while
   // this tile finds its bags, ranks and reorders its keys.
-  const uint64_t tag_hi = (uint64_t)tag << 32;
   auto publish_counts = [&]() {
     if (!a.coresident) return;  // the offsets were computed before the pass
 #pragma unroll
@@ -526,7 +531,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
 #pragma unroll
     for (int k = 0; k < DPT; ++k) {
       const int d = tid + k * kSortThreads;
-      if (d < ND) st_u64(row + d, tag_hi | s_hist[d]);
+      if (d < ND) st_u64(row + d, word_make(tag, s_hist[d]));
     }
     if (a.later) {
       // then the later passes' digits (counted in s_cnt, which stays zero
@@ -543,7 +548,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
 #pragma unroll
         for (int k = 0; k < DPT; ++k) {
           const int d = tid + k * kSortThreads;
-          if (d < (1 << a.pass_bits[p])) st_u64(lrow + d, tag_hi | s_cnt[p - 1][d]);
+          if (d < (1 << a.pass_bits[p])) st_u64(lrow + d, word_make(tag, s_cnt[p - 1][d]));
         }
       }
       __syncthreads();
@@ -652,9 +657,10 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       const int d = tid + k * kSortThreads;
       excl[k] = 0;
       if (d < ND) {
-        uint64_t fv[1] = {ld_acquire_u64(a.status + (size_t)tile * a.status_stride + d)};
-        poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, a.hdr, kSiteTileOffsets | ((uint32_t)a.pass << 4), fv);
-        excl[k] = (uint32_t)fv[0];
+        uint64_t fv[1] = {ld_relaxed_u64(a.status + (size_t)tile * a.status_stride + d)};
+        poll_batch<1>(a.status, a.status_stride, tile, 1, d, tag, a.hdr, gcall,
+                      kSiteTileOffsets | ((uint32_t)a.pass << 4), fv);
+        excl[k] = word_count(fv[0]);
       }
     }
     // the final offsets replace the digit bases
@@ -689,7 +695,7 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       a.vals_out[dst] = s_vals[s];
       a.bags_out[dst] = s_bags[s];
     } else {
-      atomicOr(&a.hdr->error, 2u);  // digit totals inconsistent with the keys
+      flag_error(a.hdr, gcall, 2u);  // digit totals inconsistent with the keys
     }
   }
 }
@@ -889,19 +895,30 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
   constexpr int NW = kUniqThreads / kWave;
   __shared__ uint32_t s_keys[kUniqTile];
   __shared__ uint32_t s_wc[NW], s_wq[NW];
-  __shared__ uint32_t s_pc, s_pq, s_prev;
+  __shared__ uint32_t s_pc, s_pq, s_prev, s_fail;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  // the sort is complete: clear the last pass's totals and advance the
-  // generation that tags the next call's coordination words
-  if (blockIdx.x == 0) {
-    for (int d = tid; d < kMaxDigits; d += kUniqThreads) a.prev_totals[d] = 0u;
-    if (tid == 0) {
-      a.hdr->gen = a.hdr->gen + 1u;
-    }
-  }
-  __syncthreads();
   const int tile = blockIdx.x;
   const int64_t tbase = (int64_t)tile * kUniqTile;
+  const bool last_tile = tbase + kUniqTile >= (int64_t)a.N;
+  // this call's generation (its first sort pass recorded it); the sort is
+  // complete, so its error bits are final: clear the last pass's totals and
+  // make the call's generation the header's
+  const uint32_t gcall = a.hdr->cur;
+  if (tile == 0) {
+    for (int d = tid; d < kMaxDigits; d += kUniqThreads) a.prev_totals[d] = 0u;
+    if (tid == 0) a.hdr->gen = gcall;
+  }
+  if (tid == 0) s_fail = call_errors(a.hdr, gcall) & kDedupErrors;
+  __syncthreads();
+  if (s_fail) {
+    // the sort failed: no unique ids, so neither a fused nor an unfused
+    // update touches any row
+    if (tile == 0 && tid == 0) {
+      a.num_unique[0] = 0;
+      a.seg[0] = a.N;
+    }
+    return;
+  }
   // every load of the tile is issued before the first LDS store
   uint32_t kv[kUniqItems];
 #pragma unroll
@@ -960,6 +977,7 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     // windows are then taken in order up to the first word not yet published
     // or the first inclusive prefix
     uint32_t pc = 0, pq = 0;
+    bool gave_up = false;
     if (tile == 0) {
       if (lane == 0) st_u64(a.status, pack_uniq(kFlagInc, tile_c, tile_q));
     } else {
@@ -967,12 +985,12 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
       int j = tile - 1;
       uint32_t spins = 0;
       const uint64_t t0 = wait_clock();
-      while (true) {
+      while (!gave_up) {
         uint64_t sv[kUniqWindows];
 #pragma unroll
         for (int i = 0; i < kUniqWindows; ++i) {
           const int jj = j - i * kWave - lane;
-          sv[i] = jj >= 0 ? ld_acquire_u64(a.status + jj) : 0;
+          sv[i] = jj >= 0 ? ld_relaxed_u64(a.status + jj) : 0;
         }
         uint32_t c = 0, q = 0;
         int took = 0;
@@ -1007,21 +1025,32 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
         if (done) break;
         j -= took;
         if (took == 0) {
-          if (wait_over(a.hdr, t0, ++spins)) {
-            if (lane == 0) flag_timeout(a.hdr, kSiteUnique);
-            break;
+          gave_up = __builtin_amdgcn_readfirstlane((int)wait_over(a.hdr, gcall, t0, ++spins)) != 0;
+          if (gave_up) {
+            if (lane == 0) flag_timeout(a.hdr, gcall, kSiteUnique);
+          } else {
+            __builtin_amdgcn_s_sleep(1);
           }
-          __builtin_amdgcn_s_sleep(1);
         }
       }
-      if (lane == 0) st_u64(a.status + tile, pack_uniq(kFlagInc, pc + tile_c, max(pq, tile_q)));
+      // a tile whose look-back gave up publishes no inclusive prefix, so no
+      // later tile builds on its short one
+      if (lane == 0 && !gave_up) st_u64(a.status + tile, pack_uniq(kFlagInc, pc + tile_c, max(pq, tile_q)));
     }
     if (lane == 0) {
       s_pc = pc;
       s_pq = pq;
+      // A tile whose look-back gave up writes nothing.  The last tile
+      // reports no unique ids if any look-back of the call gave up (the
+      // gradient reduce also checks the call's error bits).
+      s_fail = gave_up || (last_tile && (call_errors(a.hdr, gcall) & 1u));
     }
   }
   __syncthreads();
+  if (s_fail) {
+    if (last_tile && tid == 0) a.num_unique[0] = 0;
+    return;
+  }
   uint32_t u = s_pc + c_ex;
   uint32_t lastq = max(s_pq, q_ex);
 #pragma unroll

@@ -89,7 +89,13 @@ size_t emb_workspace_size(int64_t num_indices, int64_t num_bags, int32_t dim) {
   return ws_layout(num_indices, num_bags, dim).total;
 }
 
-size_t emb_workspace_error_offset(void) { return offsetof(WsHeader, error); }
+size_t emb_workspace_error_offset(void) { return offsetof(WsHeader, err); }
+
+emb_status emb_workspace_status(const void* ws, size_t ws_bytes, int32_t* status, void* stream) {
+  if (ws == nullptr || status == nullptr) return EMB_EINVAL;
+  if (((uintptr_t)ws & 255u) != 0 || ws_bytes < sizeof(WsHeader)) return EMB_EWORKSPACE;
+  return hip_status(launch_workspace_status(ws, status, (hipStream_t)stream));
+}
 
 emb_status emb_workspace_init(void* ws, size_t ws_bytes, void* stream) {
   if (ws == nullptr) return EMB_EINVAL;

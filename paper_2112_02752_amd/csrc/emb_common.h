@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "emb.h"
+#include "ws_words.h"
 
 namespace emb {
 
@@ -58,16 +59,18 @@ constexpr int kTinySeg = 16;
 constexpr int kCombineThreads = 1024;
 constexpr int kCombineChunks = 64;
 
-// Workspace header (device).  gen counts emb_unique_ids calls; it tags the
-// sort's published counts so they never need clearing.
+// Workspace header (device).  Every emb_unique_ids call on a workspace has a
+// generation g = next_gen(gen) (ws_words.h): it tags the words the sort's
+// workgroups publish to one another, so they never need clearing, and the
+// error bits of that call, so that a failure belongs to one call only.
 struct WsHeader {
-  uint32_t gen;
-  uint32_t error;
-  uint32_t reserved[8];
-  // first wait that ran out: its site code, block index and the number of
-  // waits that ran out in all (kept until the workspace is initialised again)
-  uint32_t timeout_site, timeout_block, timeouts;
-  uint32_t pad[51];
+  uint32_t gen;  // generation of the last dedup whose unique scan has run
+  uint32_t cur;  // generation of the dedup in flight (written by its first sort pass)
+  uint64_t err;  // (generation << 32) | error bits of the last call that set any
+  // the first wait that ran out since the workspace was initialised: its site
+  // code, block index and call generation; the number of waits that ran out
+  uint32_t timeout_site, timeout_block, timeout_gen, timeouts;
+  uint32_t pad[56];
 };
 static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 
@@ -198,7 +201,9 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-__device__ __forceinline__ uint64_t ld_acquire_u64(const uint64_t* p) {
+// device-coherent (agent scope) loads and stores of words other workgroups
+// publish or poll; relaxed: a poll re-reads until the word carries its tag
+__device__ __forceinline__ uint64_t ld_relaxed_u64(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_u64(uint64_t* p, uint64_t v) {
@@ -223,13 +228,16 @@ int coresident_limit(const void* kernel, int threads);
 
 // Bound of a wait for a word another workgroup publishes, in ticks of the
 // 100 MHz constant clock: 20 ms, thousands of times any wait of a healthy
-// call.  Running out sets bit 0 of the error word, records the wait, and lets
-// the wave continue, so every wave always exits; the waits of a call that has
-// already timed out give up at their next check of the error word.
+// call.  Running out sets bit 0 of the call's error bits, records the wait,
+// and lets the wave continue, so every wave always exits; the other waits of
+// a call that has timed out give up at their next check of its error bits.
 constexpr uint64_t kWaitTicks = 2000000;
 // error bits of the dedup: a wait ran out (bit 0); digit totals inconsistent
-// with the keys (bit 1).  The gradient reduce does nothing when either is set.
+// with the keys (bit 1).  The gradient reduce writes no table row when either
+// is set for the dedup it follows.
 constexpr uint32_t kDedupErrors = 3u;
+// error bit of the gradient combine: one of its waits ran out
+constexpr uint32_t kCombineError = 4u;
 
 // Site codes of the waits: (kernel << 8) | (sort pass << 4) | wait.
 enum WaitSite : uint32_t {
@@ -244,18 +252,35 @@ enum WaitSite : uint32_t {
 
 __device__ __forceinline__ uint64_t wait_clock() { return wall_clock64(); }
 
-// a wait that started at t0 has run out (or another wait of the call has)
-__device__ __forceinline__ bool wait_over(const WsHeader* h, uint64_t t0, uint32_t spins) {
-  if ((spins & 31u) == 0u && (__hip_atomic_load(&h->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 1u))
-    return true;
+// error bits of call g (0 if the error word belongs to another call)
+__device__ __forceinline__ uint32_t call_errors(const WsHeader* h, uint32_t g) {
+  const uint64_t v = __hip_atomic_load(&h->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return err_bits_of(v, g);
+}
+
+// set `bits` among the error bits of call g; the word of an earlier call is
+// replaced, not added to
+__device__ __forceinline__ void flag_error(WsHeader* h, uint32_t g, uint32_t bits) {
+  uint64_t old = __hip_atomic_load(&h->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  while (!__hip_atomic_compare_exchange_strong(&h->err, &old, err_word_with(old, g, bits), __ATOMIC_RELAXED,
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+  }
+}
+
+// a wait of call g that started at t0 has run out (or another wait of the call has)
+__device__ __forceinline__ bool wait_over(const WsHeader* h, uint32_t g, uint64_t t0, uint32_t spins) {
+  if ((spins & 31u) == 0u && (call_errors(h, g) & 1u)) return true;
   return wait_clock() - t0 > kWaitTicks;
 }
 
-// a wait ran out: set `bit` in the error word and record the first such wait
-__device__ __forceinline__ void flag_timeout(WsHeader* h, uint32_t site, uint32_t bit = 1u) {
-  atomicOr(&h->error, bit);
+// a wait of call g ran out: set `bit` in its error bits and record the first such wait
+__device__ __forceinline__ void flag_timeout(WsHeader* h, uint32_t g, uint32_t site, uint32_t bit = 1u) {
+  flag_error(h, g, bit);
   atomicAdd(&h->timeouts, 1u);
-  if (atomicCAS(&h->timeout_site, 0u, site) == 0u) h->timeout_block = blockIdx.x;
+  if (atomicCAS(&h->timeout_site, 0u, site) == 0u) {
+    h->timeout_block = blockIdx.x;
+    h->timeout_gen = g;
+  }
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }

@@ -115,5 +115,6 @@ struct ValidateLaunch {
 };
 hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_workspace_status(const void* ws, int32_t* status, hipStream_t s);
 
 }  // namespace emb

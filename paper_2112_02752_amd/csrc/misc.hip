@@ -44,7 +44,22 @@ __global__ void k_validate(const int32_t* offsets, const void* idx, int32_t idx6
   if (bits) atomicOr(reinterpret_cast<uint32_t*>(flag), bits);
 }
 
+// status of the last dedup call on a workspace (emb_workspace_status)
+__global__ void k_workspace_status(const WsHeader* h, int32_t* status) {
+  if (threadIdx.x == 0) {
+    status[0] = (int32_t)call_errors(h, h->gen);
+    status[1] = (int32_t)h->timeout_site;
+    status[2] = (int32_t)h->timeout_block;
+    status[3] = (int32_t)h->timeouts;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_workspace_status(const void* ws, int32_t* status, hipStream_t s) {
+  hipLaunchKernelGGL(k_workspace_status, dim3(1), dim3(64), 0, s, static_cast<const WsHeader*>(ws), status);
+  return hipGetLastError();
+}
 
 hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s) {
   const size_t n = bytes / 4;

@@ -273,6 +273,13 @@ __device__ __forceinline__ void finalize(const Upd& up, float* grad_rows, int64_
   apply_row<TW, G, NV>(up, grad_rows, u, r, acc, pre, sub);
 }
 
+// whether the dedup this reduce follows flagged an error: its unique scan made
+// its generation the header's, so its error bits are those of that generation
+__device__ __forceinline__ bool dedup_failed(const RArgs& a) {
+  const WsHeader* h = reinterpret_cast<const WsHeader*>(a.hdr);
+  return (call_errors(h, h->gen) & kDedupErrors) != 0u;
+}
+
 // 1 / bag length for mean pooling (a position's bag is never empty), else 1
 __device__ __forceinline__ float bag_scale(const RArgs& a, int bag) {
   return a.pool == EMB_POOL_MEAN ? 1.0f / (float)(a.offsets[bag + 1] - a.offsets[bag]) : 1.0f;
@@ -481,9 +488,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(reduce_wave
   const int wave_id = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   const int nwaves = gridDim.x * 4;
   const int U = *a.num_unique;
-  // the dedup of this workspace flagged an error (its outputs are undefined):
-  // no gradient row is formed and no table row written
-  if (reinterpret_cast<const WsHeader*>(a.hdr)->error & kDedupErrors) return;
+  if (dedup_failed(a)) {
+    // The dedup this reduce follows flagged an error: its outputs are
+    // undefined, so no table row is written.  Unfused, the gradient rows of
+    // the unique ids it reported are zeroed, so that the optimizer step
+    // applied to them afterwards leaves every row as it is (for SGD, and for
+    // Adagrad with eps > 0).
+    if (a.grad_rows) {
+      const int64_t n = (int64_t)min(max(U, 0), a.N) * a.D;
+      for (int64_t i = (int64_t)wave_id * kWave + lane; i < n; i += (int64_t)nwaves * kWave) a.grad_rows[i] = 0.f;
+    }
+    return;
+  }
   // the combine that follows starts from cleared level-2 rows and counters
   {
     const int nw = a.ncomb * 2 * a.D;
@@ -551,7 +567,7 @@ __device__ __forceinline__ void level2_sum(const RArgs& a, int g0, int g1, int g
       for (int v = 0; v < NV; ++v) {
         const int c0 = (v * G + sub) * 4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) x[q][v][e] = ld_acquire_u64(src + (c0 < a.D ? c0 + e : e));
+        for (int e = 0; e < 4; ++e) x[q][v][e] = ld_relaxed_u64(src + (c0 < a.D ? c0 + e : e));
       }
     }
 #pragma unroll
@@ -568,12 +584,12 @@ __device__ __forceinline__ void level2_sum(const RArgs& a, int g0, int g1, int g
           uint32_t spins = 0;
           const uint64_t t0 = wait_clock();
           while ((uint32_t)(x[q][v][e] >> 32) != kLevel2Tag) {
-            if (wait_over(h, t0, ++spins)) {
-              flag_timeout(h, kSiteCombine, 4u);
+            if (wait_over(h, h->gen, t0, ++spins)) {
+              flag_timeout(h, h->gen, kSiteCombine, kCombineError);
               break;
             }
             __builtin_amdgcn_s_sleep(1);
-            x[q][v][e] = ld_acquire_u64(src + c0 + e);
+            x[q][v][e] = ld_relaxed_u64(src + c0 + e);
           }
           acc[v][e] += __uint_as_float((uint32_t)x[q][v][e]);
         }
@@ -598,7 +614,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_reduce_combine(RArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), g = lane / G, sub = lane % G;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform across the wavefront
   const int U = *a.num_unique;
-  if (reinterpret_cast<const WsHeader*>(a.hdr)->error & kDedupErrors) return;  // as in k_reduce_main
+  if (dedup_failed(a)) return;  // as in k_reduce_main
   const int blk = blockIdx.x;
   const int c0 = blk * kCombineChunks, c1 = min(a.nchunks, c0 + kCombineChunks);
   if (tid == 0) s_n = 0;

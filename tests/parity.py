@@ -140,8 +140,7 @@ def gpu_step(dl: DeviceLayer, offsets: np.ndarray, indices: np.ndarray, grad: np
         grad_rows = _serial_step(dl, b, out, G, N, pool, opt, lr, eps, fused, want_grad_rows, layer, rounding, seed)
     torch.cuda.synchronize()
     U = int(layer.num_unique.cpu().item())
-    eo = emb.workspace_error_offset()
-    ws_err = int(layer.ws[eo:eo + 4].cpu().numpy().view(np.uint32)[0])
+    ws_err = layer.status()[0]
     return StepResult(
         out=out.cpu().numpy(), num_unique=U,
         unique_keys=layer.unique_keys[:U].cpu().numpy().view(np.uint32),
@@ -179,7 +178,7 @@ def global_keys(row_offset, B: int, offsets: np.ndarray, indices: np.ndarray) ->
 
 def check_against_oracle(g: StepResult, o_out, o_dd: oracle.Dedup, o_gr, tol_out=TOL_FP32):
     """Integer outputs bit-exact, floats within tolerance."""
-    assert g.ws_error == 0, f"workspace error word {g.ws_error}"
+    assert g.ws_error == 0, f"the step failed on the device: error bits {g.ws_error}"
     r = rel_rownorm(g.out, o_out)
     assert r <= tol_out, f"forward rel err {r}"
     assert g.num_unique == o_dd.num_unique, (g.num_unique, o_dd.num_unique)

@@ -166,7 +166,25 @@ def test_sparse_update_argument_errors():
 
 
 def test_error_word_offset():
-    assert emb.workspace_error_offset() == 4
+    # uint32 generation at 0, uint32 in-flight generation at 4, uint64 error word at 8
+    assert emb.workspace_error_offset() == 8
+
+
+def test_workspace_status_argument_checks():
+    L = emb.lib()
+    assert L.emb_workspace_status(None, 256, 0x100, None) == emb.EMB_EINVAL
+    assert L.emb_workspace_status(0x1000, 256, None, None) == emb.EMB_EINVAL
+    assert L.emb_workspace_status(0x1010, 256, 0x100, None) == emb.EMB_EWORKSPACE   # misaligned
+    assert L.emb_workspace_status(0x1000, 255, 0x100, None) == emb.EMB_EWORKSPACE   # smaller than the header
+
+
+def test_step_failed_message_names_the_wait():
+    e = emb.StepFailed(1, 0x120, 17, 3)
+    msg = str(e)
+    assert "sort pass 2" in msg and "digit offsets" in msg and "workgroup 17" in msg and "3 waits" in msg
+    assert "unique scan" in str(emb.StepFailed(1, 0x200, 5, 1))
+    assert "inconsistent" in str(emb.StepFailed(2, 0, 0, 0))
+    assert "combine" in str(emb.StepFailed(4, 0x300, 2, 1))
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

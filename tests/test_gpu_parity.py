@@ -482,8 +482,7 @@ def test_c5_hundred_steps_sampled_rows():
         if s % 20 == 19:
             _say(f"  step {s + 1} done")
     torch.cuda.synchronize()
-    eo = emb.workspace_error_offset()
-    assert int(layer.ws[eo:eo + 4].cpu().numpy().view(np.uint32)[0]) == 0
+    layer.check()
     parity.check_rows(dl, store, sample, w.opt)
     assert untouched.size > 0
     np.testing.assert_array_equal(dl.rows(untouched.astype(np.uint32)), synth.weight_rows(w, untouched))
@@ -647,45 +646,78 @@ def test_stale_schedule_matches_oracle_replay(name, concurrent):
     parity.check_rows(dl, store, touched, w.opt)
 
 
-@pytest.mark.skip(reason="the pipelined schedule is switched off: bench runs of it (two dedups of 204 and 240 "
-                         "tiles in flight together) ended in GPU memory faults whose cause is not yet found")
-@pytest.mark.parametrize("lookahead", [1, 2, 3])
-def test_pipelined_schedule_equals_serial(lookahead):
-    """Dedup of batch k+1 overlapped with batch k (second stream) changes
-    nothing: tables, state and pooled outputs match serial steps bitwise."""
-    _say(f"case pipelined vs serial lookahead={lookahead}")
+@pytest.mark.parametrize("group,nsteps", [(1, 5), (2, 7), (4, 10)])
+def test_pipelined_schedule_equals_serial(group, nsteps):
+    """The dedups of the next group of batches on a side stream while the main
+    stream runs the forward and update of the current group change nothing:
+    tables, state and pooled outputs equal those of serial steps bit for bit
+    (step counts that leave a partial last group included)."""
+    _say(f"case pipelined vs serial group={group} steps={nsteps}")
     import torch
     import paper_2112_02752_amd as emb
     w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
-    batches = [synth.make_batch(w, s) for s in range(6)]
+    batches = [synth.make_batch(w, s) for s in range(nsteps)]
     nmax = max(len(b.indices) for b in batches)
     dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
               torch.from_numpy(b.grad).cuda()) for b in batches]
     results = []
     for mode in ("serial", "pipelined"):
         dl = parity.device_layer_from_workload(w)
-        outs = []
+        outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in dev_b]
         if mode == "serial":
-            layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
-                              concurrent=False)
-            for b, g in dev_b:
-                out = torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda")
+            layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags)
+            for (b, g), out in zip(dev_b, outs):
                 layer.step(b, out, g)
-                outs.append(out)
         else:
             pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
-                                max_bags=w.num_bags, lookahead=lookahead)
-            for i, (b, g) in enumerate(dev_b):
-                out = torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda")
-                pipe.step(b, out, g, upcoming=[x for x, _ in dev_b[i + 1:i + 1 + lookahead]])
-                outs.append(out)
+                                max_bags=w.num_bags, group=group)
+            # two runs: the second starts after everything the first enqueued
+            half = nsteps // 2
+            pipe.run([(b, o, g) for (b, g), o in zip(dev_b[:half], outs[:half])])
+            pipe.run([(b, o, g) for (b, g), o in zip(dev_b[half:], outs[half:])])
         torch.cuda.synchronize()
+        if mode == "pipelined":
+            pipe.check()
         results.append((dl.W.cpu().numpy(), dl.state.cpu().numpy(), [o.cpu().numpy() for o in outs]))
     (w0, s0, o0), (w1, s1, o1) = results
     np.testing.assert_array_equal(w0, w1)
     np.testing.assert_array_equal(s0, s1)
     for a, b in zip(o0, o1):
         np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("name,nsteps,group", [("c3", 6, 4), ("c2", 3, 2)])
+def test_pipelined_schedule_full_size(name, nsteps, group):
+    """Full-size pipelined steps against the oracle replaying the same steps on
+    the rows they touch: every pooled output, the final rows and state, rows
+    no step touched unchanged."""
+    _say(f"case pipelined full size {name} steps={nsteps} group={group}")
+    import oracle
+    import torch
+    import paper_2112_02752_amd as emb
+    w = synth.workload(name)
+    batches = [synth.make_batch(w, s) for s in range(nsteps)]
+    nmax = max(len(b.indices) for b in batches)
+    dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
+              torch.from_numpy(b.grad).cuda()) for b in batches]
+    dl = parity.device_layer_from_workload(w)
+    pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
+                        group=group)
+    outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in dev_b]
+    pipe.run([(b, o, g) for (b, g), o in zip(dev_b, outs)])
+    torch.cuda.synchronize()
+    pipe.check()
+    keys = [parity.global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices) for b in batches]
+    touched = np.unique(np.concatenate(keys))
+    store = oracle.RowStore(synth.weight_rows(w, touched), keys=touched.astype(np.uint32),
+                            state=np.zeros(len(touched), np.float32) if w.opt == "adagrad" else None)
+    for k, b in enumerate(batches):
+        o_out, _, _ = oracle.step(w.num_tables, w.row_offset, w.bags_per_table, b.offsets, b.indices, b.grad, store,
+                                  w.pool, w.opt, w.lr, w.eps)
+        r = parity.rel_rownorm(outs[k].cpu().numpy(), o_out)
+        assert r <= parity.TOL_FP32, f"pooled output of step {k}: rel err {r}"
+    parity.check_rows(dl, store, touched, w.opt)
+    parity.check_untouched(dl, w, touched)
 
 
 # ------------------------------------------------------------------ routing

@@ -456,6 +456,35 @@ def test_sr_bits_match_the_input_generators_splitmix64():
             assert oracle.sr_bits(seed, c) == int(L.synth_hash(seed, c)) >> 48, (seed, c)
 
 
+# splitmix64 (Steele, Lea and Flood 2014) started from state 0: its first
+# four outputs, the published reference sequence (each output mixes the state
+# after adding the golden-ratio increment 0x9e3779b97f4a7c15)
+SPLITMIX64_SEED0 = (0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F, 0xF88BB8A8724C81EC)
+SPLITMIX_INCREMENT = 0x9E3779B97F4A7C15
+
+
+def test_sr_bits_known_answers_of_splitmix64():
+    """Pins the oracle's random bits to the published splitmix64 outputs:
+    sr_bits(seed, c) is the top 16 bits of splitmix64's output for state
+    seed ^ (its output for state c).  With c = 0 the inner output is the
+    first published value; a seed of that value xor i * increment makes the
+    outer state i * increment, whose output is the (i+1)-th published value."""
+    inner = SPLITMIX64_SEED0[0]   # the output for state 0
+    for i, expect in enumerate(SPLITMIX64_SEED0):
+        seed = inner ^ ((i * SPLITMIX_INCREMENT) % 2 ** 64)
+        assert oracle.sr_bits(seed, 0) == expect >> 48, (i, hex(expect))
+
+
+def test_input_generator_hash_known_answers_of_splitmix64():
+    """The input generator's counter hash pins to the same published outputs
+    (synth_hash(seed, c) = splitmix64 output for state seed ^ output for state c)."""
+    import synth
+    L = synth._lib()
+    inner = SPLITMIX64_SEED0[0]
+    for i, expect in enumerate(SPLITMIX64_SEED0):
+        assert int(L.synth_hash(inner ^ ((i * SPLITMIX_INCREMENT) % 2 ** 64), 0)) == expect, i
+
+
 def _bf16_neighbours(x: np.float32):
     u = int(np.array([x], np.float32).view(np.uint32)[0])
     down = u >> 16
@@ -526,3 +555,37 @@ def test_invalid_inputs_are_rejected():
         oracle.pool_fwd(1, ro, 1, np.array([0, 1], np.int32), np.array([4], np.int32), st, "sum")
     with pytest.raises(oracle.OracleError):
         oracle.unique_ids(1, ro, 1, np.array([0, 1], np.int32), np.array([-1], np.int32))
+
+
+# ------------------------------------------------------- thread count
+
+@pytest.mark.parametrize("name,rounding", [("c2", "nearest"), ("c4", "stochastic"), ("c5", "nearest")])
+def test_results_do_not_depend_on_thread_count(name, rounding):
+    """The oracle's parallel loops (bags, segments, rows) compute every
+    output on one thread in a fixed order: one thread and eight give the
+    same forward, dedup, gradient rows, rows and state bit for bit."""
+    import synth
+    w = synth.scaled(synth.workload(name), rows_div=200, bags_div=16, name=f"{name}-small")
+    b = synth.make_batch(w, 3)
+    keys = np.unique((w.row_offset[np.repeat(np.arange(w.num_bags), np.diff(b.offsets)) // w.bags_per_table]
+                      + b.indices).astype(np.uint32))
+    results = []
+    try:
+        for threads in (1, 8):
+            oracle.set_threads(threads)
+            assert oracle.get_threads() == threads
+            store = oracle.RowStore(synth.weight_rows(w, keys), keys=keys,
+                                    state=np.zeros(len(keys), np.float32) if w.opt == "adagrad" else None)
+            out, dd, gr = oracle.step(w.num_tables, w.row_offset, w.bags_per_table, b.offsets, b.indices, b.grad,
+                                      store, w.pool, w.opt, w.lr, w.eps, rounding, 11)
+            results.append((out, dd, gr, store))
+    finally:
+        oracle.set_threads(0)
+    (o1, d1, g1, s1), (o8, d8, g8, s8) = results
+    np.testing.assert_array_equal(o1, o8)
+    for f in ("unique_keys", "counts", "seg_offsets", "perm"):
+        np.testing.assert_array_equal(getattr(d1, f), getattr(d8, f))
+    np.testing.assert_array_equal(g1, g8)
+    np.testing.assert_array_equal(s1.vals, s8.vals)
+    if s1.state is not None:
+        np.testing.assert_array_equal(s1.state, s8.state)

@@ -18,8 +18,8 @@ GOLDEN = os.path.join(ROOT, "tests", "golden")
 MUTANTS = {
     "fwd_sign": ("acc[d] += store_get(&s, store_vals, slot, d);", "acc[d] -= store_get(&s, store_vals, slot, d);"),
     "fwd_drop_mean": ("if (pool == 1 && L > 0) v = v / (double)L;", "if (pool == 2 && L > 0) v = v / (double)L;"),
-    "fwd_skip_last": ("for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {\n      int64_t slot",
-                      "for (int32_t j = offsets[m]; j + 1 < offsets[m + 1]; ++j) {\n      int64_t slot"),
+    "fwd_skip_last": ("for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {\n        int64_t slot",
+                      "for (int32_t j = offsets[m]; j + 1 < offsets[m + 1]; ++j) {\n        int64_t slot"),
     "key_no_table_offset": ("a[j].key = (uint32_t)(row_offset[m / B] + idx[j]);", "a[j].key = (uint32_t)(idx[j]);"),
     "unstable_ties": ("return (x->pos > y->pos) - (x->pos < y->pos);", "return (x->pos < y->pos) - (x->pos > y->pos);"),
     "grad_transposed": ("sum[d] += scale * (double)G[(int64_t)m * D + d];",
@@ -52,8 +52,8 @@ def _build_mutant(tmp_path, name):
     path = tmp_path / f"oracle_{name}.c"
     path.write_text(src.replace(old, new))
     so = tmp_path / f"liboracle_{name}.so"
-    subprocess.check_call(["gcc", "-O1", "-fPIC", "-shared", "-ffp-contract=off", "-std=c11", str(path), "-o",
-                           str(so), "-lm"])
+    subprocess.check_call(["gcc", "-O1", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-std=c11", str(path),
+                           "-o", str(so), "-lm"])
     return str(so)
 
 
@@ -84,6 +84,7 @@ def _run_pins(so_path):
             lambda: T.test_route_matches_numpy(8, 2),
             lambda: T.test_route_fragments_reassemble_the_forward("sum", False),
             lambda: T.test_sr_bits_match_the_input_generators_splitmix64(),
+            lambda: T.test_sr_bits_known_answers_of_splitmix64(),
             lambda: T.test_bf16_stochastic_rounding_is_exactly_unbiased_over_all_random_bits(),
         ]
         for p in pins:
@@ -98,8 +99,8 @@ def _run_pins(so_path):
 
 def test_unmutated_copy_passes(tmp_path):
     so = tmp_path / "liboracle_same.so"
-    subprocess.check_call(["gcc", "-O1", "-fPIC", "-shared", "-ffp-contract=off", "-std=c11", SRC, "-o", str(so),
-                           "-lm"])
+    subprocess.check_call(["gcc", "-O1", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-std=c11", SRC, "-o",
+                           str(so), "-lm"])
     assert _run_pins(str(so))
 
 

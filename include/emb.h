@@ -194,6 +194,22 @@ emb_status emb_route_ids(const emb_tables* tables, const emb_batch* batch, int32
                          const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids, int32_t* send_pos,
                          int32_t* send_bag, void* ws, size_t ws_bytes, void* stream);
 
+/* emb_route_ids for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same outputs, bit for bit, with the per-block owner counts kept in a
+ * scratch array inside the library instead of a workspace argument.  The
+ * array holds EMB_ROUTE_SCRATCH_BYTES (4 MiB) on every GPU the library runs
+ * on, for the life of the process; a batch for which
+ * emb_route_workspace_size(N, M, world_size) exceeds it is rejected with
+ * EMB_EUNSUPPORTED before anything is enqueued.  The call allocates nothing;
+ * all calls on one GPU share that GPU's array, so calls that overlap in time
+ * on one GPU (different streams without ordering) race on it.  Nothing in the
+ * array needs clearing: every call writes each entry it reads. */
+#define EMB_ROUTE_SCRATCH_BYTES (4u << 20)
+emb_status emb_route_ids_noalloc(const emb_tables* tables, const emb_batch* batch, int32_t world_size,
+                                 const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids,
+                                 int32_t* send_pos, int32_t* send_bag, void* stream);
+
 /* Debug check of device contents (never on the timed path): flag[0] (device
  * int32) is set to 0 if the batch is well formed, else to a bitwise OR of
  * 1 (offsets[0] != 0), 2 (decreasing offsets), 4 (offsets[M] != N),

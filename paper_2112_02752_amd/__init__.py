@@ -27,7 +27,7 @@ DTYPE = {"fp32": FP32, "bf16": BF16}
 
 EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_grad_reduce",
             "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_workspace_status",
-            "emb_status_string", "emb_route_workspace_size", "emb_route_ids")
+            "emb_status_string", "emb_route_workspace_size", "emb_route_ids", "emb_route_ids_noalloc")
 
 
 class EmbError(RuntimeError):
@@ -111,6 +111,8 @@ def lib():
         L.emb_route_workspace_size.argtypes = [i64, i64, i32]
         L.emb_route_ids.restype = i32
         L.emb_route_ids.argtypes = [T, B, i32, ctypes.POINTER(ctypes.c_int64), vp, vp, vp, vp, vp, sz, vp]
+        L.emb_route_ids_noalloc.restype = i32
+        L.emb_route_ids_noalloc.argtypes = [T, B, i32, ctypes.POINTER(ctypes.c_int64), vp, vp, vp, vp, vp]
         L.emb_validate_batch.restype = i32
         L.emb_validate_batch.argtypes = [T, B, vp, vp]
         L.emb_workspace_error_offset.restype = sz
@@ -247,6 +249,20 @@ def route_ids(tables: Tables, batch: Batch, shard_start: Sequence[int], send_cou
     _check("emb_route_ids", lib().emb_route_ids(
         ctypes.byref(tables.c()), ctypes.byref(batch.c()), W, ss, _ptr(send_counts), _ptr(send_ids), _ptr(send_pos),
         _ptr(send_bag), _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+
+
+def route_ids_noalloc(tables: Tables, batch: Batch, shard_start: Sequence[int], send_counts, send_ids, send_pos,
+                      send_bag, stream=None) -> None:
+    """route_ids without a workspace (the library's per-device scratch array
+    holds the per-block counts); for callers that cannot allocate."""
+    W = len(shard_start) - 1
+    ss = (ctypes.c_int64 * len(shard_start))(*[int(x) for x in shard_start])
+    _check("emb_route_ids_noalloc", lib().emb_route_ids_noalloc(
+        ctypes.byref(tables.c()), ctypes.byref(batch.c()), W, ss, _ptr(send_counts), _ptr(send_ids), _ptr(send_pos),
+        _ptr(send_bag), _stream(stream)))
+
+
+ROUTE_SCRATCH_BYTES = 4 << 20
 
 
 def workspace_error_offset() -> int:

@@ -69,6 +69,45 @@ emb_status check_update(const emb_update* u) {
 
 emb_status hip_status(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; }
 
+// host checks of a routing call; fills the launch descriptor (ws left null)
+emb_status route_prepare(const emb_tables* tables, const emb_batch* batch, int32_t world_size,
+                         const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids, int32_t* send_pos,
+                         int32_t* send_bag, RouteLaunch* p) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  st = check_batch(batch, tables->num_tables, &M);
+  if (st != EMB_OK) return st;
+  if (world_size < 1 || world_size > kMaxRanks || shard_start == nullptr || send_counts == nullptr) return EMB_EINVAL;
+  if (shard_start[0] != 0 || shard_start[world_size] != R) return EMB_EINVAL;
+  ShardBounds sb;
+  for (int r = 0; r < world_size; ++r) {
+    if (shard_start[r + 1] < shard_start[r]) return EMB_EINVAL;
+    sb.off[r] = (uint32_t)shard_start[r];
+  }
+  sb.off[world_size] = (uint32_t)R;
+  const int64_t N = batch->num_indices;
+  if (N > 0 && (send_ids == nullptr || send_pos == nullptr || send_bag == nullptr)) return EMB_EINVAL;
+  *p = RouteLaunch{};
+  p->offsets = batch->offsets;
+  p->idx = batch->indices;
+  p->idx64 = batch->index_bytes == 8;
+  p->ro = ro;
+  p->sb = sb;
+  p->B = batch->bags_per_table;
+  p->M = M;
+  p->W = world_size;
+  p->N = N;
+  p->send_counts = send_counts;
+  p->send_ids = send_ids;
+  p->send_pos = send_pos;
+  p->send_bag = send_bag;
+  return EMB_OK;
+}
+
+
 }  // namespace
 
 extern "C" {
@@ -256,41 +295,23 @@ size_t emb_route_workspace_size(int64_t num_indices, int64_t num_bags, int32_t w
 emb_status emb_route_ids(const emb_tables* tables, const emb_batch* batch, int32_t world_size,
                          const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids, int32_t* send_pos,
                          int32_t* send_bag, void* ws, size_t ws_bytes, void* stream) {
-  TableOffsets ro;
-  int64_t R = 0;
-  emb_status st = check_tables(tables, &ro, &R);
+  RouteLaunch p;
+  emb_status st = route_prepare(tables, batch, world_size, shard_start, send_counts, send_ids, send_pos, send_bag, &p);
   if (st != EMB_OK) return st;
-  int32_t M = 0;
-  st = check_batch(batch, tables->num_tables, &M);
-  if (st != EMB_OK) return st;
-  if (world_size < 1 || world_size > kMaxRanks || shard_start == nullptr || send_counts == nullptr) return EMB_EINVAL;
-  if (shard_start[0] != 0 || shard_start[world_size] != R) return EMB_EINVAL;
-  ShardBounds sb;
-  for (int r = 0; r < world_size; ++r) {
-    if (shard_start[r + 1] < shard_start[r]) return EMB_EINVAL;
-    sb.off[r] = (uint32_t)shard_start[r];
-  }
-  sb.off[world_size] = (uint32_t)R;
-  const int64_t N = batch->num_indices;
-  if (N > 0 && (send_ids == nullptr || send_pos == nullptr || send_bag == nullptr || ws == nullptr))
-    return EMB_EINVAL;
-  if (ws_bytes < emb_route_workspace_size(N, M, world_size)) return EMB_EWORKSPACE;
-  RouteLaunch p{};
-  p.offsets = batch->offsets;
-  p.idx = batch->indices;
-  p.idx64 = batch->index_bytes == 8;
-  p.ro = ro;
-  p.sb = sb;
-  p.B = batch->bags_per_table;
-  p.M = M;
-  p.W = world_size;
-  p.N = N;
+  if (p.N > 0 && ws == nullptr) return EMB_EINVAL;
+  if (ws_bytes < emb_route_workspace_size(p.N, p.M, world_size)) return EMB_EWORKSPACE;
   p.ws = ws;
-  p.send_counts = send_counts;
-  p.send_ids = send_ids;
-  p.send_pos = send_pos;
-  p.send_bag = send_bag;
   return hip_status(launch_route(p, (hipStream_t)stream));
+}
+
+emb_status emb_route_ids_noalloc(const emb_tables* tables, const emb_batch* batch, int32_t world_size,
+                                 const int64_t* shard_start, int32_t* send_counts, int32_t* send_ids,
+                                 int32_t* send_pos, int32_t* send_bag, void* stream) {
+  RouteLaunch p;
+  emb_status st = route_prepare(tables, batch, world_size, shard_start, send_counts, send_ids, send_pos, send_bag, &p);
+  if (st != EMB_OK) return st;
+  if (!route_fits_scratch(p.N, p.M, world_size)) return EMB_EUNSUPPORTED;
+  return hip_status(launch_route_noalloc(p, (hipStream_t)stream));
 }
 
 emb_status emb_validate_batch(const emb_tables* tables, const emb_batch* batch, int32_t* flag, void* stream) {

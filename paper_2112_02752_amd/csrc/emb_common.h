@@ -172,6 +172,10 @@ struct ShardBounds {
   uint32_t off[kMaxRanks + 1];
 };
 constexpr int kRouteBags = 1024;
+// owner counts the allocation-free routing entry point can hold (4 MiB), and
+// the devices it keeps a scratch address for
+constexpr size_t kRouteScratchInts = (size_t)1 << 20;
+constexpr int kMaxDevices = 64;
 constexpr int kRoutePositions = 256;
 constexpr int kRouteScanThreads = 1024;
 

@@ -103,6 +103,10 @@ struct RouteLaunch {
   int32_t* send_bag;
 };
 hipError_t launch_route(const RouteLaunch& p, hipStream_t s);
+// the same on the library's per-device scratch array (p.ws is ignored);
+// route_fits_scratch says whether a batch's per-block counts fit it
+hipError_t launch_route_noalloc(RouteLaunch p, hipStream_t s);
+bool route_fits_scratch(int64_t N, int64_t M, int32_t W);
 
 struct ValidateLaunch {
   const int32_t* offsets;

@@ -10,12 +10,42 @@
 // one wavefront over a range of consecutive bags, whose positions are
 // consecutive too; their offsets are staged in LDS, so a position's bag is an
 // LDS binary search and the stable rank among equal owners a few ballots.
+#include <mutex>
+
 #include "emb_common.h"
 #include "kernels.h"
 
 namespace emb {
 
 namespace {
+
+// Per-block owner counts of emb_route_ids_noalloc, for callers that cannot
+// allocate: a device array that every call on a GPU shares (each GPU holds its
+// own copy for the life of the process).  The count kernel writes every entry
+// a call reads, so nothing in it needs clearing; calls that overlap on one GPU
+// race on it.
+static __device__ __align__(256) int32_t scratch[kRouteScratchInts];
+
+// device address of this GPU's copy of `scratch`, found once per device with
+// that device current (the host-side name `scratch` is not a device address)
+std::mutex g_scratch_mu;
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t scratch_for_current_device(int32_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 struct RouteArgs {
   const int32_t* offsets;
@@ -166,6 +196,19 @@ RoutePlan route_plan(int64_t N, int64_t M) {
   p.bags_per_block = (int32_t)(want < 1 ? 1 : (want > kRouteBags ? kRouteBags : want));
   p.nblocks = M > 0 ? (int32_t)((M + p.bags_per_block - 1) / p.bags_per_block) : 0;
   return p;
+}
+
+bool route_fits_scratch(int64_t N, int64_t M, int32_t W) {
+  const RoutePlan plan = route_plan(N, M);
+  return (int64_t)W * (int64_t)(plan.nblocks > 0 ? plan.nblocks : 1) <= (int64_t)kRouteScratchInts;
+}
+
+hipError_t launch_route_noalloc(RouteLaunch p, hipStream_t s) {
+  int32_t* ptr = nullptr;
+  const hipError_t e = scratch_for_current_device(&ptr);
+  if (e != hipSuccess) return e;
+  p.ws = ptr;
+  return launch_route(p, s);
 }
 
 hipError_t launch_route(const RouteLaunch& p, hipStream_t s) {

@@ -22,8 +22,12 @@
  * Conventions shared by every entry point:
  *  - Pointers are DEVICE pointers unless marked "host".  The caller
  *    allocates and frees every buffer, including the workspace; the library
- *    allocates no memory, keeps no pointer after returning and holds no state
- *    between calls apart from its loaded code.
+ *    allocates no memory (emb_route_ids_noalloc's scratch array is part of
+ *    its loaded code) and keeps no pointer after returning.  The state
+ *    carried from call to call lives in the caller's dedup workspace: its
+ *    header (call generation, per-call error word) must be zeroed once by
+ *    emb_workspace_init, and its coordination words are tagged by call, so
+ *    they never need clearing again.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Every call only enqueues work on it; nothing synchronises.  Buffers must
  *    stay alive until the stream has reached the enqueued work.
@@ -109,24 +113,32 @@ typedef struct {
   uint64_t seed;
 } emb_update;
 
-/* Forward: out[m][d] = scale_m * sum over bag m of W[key(j)][d], fp32
- * accumulation (bf16 rows are widened exactly).  out: device fp32 [M][D],
- * fully overwritten (empty bags get zeros).  The layer's forward as defined
- * above (paper: Introduction, the sparse-ids-to-dense-features layer). */
+/* Forward (the pull of the embedding stage): out[m][d] = scale_m * sum over
+ * bag m of W[key(j)][d], fp32 accumulation (bf16 rows are widened exactly).
+ * out: device fp32 [M][D], fully overwritten (empty bags get zeros).  The
+ * layer's forward as defined above (paper: Introduction, the layer that turns
+ * sparse ids into dense features at a high data-access cost; Section
+ * "Multi-mode Execution", heterogeneous pipeline paragraph). */
 emb_status emb_pool_fwd(const emb_tables* tables, const emb_batch* batch, int32_t pool, float* out,
                         void* stream);
 
 /* Bytes of workspace that emb_unique_ids / emb_grad_reduce need for batches
- * of up to num_indices ids and num_bags bags, rows of dim floats.  Returns 0
- * for invalid sizes. */
+ * of up to num_indices ids (N < 2^30: published counts and offsets keep 30
+ * bits) and num_bags bags, rows of dim floats.  The size does not depend on
+ * the tables' row count.  Returns 0 for invalid sizes. */
 size_t emb_workspace_size(int64_t num_indices, int64_t num_bags, int32_t dim);
 
 /* Zero-fill a freshly allocated workspace (enqueued on stream).  Must run once
- * before the workspace's first use; every later call leaves the workspace's
- * internal counters back at their initial values when its work completes. */
+ * before the workspace's first use: it zeroes the header that carries each
+ * call's generation and error record; later calls need no clearing (their
+ * coordination words are tagged by call, and the counters they use are
+ * cleared by the kernel that uses them). */
 emb_status emb_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
-/* Dedup of the batch's ids, the step that makes the sparse update race-free:
+/* Dedup of the batch's ids, the step that makes the sparse update (the push
+ * of the embedding stage, paper: Section "Multi-mode Execution",
+ * heterogeneous pipeline paragraph) race-free: every touched row gets
+ * exactly one owner.
  *   key[j]          = row_offset[t(j)] + indices[j]   (uint32)
  *   sort_perm       = the stable ascending sort of positions 0..N-1 by key
  *                     (equal keys keep position order), device int32 [N]
@@ -142,7 +154,9 @@ emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint
                           int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
                           void* stream);
 
-/* Backward segment-reduce, optionally fused with the optimizer step:
+/* Backward segment-reduce (the gradient the embedding stage pushes back,
+ * paper: Section "Multi-mode Execution", heterogeneous pipeline paragraph),
+ * optionally fused with the optimizer step:
  *   g_u[d] = sum over sorted positions k in segment u of scale_{m(k)} * grad_out[m(k)][d],
  * m(k) the bag holding position sort_perm[k], in a fixed order per segment
  * (deterministic, no float atomics).  grad_out: device fp32 [M][D].
@@ -157,7 +171,9 @@ emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int
                            const int32_t* num_unique, float* grad_rows, const emb_update* fuse, void* ws,
                            size_t ws_bytes, void* stream);
 
-/* Unfused optimizer step: for u < num_unique[0], row r = unique_keys[u] gets
+/* Unfused optimizer step (the push of the sparse update to the touched rows,
+ * paper: Section "Multi-mode Execution", heterogeneous pipeline paragraph):
+ * for u < num_unique[0], row r = unique_keys[u] gets
  * opt(W_r, grad_rows[u]) as defined for emb_update.  max_unique (host) bounds
  * num_unique[0] (the batch's N is a valid bound).  unique_keys must be
  * distinct (one owner per row). */

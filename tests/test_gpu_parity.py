@@ -282,8 +282,9 @@ def test_workload_full_size_one_step(name):
 def test_sort_tile_modes(rows_div, bags, concurrent):
     """Batches of the 50M-row workload's shape whose sizes select each sort
     mode: co-resident passes with 2048-, 2560- and 4096-key tiles (at most
-    one block per compute unit) and the ticket look-back beyond that, for
-    26-bit keys (three passes) and 20-bit keys (rows / 50: two passes)."""
+    one block per compute unit) and reduce-then-scan passes (tile counts and
+    a column scan before each pass) beyond that, for 26-bit keys (three
+    passes) and 20-bit keys (rows / 50: two passes)."""
     import dataclasses
     w = dataclasses.replace(synth.scaled(synth.workload("c3"), rows_div=rows_div), bags_per_table=bags,
                             name=f"c3/r{rows_div}-b{bags}")

@@ -359,6 +359,7 @@ int oracle_route_ids(int32_t T, const int64_t* row_offset, int32_t B, const int3
   for (int32_t r = 0; r < W; ++r)
     if (shard_start[r + 1] < shard_start[r]) return ORC_BAD_ARG;
   int64_t M = (int64_t)T * B;
+  int64_t N = offsets[M];
   int64_t k = 0;
   for (int32_t r = 0; r < W; ++r) {
     send_counts[r] = 0;
@@ -366,6 +367,7 @@ int oracle_route_ids(int32_t T, const int64_t* row_offset, int32_t B, const int3
       for (int32_t j = offsets[m]; j < offsets[m + 1]; ++j) {
         int64_t key = row_offset[m / B] + idx[j];
         if (key < shard_start[r] || key >= shard_start[r + 1]) continue;
+        if (k >= N) return ORC_BAD_ARG; /* every position has one owner: N entries in all */
         send_ids[k] = (int32_t)(key - shard_start[r]);
         send_pos[k] = j;
         send_bag[k] = (int32_t)m;

@@ -54,12 +54,15 @@ def parse():
     ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
                     help="optimizer instead of the workload's own (adagrad_ew: element-wise, state [R][D])")
     ap.add_argument("--schedule", choices=("pipelined", "auto", "serial", "concurrent"), default="pipelined",
-                    help="pipelined: the dedups of the next group of batches on a side stream while the main "
+                    help="pipelined: the dedups of the next group of batches on side streams while the main "
                          "stream runs the forward and update of the current group; concurrent: the forward of a "
                          "batch on a side stream at the same time as its id dedup; serial: forward, dedup, "
                          "reduce + update one after another on one stream; auto: concurrent for batches of at "
                          "least a million lookups, else serial")
-    ap.add_argument("--group", type=int, default=4, help="batches per group of the pipelined schedule")
+    ap.add_argument("--group", type=int, default=6, help="batches per group of the pipelined schedule")
+    ap.add_argument("--side-streams", type=int, default=3,
+                    help="side streams of the pipelined schedule (more than one: the dedups of a group run "
+                         "concurrently with emb_unique_ids_concurrent)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
@@ -275,7 +278,7 @@ def main():
                 clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
     elif args.schedule == "pipelined":
         pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
-                            group=args.group)
+                            group=args.group, side_streams=args.side_streams)
 
         def run_steps(lo, hi):
             pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in range(lo, hi)], sp)
@@ -469,6 +472,7 @@ def main():
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
                    "table_bytes": w.weight_bytes, "schedule": args.schedule,
                    "group": args.group if args.schedule == "pipelined" else None,
+                   "side_streams": args.side_streams if args.schedule == "pipelined" else None,
                    "overlapped_steps": args.steps if args.schedule == "pipelined" else
                    sum(1 for i in range(args.warmup, total)
                        if clayer is not None and clayer.overlaps(dev_batches[i][2]))},

@@ -154,6 +154,19 @@ emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint
                           int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
                           void* stream);
 
+/* emb_unique_ids with the same outputs, bit for bit, from kernels in which no
+ * workgroup ever waits for another (the sort's passes each preceded by their
+ * tile counts and a column scan, the unique scan preceded by its tile counts
+ * and their scan).  emb_unique_ids may make the workgroups of a pass wait for
+ * one another when they all fit the device at once, so at most one such call
+ * may be in flight on a device; any number of these may run concurrently, on
+ * any streams, beside any other work (each with its own outputs and
+ * workspace).  Slower alone; used to run the dedups of several upcoming
+ * batches at once beside the forward and update of the current ones. */
+emb_status emb_unique_ids_concurrent(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys,
+                                     int32_t* counts, int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique,
+                                     void* ws, size_t ws_bytes, void* stream);
+
 /* Backward segment-reduce (the gradient the embedding stage pushes back,
  * paper: Section "Multi-mode Execution", heterogeneous pipeline paragraph),
  * optionally fused with the optimizer step:

@@ -25,7 +25,8 @@ POOL = {"sum": 0, "mean": 1}
 OPT = {"sgd": 0, "adagrad": 1, "adagrad_ew": 2}
 DTYPE = {"fp32": FP32, "bf16": BF16}
 
-EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_grad_reduce",
+EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_unique_ids_concurrent",
+            "emb_grad_reduce",
             "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_workspace_status",
             "emb_status_string", "emb_route_workspace_size", "emb_route_ids", "emb_route_ids_noalloc")
 
@@ -103,6 +104,8 @@ def lib():
         L.emb_workspace_init.argtypes = [vp, sz, vp]
         L.emb_unique_ids.restype = i32
         L.emb_unique_ids.argtypes = [T, B, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.emb_unique_ids_concurrent.restype = i32
+        L.emb_unique_ids_concurrent.argtypes = [T, B, vp, vp, vp, vp, vp, vp, sz, vp]
         L.emb_grad_reduce.restype = i32
         L.emb_grad_reduce.argtypes = [T, B, i32, vp, vp, vp, vp, vp, vp, Up, vp, sz, vp]
         L.emb_sparse_update.restype = i32
@@ -203,8 +206,11 @@ def pool_fwd(tables: Tables, batch: Batch, pool: str, out, stream=None) -> None:
 
 
 def unique_ids(tables: Tables, batch: Batch, unique_keys, counts, seg_offsets, sort_perm, num_unique, ws,
-               stream=None) -> None:
-    _check("emb_unique_ids", lib().emb_unique_ids(
+               stream=None, concurrent: bool = False) -> None:
+    """The batch's dedup; ``concurrent`` selects emb_unique_ids_concurrent
+    (no workgroup waits for another; any number may be in flight at once)."""
+    fn = "emb_unique_ids_concurrent" if concurrent else "emb_unique_ids"
+    _check(fn, getattr(lib(), fn)(
         ctypes.byref(tables.c()), ctypes.byref(batch.c()), _ptr(unique_keys), _ptr(counts), _ptr(seg_offsets),
         _ptr(sort_perm), _ptr(num_unique), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
@@ -496,42 +502,48 @@ class _Hip:
 
 class Pipeline:
     """Training steps of the layer with the id dedups of the next group of
-    batches running on a side stream while the main stream runs the forward
+    batches running on side streams while the main stream runs the forward
     and the fused update of the current group.
 
     The dedup reads only a batch's ids and offsets, never the table, so
     running it ahead changes no result: every forward still follows the
     previous update on the main stream, and tables, state and pooled outputs
-    equal those of serial steps bit for bit.  The dedups are serialised on
-    the side stream, so at most one runs at a time, next to forward and
-    reduce kernels that never wait for other workgroups: every workgroup of a
-    sort pass is dispatched once the main stream's workgroups retire, which
-    they do without waiting on the dedup.  Two sets of ``group`` dedup
-    buffers alternate; the side stream overwrites a set only after the main
-    stream's group that read it, so each direction takes one cross-stream
-    wait per group (each costs the host 15-25 us on ROCm when the event is
-    still pending, hence groups rather than single steps).
+    equal those of serial steps bit for bit.  With one side stream the dedups
+    run one after another with emb_unique_ids (whose sort may make the
+    workgroups of a pass wait for one another, which is safe with one dedup
+    in flight next to kernels that never wait).  With several side streams the
+    dedups of a group are dealt round-robin over them and run concurrently
+    with emb_unique_ids_concurrent, in which no workgroup waits for another.
+    Two sets of ``group`` dedup buffers alternate; the side streams overwrite
+    a set only after the main stream's group that read it, so each group
+    costs one cross-stream wait per stream and direction (each costs the host
+    15-25 us on ROCm while its event is pending, hence groups rather than
+    single steps).
 
     This is the paper's embedding stage run ahead of the dense stage
     (Section "Multi-mode Execution", heterogeneous pipeline) with no
     staleness: only the dedup, which the table never feeds, runs early."""
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0, group: int = 4, rounding: str = "nearest", seed: int = 0):
+                 max_indices: int = 0, max_bags: int = 0, group: int = 6, side_streams: int = 3,
+                 rounding: str = "nearest", seed: int = 0):
         import torch
-        if group < 1:
-            raise ValueError("group must be >= 1")
+        if group < 1 or side_streams < 1:
+            raise ValueError("group and side_streams must be >= 1")
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
         dev = tables.weights.device
         D = int(tables.weights.shape[1])
-        self.K = group
+        self.K, self.S = group, min(side_streams, group)
         self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(2 * group)]
         self.max_indices = max(1, max_indices)
-        self._side_stream = torch.cuda.Stream(device=dev)
-        self.side = int(self._side_stream.cuda_stream)
+        self._side_streams = [torch.cuda.Stream(device=dev) for _ in range(self.S)]
+        self.sides = [int(x.cuda_stream) for x in self._side_streams]
         self._ev_start = _Hip.event()
-        self._ev_side = [_Hip.event(), _Hip.event()]   # a group's dedups are done (per set parity)
-        self._ev_main = [_Hip.event(), _Hip.event()]   # the main stream's group that read a set is done
+        # a group's dedups are done (per set parity and side stream); the main
+        # stream's group that read a set is done (per parity)
+        self._ev_side = [[_Hip.event() for _ in range(self.S)] for _ in range(2)]
+        self._ev_main = [_Hip.event(), _Hip.event()]
+        self._dedup_fn = "emb_unique_ids_concurrent" if self.S > 1 else "emb_unique_ids"
         self._status = torch.zeros(4, dtype=torch.int32, device=dev)
         self._ct = ctypes.byref(tables.c())
         self.rounding, self.seed, self.steps_done = rounding, seed, 0
@@ -544,7 +556,7 @@ class Pipeline:
     def __del__(self):
         try:
             L = _Hip.lib()
-            for e in [self._ev_start] + self._ev_side + self._ev_main:
+            for e in [self._ev_start] + self._ev_side[0] + self._ev_side[1] + self._ev_main:
                 L.hipEventDestroy(e)
         except Exception:
             pass
@@ -554,7 +566,7 @@ class Pipeline:
         ``steps``, in order, on ``stream`` (the forward of each batch into its
         ``out``, then its backward with ``grad_out`` and the optimizer step).
         Every step's results are complete when ``stream`` reaches the end of
-        the enqueued work; the side stream's work all precedes it."""
+        the enqueued work; the side streams' work all precedes it."""
         steps = list(steps)
         for b, _, _ in steps:
             if int(b.indices.numel()) > self.max_indices:
@@ -562,29 +574,34 @@ class Pipeline:
         if not steps:
             return
         L = lib()
+        dedup = getattr(L, self._dedup_fn)
         main = _stream(stream)
-        K = self.K
+        K, S = self.K, self.S
         ngroups = (len(steps) + K - 1) // K
-        # the side stream starts after everything already on the main stream
+        # the side streams start after everything already on the main stream
         _Hip.record(self._ev_start, main)
-        _Hip.wait(self.side, self._ev_start)
+        for sp in self.sides:
+            _Hip.wait(sp, self._ev_start)
 
         def dedups(g):
             par = g % 2
             for i, (b, _, _) in enumerate(steps[g * K:(g + 1) * K]):
                 uk, cnt, seg, perm, nu, ws, wsb = self._set_args[par * K + i]
-                _check("emb_unique_ids", L.emb_unique_ids(self._ct, ctypes.byref(b.c()), uk, cnt, seg, perm, nu, ws,
-                                                          wsb, self.side))
-            _Hip.record(self._ev_side[par], self.side)
+                _check(self._dedup_fn, dedup(self._ct, ctypes.byref(b.c()), uk, cnt, seg, perm, nu, ws, wsb,
+                                             self.sides[i % S]))
+            for s, sp in enumerate(self.sides):
+                _Hip.record(self._ev_side[par][s], sp)
 
         dedups(0)
         for g in range(ngroups):
             if g + 1 < ngroups:
                 if g >= 1:
                     # the sets of group g + 1 were read by the main stream's group g - 1
-                    _Hip.wait(self.side, self._ev_main[(g + 1) % 2])
+                    for sp in self.sides:
+                        _Hip.wait(sp, self._ev_main[(g + 1) % 2])
                 dedups(g + 1)
-            _Hip.wait(main, self._ev_side[g % 2])
+            for ev in self._ev_side[g % 2]:
+                _Hip.wait(main, ev)
             for i, (b, out, grad_out) in enumerate(steps[g * K:(g + 1) * K]):
                 uk, cnt, seg, perm, nu, ws, wsb = self._set_args[(g % 2) * K + i]
                 cb = ctypes.byref(b.c())

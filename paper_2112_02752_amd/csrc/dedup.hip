@@ -1164,6 +1164,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     return nd / (nd < kRangeDigits ? nd : kRangeDigits);
   };
   for (const int it : {kSortItemsCore, kSortItemsMid, kSortItemsWide}) {
+    if (p.waitfree) break;
     core_tiles = (N + kSortThreads * it - 1) / (kSortThreads * it);
     core_groups = (core_tiles + kPrefixGroup - 1) / kPrefixGroup;
     ranges = p.plan.passes > 1 ? 1 : 0;
@@ -1183,7 +1184,8 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   const int sort_cores = sort_it > 0 ? 1 : 0;
   const int tile_keys = kSortThreads * (sort_cores ? sort_it : kSortItemsWide);
   const int sort_tiles = (N + tile_keys - 1) / tile_keys;
-  const int uniq_cores = uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
+  const int uniq_cores =
+      !p.waitfree && uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
   uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
   hipError_t e = hipSuccess;
 

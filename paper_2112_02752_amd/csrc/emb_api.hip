@@ -169,9 +169,9 @@ emb_status emb_pool_fwd(const emb_tables* tables, const emb_batch* batch, int32_
   return hip_status(launch_pool_fwd(p, (hipStream_t)stream));
 }
 
-emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys, int32_t* counts,
-                          int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
-                          void* stream) {
+static emb_status unique_ids(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys, int32_t* counts,
+                             int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
+                             int32_t waitfree, void* stream) {
   TableOffsets ro;
   int64_t R = 0;
   emb_status st = check_tables(tables, &ro, &R);
@@ -203,7 +203,20 @@ emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint
   p.seg_offsets = seg_offsets;
   p.sort_perm = sort_perm;
   p.num_unique = num_unique;
+  p.waitfree = waitfree;
   return hip_status(launch_dedup(p, (hipStream_t)stream));
+}
+
+emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys, int32_t* counts,
+                          int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique, void* ws, size_t ws_bytes,
+                          void* stream) {
+  return unique_ids(tables, batch, unique_keys, counts, seg_offsets, sort_perm, num_unique, ws, ws_bytes, 0, stream);
+}
+
+emb_status emb_unique_ids_concurrent(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys,
+                                     int32_t* counts, int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique,
+                                     void* ws, size_t ws_bytes, void* stream) {
+  return unique_ids(tables, batch, unique_keys, counts, seg_offsets, sort_perm, num_unique, ws, ws_bytes, 1, stream);
 }
 
 emb_status emb_grad_reduce(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* grad_out,

@@ -42,6 +42,10 @@ struct DedupLaunch {
   int32_t* seg_offsets;
   int32_t* sort_perm;
   int32_t* num_unique;
+  // 1: only kernels in which no workgroup waits for another (reduce-then-scan
+  // sort passes and unique scan), so that any number of dedups may be in
+  // flight on a device at once
+  int32_t waitfree;
 };
 hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s);
 

@@ -647,13 +647,13 @@ def test_stale_schedule_matches_oracle_replay(name, concurrent):
     parity.check_rows(dl, store, touched, w.opt)
 
 
-@pytest.mark.parametrize("group,nsteps", [(1, 5), (2, 7), (4, 10)])
-def test_pipelined_schedule_equals_serial(group, nsteps):
+@pytest.mark.parametrize("group,sides,nsteps", [(1, 1, 5), (2, 1, 7), (4, 1, 10), (2, 2, 7), (6, 3, 13)])
+def test_pipelined_schedule_equals_serial(group, sides, nsteps):
     """The dedups of the next group of batches on a side stream while the main
     stream runs the forward and update of the current group change nothing:
     tables, state and pooled outputs equal those of serial steps bit for bit
     (step counts that leave a partial last group included)."""
-    _say(f"case pipelined vs serial group={group} steps={nsteps}")
+    _say(f"case pipelined vs serial group={group} side streams={sides} steps={nsteps}")
     import torch
     import paper_2112_02752_amd as emb
     w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
@@ -671,7 +671,7 @@ def test_pipelined_schedule_equals_serial(group, nsteps):
                 layer.step(b, out, g)
         else:
             pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
-                                max_bags=w.num_bags, group=group)
+                                max_bags=w.num_bags, group=group, side_streams=sides)
             # two runs: the second starts after everything the first enqueued
             half = nsteps // 2
             pipe.run([(b, o, g) for (b, g), o in zip(dev_b[:half], outs[:half])])
@@ -687,12 +687,13 @@ def test_pipelined_schedule_equals_serial(group, nsteps):
         np.testing.assert_array_equal(a, b)
 
 
-@pytest.mark.parametrize("name,nsteps,group", [("c3", 6, 4), ("c2", 3, 2)])
-def test_pipelined_schedule_full_size(name, nsteps, group):
+@pytest.mark.parametrize("name,nsteps,group,sides", [("c3", 6, 4, 1), ("c3", 13, 6, 3), ("c2", 3, 2, 1),
+                                                     ("c2", 5, 4, 2)])
+def test_pipelined_schedule_full_size(name, nsteps, group, sides):
     """Full-size pipelined steps against the oracle replaying the same steps on
     the rows they touch: every pooled output, the final rows and state, rows
     no step touched unchanged."""
-    _say(f"case pipelined full size {name} steps={nsteps} group={group}")
+    _say(f"case pipelined full size {name} steps={nsteps} group={group} side streams={sides}")
     import oracle
     import torch
     import paper_2112_02752_amd as emb
@@ -703,7 +704,7 @@ def test_pipelined_schedule_full_size(name, nsteps, group):
               torch.from_numpy(b.grad).cuda()) for b in batches]
     dl = parity.device_layer_from_workload(w)
     pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
-                        group=group)
+                        group=group, side_streams=sides)
     outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in dev_b]
     pipe.run([(b, o, g) for (b, g), o in zip(dev_b, outs)])
     torch.cuda.synchronize()
@@ -719,6 +720,61 @@ def test_pipelined_schedule_full_size(name, nsteps, group):
         assert r <= parity.TOL_FP32, f"pooled output of step {k}: rel err {r}"
     parity.check_rows(dl, store, touched, w.opt)
     parity.check_untouched(dl, w, touched)
+
+
+def _dedup_concurrent_vs_oracle(row_offset, B, off, idx, M):
+    import oracle
+    import torch
+    import paper_2112_02752_amd as emb
+    N = len(idx)
+    dev = "cuda"
+    tables = emb.Tables(torch.empty((1, 4), dtype=torch.float32, device=dev), [int(x) for x in row_offset])
+    b = emb.Batch(torch.from_numpy(np.ascontiguousarray(off, np.int32)).to(dev),
+                  torch.from_numpy(np.ascontiguousarray(idx, np.int32)).to(dev), B)
+    bufs = emb.DedupBuffers(dev, N, M, 4)
+    emb.unique_ids(tables, b, bufs.unique_keys, bufs.counts, bufs.seg_offsets, bufs.sort_perm, bufs.num_unique,
+                   bufs.ws, concurrent=True)
+    torch.cuda.synchronize()
+    assert emb.read_status(bufs.ws)[0] == 0
+    ref = oracle.unique_ids(len(row_offset) - 1, np.asarray(row_offset, np.int64), B,
+                            np.ascontiguousarray(off, np.int32), np.ascontiguousarray(idx, np.int32))
+    U = int(bufs.num_unique.cpu().item())
+    assert U == ref.num_unique
+    np.testing.assert_array_equal(bufs.unique_keys[:U].cpu().numpy().view(np.uint32), ref.unique_keys)
+    np.testing.assert_array_equal(bufs.counts[:U].cpu().numpy(), ref.counts)
+    np.testing.assert_array_equal(bufs.seg_offsets[:U + 1].cpu().numpy(), ref.seg_offsets)
+    np.testing.assert_array_equal(bufs.sort_perm[:N].cpu().numpy(), ref.perm)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c5"])
+def test_unique_ids_concurrent_full_size(name):
+    """emb_unique_ids_concurrent (no workgroup waits for another) gives the
+    oracle's dedup bit for bit at full size."""
+    w = synth.workload(name)
+    b = synth.make_batch(w, 2, with_grad=False)
+    _say(f"case unique_ids_concurrent {name} N={len(b.indices)}")
+    _dedup_concurrent_vs_oracle(w.row_offset, w.bags_per_table, b.offsets, b.indices, w.num_bags)
+
+
+@pytest.mark.parametrize("case", ["empty", "one", "same", "tables"])
+def test_unique_ids_concurrent_edge_cases(case):
+    rng = np.random.default_rng(5)
+    if case == "empty":
+        rows, B = [100], 8
+        off, idx = np.zeros(B + 1, np.int32), np.zeros(0, np.int32)
+    elif case == "one":
+        rows, B = [1000], 1
+        off, idx = np.array([0, 1], np.int32), np.array([999], np.int32)
+    elif case == "same":
+        rows, B = [1 << 20], 2000
+        lens = rng.integers(1, 60, size=B)
+        off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        idx = np.full(int(off[-1]), 123457, np.int32)
+    else:
+        rows, B = [37, 100_000, 1, 5_000_000], 3000
+        off, idx = _rand_batch(rng, rows, B, 40, empty_frac=0.1, zipf=1.3)
+    _say(f"case unique_ids_concurrent edge {case}")
+    _dedup_concurrent_vs_oracle(_row_offset(rows), B, off, idx, len(rows) * B)
 
 
 # ------------------------------------------------------------------ routing

@@ -27,7 +27,11 @@
  *    carried from call to call lives in the caller's dedup workspace: its
  *    header (call generation, per-call error word) must be zeroed once by
  *    emb_workspace_init, and its coordination words are tagged by call, so
- *    they never need clearing again.
+ *    they never need clearing again.  The regions of a workspace are placed
+ *    by its size and the tables' dim, not by the batch, so every call on a
+ *    workspace must pass the same ws_bytes and tables of the same dim (after
+ *    a change of either, run emb_workspace_init again); batches of any size
+ *    up to the one it was sized for may then follow each other in any order.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Every call only enqueues work on it; nothing synchronises.  Buffers must
  *    stay alive until the stream has reached the enqueued work.
@@ -166,6 +170,48 @@ emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint
 emb_status emb_unique_ids_concurrent(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys,
                                      int32_t* counts, int32_t* seg_offsets, int32_t* sort_perm, int32_t* num_unique,
                                      void* ws, size_t ws_bytes, void* stream);
+
+/* The buffers of one dedup: emb_unique_ids outputs and workspace (device
+ * pointers; ws_bytes >= emb_workspace_size of the largest batch, the
+ * workspace initialised by emb_workspace_init). */
+typedef struct {
+  uint32_t* unique_keys; /* [>= N] */
+  int32_t* counts;       /* [>= N] */
+  int32_t* seg_offsets;  /* [>= N + 1] */
+  int32_t* sort_perm;    /* [>= N] */
+  int32_t* num_unique;   /* [1] */
+  void* ws;
+  size_t ws_bytes;
+} emb_dedup_set;
+
+/* n_steps training steps of the layer enqueued with the pipelined schedule:
+ * step k pools batches[k] into outs[k] (device fp32 [M][D]) and applies the
+ * fused backward and optimizer step with grads[k] (device fp32 [M][D]), in
+ * order, on main_stream, exactly as emb_pool_fwd, emb_unique_ids and
+ * emb_grad_reduce one after another would, bit for bit.  The dedups of each
+ * next group of `group` batches run early on the n_side side streams (dealt
+ * round-robin), since the dedup never reads the table: the dedup of step k
+ * overlaps the forward and update of the steps before it -- the paper's
+ * embedding stage run ahead within its pipeline (Section "Multi-mode
+ * Execution", heterogeneous pipeline paragraph), here with no staleness.
+ * With n_side = 1 the dedups are emb_unique_ids, one at a time; with
+ * n_side > 1 they are emb_unique_ids_concurrent (no workgroup waits for
+ * another), several at a time.
+ *   sets:    host [2 * group] buffer sets, used alternately by groups
+ *   events:  host [3 + 2 * n_side] hipEvent_t created by the caller (no
+ *            timing needed); the library only records and waits on them
+ *   update:  the optimizer; step k uses update->seed + k for bf16
+ *            stochastic rounding
+ * All of the side streams' work precedes the end of the work enqueued on
+ * main_stream, so one synchronisation of main_stream completes every step.
+ * The side streams must differ from main_stream; calls that share sets,
+ * events or side streams must be ordered.  Host-checkable errors return
+ * before anything is enqueued; an error of a later step (a batch larger than
+ * the sets' buffers) returns with the earlier steps enqueued. */
+emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_update* update, int32_t n_steps,
+                              const emb_batch* batches, float* const* outs, const float* const* grads,
+                              int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,
+                              void* const* side_streams, void* const* events);
 
 /* Backward segment-reduce (the gradient the embedding stage pushes back,
  * paper: Section "Multi-mode Execution", heterogeneous pipeline paragraph),

@@ -28,7 +28,8 @@ DTYPE = {"fp32": FP32, "bf16": BF16}
 EXPORTED = ("emb_pool_fwd", "emb_workspace_size", "emb_workspace_init", "emb_unique_ids", "emb_unique_ids_concurrent",
             "emb_grad_reduce",
             "emb_sparse_update", "emb_validate_batch", "emb_workspace_error_offset", "emb_workspace_status",
-            "emb_status_string", "emb_route_workspace_size", "emb_route_ids", "emb_route_ids_noalloc")
+            "emb_status_string", "emb_route_workspace_size", "emb_route_ids", "emb_route_ids_noalloc",
+            "emb_pipeline_steps")
 
 
 class EmbError(RuntimeError):
@@ -83,6 +84,12 @@ class CUpdate(ctypes.Structure):
 ROUNDING = {"nearest": 0, "stochastic": 1}
 
 
+class CDedupSet(ctypes.Structure):
+    _fields_ = [("unique_keys", ctypes.c_void_p), ("counts", ctypes.c_void_p), ("seg_offsets", ctypes.c_void_p),
+                ("sort_perm", ctypes.c_void_p), ("num_unique", ctypes.c_void_p), ("ws", ctypes.c_void_p),
+                ("ws_bytes", ctypes.c_size_t)]
+
+
 _lib = None
 
 
@@ -114,6 +121,9 @@ def lib():
         L.emb_route_workspace_size.argtypes = [i64, i64, i32]
         L.emb_route_ids.restype = i32
         L.emb_route_ids.argtypes = [T, B, i32, ctypes.POINTER(ctypes.c_int64), vp, vp, vp, vp, vp, sz, vp]
+        PV = ctypes.POINTER(vp)
+        L.emb_pipeline_steps.restype = i32
+        L.emb_pipeline_steps.argtypes = [T, i32, Up, i32, B, PV, PV, i32, ctypes.POINTER(CDedupSet), vp, i32, PV, PV]
         L.emb_route_ids_noalloc.restype = i32
         L.emb_route_ids_noalloc.argtypes = [T, B, i32, ctypes.POINTER(ctypes.c_int64), vp, vp, vp, vp, vp]
         L.emb_validate_batch.restype = i32
@@ -330,10 +340,10 @@ class Layer:
         self.ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
         workspace_init(self.ws)
         i32 = dict(dtype=torch.int32, device=dev)
-        self.unique_keys = torch.empty(n, **i32)
-        self.counts = torch.empty(n, **i32)
-        self.seg_offsets = torch.empty(n + 1, **i32)
-        self.sort_perm = torch.empty(n, **i32)
+        self.unique_keys = torch.zeros(n, **i32)
+        self.counts = torch.zeros(n, **i32)
+        self.seg_offsets = torch.zeros(n + 1, **i32)
+        self.sort_perm = torch.zeros(n, **i32)
         self.num_unique = torch.zeros(1, **i32)
         self._status = torch.zeros(4, **i32)
         self.max_indices = n
@@ -451,10 +461,10 @@ class DedupBuffers:
         self.ws = torch.empty(wsb, dtype=torch.uint8, device=device)
         workspace_init(self.ws)
         i32 = dict(dtype=torch.int32, device=device)
-        self.unique_keys = torch.empty(n, **i32)
-        self.counts = torch.empty(n, **i32)
-        self.seg_offsets = torch.empty(n + 1, **i32)
-        self.sort_perm = torch.empty(n, **i32)
+        self.unique_keys = torch.zeros(n, **i32)
+        self.counts = torch.zeros(n, **i32)
+        self.seg_offsets = torch.zeros(n + 1, **i32)
+        self.sort_perm = torch.zeros(n, **i32)
         self.num_unique = torch.zeros(1, **i32)
 
 
@@ -538,25 +548,25 @@ class Pipeline:
         self.max_indices = max(1, max_indices)
         self._side_streams = [torch.cuda.Stream(device=dev) for _ in range(self.S)]
         self.sides = [int(x.cuda_stream) for x in self._side_streams]
-        self._ev_start = _Hip.event()
-        # a group's dedups are done (per set parity and side stream); the main
-        # stream's group that read a set is done (per parity)
-        self._ev_side = [[_Hip.event() for _ in range(self.S)] for _ in range(2)]
-        self._ev_main = [_Hip.event(), _Hip.event()]
-        self._dedup_fn = "emb_unique_ids_concurrent" if self.S > 1 else "emb_unique_ids"
+        # events the native schedule records and waits on: the start, the main
+        # stream's group done (per set parity), each side stream's group done
+        # (per parity and stream)
+        self._events = [_Hip.event() for _ in range(3 + 2 * self.S)]
+        self._events_c = (ctypes.c_void_p * len(self._events))(*self._events)
+        self._sides_c = (ctypes.c_void_p * self.S)(*self.sides)
+        self._sets_c = (CDedupSet * len(self.sets))(*[
+            CDedupSet(_ptr(b.unique_keys), _ptr(b.counts), _ptr(b.seg_offsets), _ptr(b.sort_perm),
+                      _ptr(b.num_unique), _ptr(b.ws), b.ws.numel() * b.ws.element_size()) for b in self.sets])
         self._status = torch.zeros(4, dtype=torch.int32, device=dev)
         self._ct = ctypes.byref(tables.c())
         self.rounding, self.seed, self.steps_done = rounding, seed, 0
         self._updc = _update(opt, lr, eps, state, rounding, seed)
-        self._upd = ctypes.byref(self._updc)
         self._pool = POOL[pool]
-        self._set_args = [(_ptr(b.unique_keys), _ptr(b.counts), _ptr(b.seg_offsets), _ptr(b.sort_perm),
-                           _ptr(b.num_unique), _ptr(b.ws), b.ws.numel() * b.ws.element_size()) for b in self.sets]
 
     def __del__(self):
         try:
             L = _Hip.lib()
-            for e in [self._ev_start] + self._ev_side[0] + self._ev_side[1] + self._ev_main:
+            for e in self._events:
                 L.hipEventDestroy(e)
         except Exception:
             pass
@@ -564,53 +574,25 @@ class Pipeline:
     def run(self, steps, stream=None) -> None:
         """Enqueue one training step per ``(batch, out, grad_out)`` of
         ``steps``, in order, on ``stream`` (the forward of each batch into its
-        ``out``, then its backward with ``grad_out`` and the optimizer step).
-        Every step's results are complete when ``stream`` reaches the end of
-        the enqueued work; the side streams' work all precedes it."""
+        ``out``, then its backward with ``grad_out`` and the optimizer step),
+        through one call of the native schedule (emb_pipeline_steps).  Every
+        step's results are complete when ``stream`` reaches the end of the
+        enqueued work; the side streams' work all precedes it."""
         steps = list(steps)
         for b, _, _ in steps:
             if int(b.indices.numel()) > self.max_indices:
                 raise ValueError("batch larger than the pipeline's buffers")
-        if not steps:
+        n = len(steps)
+        if n == 0:
             return
-        L = lib()
-        dedup = getattr(L, self._dedup_fn)
-        main = _stream(stream)
-        K, S = self.K, self.S
-        ngroups = (len(steps) + K - 1) // K
-        # the side streams start after everything already on the main stream
-        _Hip.record(self._ev_start, main)
-        for sp in self.sides:
-            _Hip.wait(sp, self._ev_start)
-
-        def dedups(g):
-            par = g % 2
-            for i, (b, _, _) in enumerate(steps[g * K:(g + 1) * K]):
-                uk, cnt, seg, perm, nu, ws, wsb = self._set_args[par * K + i]
-                _check(self._dedup_fn, dedup(self._ct, ctypes.byref(b.c()), uk, cnt, seg, perm, nu, ws, wsb,
-                                             self.sides[i % S]))
-            for s, sp in enumerate(self.sides):
-                _Hip.record(self._ev_side[par][s], sp)
-
-        dedups(0)
-        for g in range(ngroups):
-            if g + 1 < ngroups:
-                if g >= 1:
-                    # the sets of group g + 1 were read by the main stream's group g - 1
-                    for sp in self.sides:
-                        _Hip.wait(sp, self._ev_main[(g + 1) % 2])
-                dedups(g + 1)
-            for ev in self._ev_side[g % 2]:
-                _Hip.wait(main, ev)
-            for i, (b, out, grad_out) in enumerate(steps[g * K:(g + 1) * K]):
-                uk, cnt, seg, perm, nu, ws, wsb = self._set_args[(g % 2) * K + i]
-                cb = ctypes.byref(b.c())
-                self._updc.seed = self.seed + self.steps_done
-                self.steps_done += 1
-                _check("emb_pool_fwd", L.emb_pool_fwd(self._ct, cb, self._pool, _ptr(out), main))
-                _check("emb_grad_reduce", L.emb_grad_reduce(self._ct, cb, self._pool, _ptr(grad_out), perm, seg, uk,
-                                                            nu, None, self._upd, ws, wsb, main))
-            _Hip.record(self._ev_main[g % 2], main)
+        batches = (CBatch * n)(*[b.c() for b, _, _ in steps])
+        outs = (ctypes.c_void_p * n)(*[_ptr(o) for _, o, _ in steps])
+        grads = (ctypes.c_void_p * n)(*[_ptr(g) for _, _, g in steps])
+        self._updc.seed = self.seed + self.steps_done
+        _check("emb_pipeline_steps", lib().emb_pipeline_steps(
+            self._ct, self._pool, ctypes.byref(self._updc), n, batches, outs, grads, self.K, self._sets_c,
+            _stream(stream), self.S, self._sides_c, self._events_c))
+        self.steps_done += n
 
     def status(self, stream=None):
         """Per buffer set, the status of its last step (emb_workspace_status);

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libemb.so")
-SOURCES = ["emb_api.hip", "pool_fwd.hip", "dedup.hip", "reduce.hip", "misc.hip", "route.hip"]
+SOURCES = ["emb_api.hip", "pool_fwd.hip", "dedup.hip", "reduce.hip", "misc.hip", "route.hip", "pipeline.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -1261,7 +1261,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     if (!sort_cores) {
       // reduce-then-scan: the tiles' digit counts, then their prefixes over
       // the tiles and the digit totals
-      uint32_t* counts = reinterpret_cast<uint32_t*>(back + L.rows);
+      uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.tile_counts);
       CountArgs ca{};
       ca.keys = kin;
       ca.N = N;

@@ -50,11 +50,35 @@ int key_bits_for(int64_t R) {
   return bits;
 }
 
+// The largest batch (ids) whose layout fits ws_bytes with rows of D floats.
+// Layouts grow with the batch, so a bisection finds it; the last answer of
+// each thread is kept, since a workspace is normally used with one size.
+int64_t ws_capacity(size_t ws_bytes, int32_t D) {
+  thread_local size_t c_bytes = 0;
+  thread_local int32_t c_dim = 0;
+  thread_local int64_t c_cap = -1;
+  if (c_cap >= 0 && c_bytes == ws_bytes && c_dim == D) return c_cap;
+  int64_t lo = 0, hi = kMaxIndices - 1;
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo + 1) / 2;
+    if (ws_layout(mid, 0, D).total <= ws_bytes) lo = mid; else hi = mid - 1;
+  }
+  c_bytes = ws_bytes;
+  c_dim = D;
+  c_cap = lo;
+  return lo;
+}
+
+// Regions are placed by the workspace's capacity, not by the batch: for one
+// ws_bytes and dim every byte belongs to the same region in every call, so a
+// region of call-tagged words only ever holds such words (or the zeros of
+// emb_workspace_init), never another call's keys, positions or counts, which
+// could pass for a word of the current call.
 emb_status check_ws(const void* ws, size_t ws_bytes, int64_t N, int64_t M, int32_t D, WsLayout* lay) {
   if (ws == nullptr) return EMB_EINVAL;
   if (((uintptr_t)ws & 255u) != 0) return EMB_EWORKSPACE;
-  *lay = ws_layout(N, M, D);
-  if (ws_bytes < lay->total) return EMB_EWORKSPACE;
+  if (ws_bytes < ws_layout(N, M, D).total) return EMB_EWORKSPACE;
+  *lay = ws_layout(ws_capacity(ws_bytes, D), M, D);
   return EMB_OK;
 }
 

@@ -84,7 +84,7 @@ static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 struct WsLayout {
   // front (offsets from the workspace base)
   size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_keys, sorted_bag, uniq_status,
-      chunk_seg, partials, level2, arrivals, front;
+      tile_counts, chunk_seg, partials, level2, arrivals, front;
   // back (offsets from the back base)
   size_t pass_status, rows, grp, later, back;
   size_t total;
@@ -129,6 +129,12 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   off = align256(off + n4);
   L.uniq_status = off;
   off = align256(off + sizeof(uint64_t) * L.uniq_tiles);
+  // plain digit counts of the passes whose tiles are not all resident at
+  // once (tiles of kSortThreads * kSortItemsWide keys); never shares bytes
+  // with the call-tagged words of the back region
+  L.tile_counts = off;
+  off = align256(off + sizeof(uint32_t) * (size_t)((n + kSortThreads * kSortItemsWide - 1) / (kSortThreads * kSortItemsWide)) *
+                           kMaxDigits);
   L.chunk_seg = off;
   off = align256(off + sizeof(int32_t) * (L.chunks + 1));
   L.partials = off;

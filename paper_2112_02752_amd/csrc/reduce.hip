@@ -793,12 +793,12 @@ hipError_t launch_grad_reduce(const ReduceLaunch& p, hipStream_t s) {
   ra.partials = reinterpret_cast<float*>(ws + p.lay.partials);
   ra.level2 = reinterpret_cast<uint64_t*>(ws + p.lay.level2);
   ra.arrivals = reinterpret_cast<uint32_t*>(ws + p.lay.arrivals);
-  ra.ncomb = (int32_t)p.lay.combine_blocks;
+  ra.nchunks = (p.N + kChunk - 1) / kChunk;
+  ra.ncomb = (ra.nchunks + kCombineChunks - 1) / kCombineChunks;  // of this batch (the layout is the workspace's)
   ra.hdr = ws + p.lay.hdr;
   ra.N = p.N;
   ra.D = p.D;
   ra.pool = p.pool;
-  ra.nchunks = (p.N + kChunk - 1) / kChunk;
   ra.up.W = p.W;
   ra.up.state = p.state;
   ra.up.D = p.D;

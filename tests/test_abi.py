@@ -192,3 +192,30 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(emb, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         emb.lib()
+
+
+def test_pipeline_steps_argument_checks():
+    """Host checks of emb_pipeline_steps return before anything is enqueued."""
+    L = emb.lib()
+    t = _tables()
+    upd = emb.CUpdate(0, 0.1, 0.0, None, 0, 0)
+    b = (emb.CBatch * 1)(emb.CBatch(1, 0x1000, 0x2000, 10, 4))
+    ptrs = (ctypes.c_void_p * 1)(0x3000)
+    sets = (emb.CDedupSet * 2)()
+    sides = (ctypes.c_void_p * 2)(0x10, 0x20)
+    events = (ctypes.c_void_p * 7)(*([0x40] * 7))
+    no_events = (ctypes.c_void_p * 7)(*([0x40] * 6 + [0]))
+    f = L.emb_pipeline_steps
+    tb, ub = ctypes.byref(t), ctypes.byref(upd)
+    assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_OK   # nothing to do
+    assert f(None, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 0, None, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, -1, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 0, sets, None, 1, sides, events) == emb.EMB_EINVAL      # group 0
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 2, sides, events) == emb.EMB_EINVAL      # sides > group
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 2, sets, None, 0, sides, events) == emb.EMB_EINVAL      # no side stream
+    assert f(tb, 0, ub, 1, None, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, None, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 2, sets, None, 2, sides, no_events) == emb.EMB_EINVAL   # a null event
+    same = (ctypes.c_void_p * 2)(0x10, 0x77)
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 2, sets, 0x77, 2, same, events) == emb.EMB_EINVAL       # side == main

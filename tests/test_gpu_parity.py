@@ -777,6 +777,65 @@ def test_unique_ids_concurrent_edge_cases(case):
     _dedup_concurrent_vs_oracle(_row_offset(rows), B, off, idx, len(rows) * B)
 
 
+def test_workspace_shared_by_both_dedups_and_all_sizes():
+    """One workspace serves both dedups and batches of very different sizes,
+    in any order: co-resident passes after wait-free ones (whose plain tile
+    counts must never sit where the co-resident passes poll call-tagged
+    words) and small batches after large ones (whose arrays must never sit
+    where a smaller batch's tagged words go).  Every dedup, and the unfused
+    gradient reduce that follows it on the same workspace, matches the
+    oracle, and no call reports an error."""
+    import oracle
+    import torch
+    import paper_2112_02752_amd as emb
+    dev = "cuda"
+    D = 64
+    rng = np.random.default_rng(11)
+    small_rows, small_B = [1000, 50_000], 300
+    cases = []
+    for name, seed, concurrent in [("c3", 0, True), ("c3", 1, False), ("c5", 0, False), ("small", 0, False),
+                                   ("c3", 2, False), ("c3", 3, True), ("c3", 6, False), ("c2", 0, False),
+                                   ("small", 1, True), ("c3", 4, False), ("c2", 1, True), ("c3", 5, False)]:
+        if name == "small":
+            off, idx = _rand_batch(rng, small_rows, small_B, 30, empty_frac=0.05, zipf=1.2)
+            G = rng.standard_normal((len(off) - 1, D)).astype(np.float32)
+            cases.append((name, concurrent, _row_offset(small_rows), small_B, off, idx, G, "sum"))
+        else:
+            w = synth.workload(name)
+            assert w.dim == D
+            b = synth.make_batch(w, seed)
+            cases.append((name, concurrent, w.row_offset, w.bags_per_table, b.offsets, b.indices, b.grad, w.pool))
+    N = max(len(c[5]) for c in cases)
+    M = max(len(c[4]) - 1 for c in cases)
+    bufs = emb.DedupBuffers(dev, N, M, D)
+    Wd = torch.empty((1, D), dtype=torch.float32, device=dev)  # never read: no update here
+    gr = torch.zeros((N, D), dtype=torch.float32, device=dev)
+    for k, (name, concurrent, ro, B, off, idx, G, pool) in enumerate(cases):
+        n = len(idx)
+        _say(f"case shared workspace call {k}: {name} N={n} concurrent={concurrent}")
+        tables = emb.Tables(Wd, [int(x) for x in ro])
+        b = emb.Batch(torch.from_numpy(np.ascontiguousarray(off, np.int32)).to(dev),
+                      torch.from_numpy(np.ascontiguousarray(idx, np.int32)).to(dev), B)
+        Gd = torch.from_numpy(G).to(dev)
+        emb.unique_ids(tables, b, bufs.unique_keys, bufs.counts, bufs.seg_offsets, bufs.sort_perm, bufs.num_unique,
+                       bufs.ws, concurrent=concurrent)
+        emb.grad_reduce(tables, b, pool, Gd, bufs.sort_perm, bufs.seg_offsets, bufs.unique_keys, bufs.num_unique,
+                        bufs.ws, grad_rows=gr)
+        torch.cuda.synchronize()
+        assert emb.read_status(bufs.ws)[0] == 0, f"call {k} ({name}) reported an error"
+        ref = oracle.unique_ids(len(ro) - 1, np.asarray(ro, np.int64), B, np.ascontiguousarray(off, np.int32),
+                                np.ascontiguousarray(idx, np.int32))
+        U = int(bufs.num_unique.cpu().item())
+        assert U == ref.num_unique, f"call {k} ({name})"
+        np.testing.assert_array_equal(bufs.unique_keys[:U].cpu().numpy().view(np.uint32), ref.unique_keys)
+        np.testing.assert_array_equal(bufs.counts[:U].cpu().numpy(), ref.counts)
+        np.testing.assert_array_equal(bufs.seg_offsets[:U + 1].cpu().numpy(), ref.seg_offsets)
+        np.testing.assert_array_equal(bufs.sort_perm[:n].cpu().numpy(), ref.perm)
+        o_gr, _ = oracle.grad_reduce(len(ro) - 1, B, np.ascontiguousarray(off, np.int32), G, pool, ref)
+        r = parity.rel_rownorm(gr[:U].cpu().numpy(), o_gr)
+        assert r <= parity.TOL_FP32, f"call {k} ({name}): gradient rows rel err {r}"
+
+
 # ------------------------------------------------------------------ routing
 
 def _route_gpu(row_offset, B, off, idx, shard, W_dev=None, idx64=False):

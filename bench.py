@@ -48,7 +48,9 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=60,
+                    help="untimed steps first, each on a batch of its own (the pipelined schedule needs "
+                         "several groups of them to reach its steady state)")
     ap.add_argument("--workload", default="c3")
     ap.add_argument("--bags", type=int, default=None, help="bags per table instead of the workload's own")
     ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
@@ -225,7 +227,13 @@ def main():
         w = dataclasses.replace(w, bags_per_table=args.bags, name=f"{w.name}-b{args.bags}",
                                 description=f"{w.description}; {args.bags} bags per table instead")
     dev = "cuda"
-    total = args.warmup + args.steps
+    # every step, warm-up or timed, gets a batch of its own: the warm-up
+    # steps touch as much of the table as steady-state training has touched
+    # recently (with fewer distinct warm-up batches the first timed steps
+    # run slower)
+    n_warm = args.warmup
+    t0_batch = n_warm
+    total = n_warm + args.steps
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
     t0 = time.time()
     batches = [synth.make_batch(w, s) for s in range(total)]
@@ -273,18 +281,18 @@ def main():
         clayer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
                            concurrent=True if args.schedule == "concurrent" else "auto")
 
-        def run_steps(lo, hi):
-            for i in range(lo, hi):
+        def run_steps(idx):
+            for i in idx:
                 clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
     elif args.schedule == "pipelined":
         pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
                             group=args.group, side_streams=args.side_streams)
 
-        def run_steps(lo, hi):
-            pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in range(lo, hi)], sp)
+        def run_steps(idx):
+            pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in idx], sp)
     else:
-        def run_steps(lo, hi):
-            for i in range(lo, hi):
+        def run_steps(idx):
+            for i in idx:
                 layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
 
     def check_status(where):
@@ -299,7 +307,7 @@ def main():
             print(f"bench.py: {where}: {e}", file=sys.stderr, flush=True)
             sys.exit(3)
 
-    run_steps(0, args.warmup)
+    run_steps(range(n_warm))
     torch.cuda.synchronize()
     check_status("warm-up")
 
@@ -309,7 +317,7 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     e_all[0].record(stream)
-    run_steps(args.warmup, total)
+    run_steps(range(t0_batch, total))
     e_all[1].record(stream)
     t_enq = time.perf_counter() - t_start
     torch.cuda.synchronize()
@@ -320,7 +328,7 @@ def main():
     # the same batches again as serial steps with an event pair around each
     # step: the distribution of serial step times
     sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
-    for k, i in enumerate(range(args.warmup, total)):
+    for k, i in enumerate(range(t0_batch, total)):
         sev[k][0].record(stream)
         layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
         sev[k][1].record(stream)
@@ -332,7 +340,7 @@ def main():
     # per-phase times for the roofline
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
-    for k, i in enumerate(range(args.warmup, total)):
+    for k, i in enumerate(range(t0_batch, total)):
         step(i, evs[k])
     torch.cuda.synchronize()
     ph = {"fwd": [], "dedup": [], "bwd_update": []}
@@ -348,7 +356,7 @@ def main():
     cold = None
     if not args.no_cold:
         cold_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-        for k, i in enumerate(range(args.warmup, total)):
+        for k, i in enumerate(range(t0_batch, total)):
             flush.fill_(k & 0xff)
             step(i, cold_evs[k])
         torch.cuda.synchronize()
@@ -385,21 +393,21 @@ def main():
         rcnt = torch.empty(Wr, **i32)
         rids, rpos, rbag = (torch.empty(nmax, **i32) for _ in range(3))
         rws = torch.empty(emb.route_workspace_size(nmax, w.num_bags, Wr), dtype=torch.uint8, device=dev)
-        for i in range(args.warmup):
+        for i in range(n_warm):
             emb.route_ids(tables, dev_batches[i][0], shard, rcnt, rids, rpos, rbag, rws, sp)
         rev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
         torch.cuda.synchronize()
-        for k, i in enumerate(range(args.warmup, total)):
+        for k, i in enumerate(range(t0_batch, total)):
             rev[k][0].record(stream)
             emb.route_ids(tables, dev_batches[i][0], shard, rcnt, rids, rpos, rbag, rws, sp)
             rev[k][1].record(stream)
         torch.cuda.synchronize()
         r_s = float(np.median([e[0].elapsed_time(e[1]) * 1e-3 for e in rev]))
-        r_bytes = 4 * (w.num_bags + 1) + 4 * np.mean([dev_batches[i][2] for i in range(args.warmup, total)]) * 4 \
+        r_bytes = 4 * (w.num_bags + 1) + 4 * np.mean([dev_batches[i][2] for i in range(t0_batch, total)]) * 4 \
             + 4 * Wr
         routing = {"ranks": Wr, "shard": "equal row ranges", "kernels": "k_route_count, k_route_scan, "
                    "k_route_scatter (emb_route_ids)", "median_us": r_s * 1e6,
-                   "ids_per_s": float(np.mean([dev_batches[i][2] for i in range(args.warmup, total)])) / r_s,
+                   "ids_per_s": float(np.mean([dev_batches[i][2] for i in range(t0_batch, total)])) / r_s,
                    "bytes_per_launch": float(r_bytes), "achieved_GBs": r_bytes / r_s / 1e9,
                    "frac": r_bytes / r_s / 1e9 / HBM_PEAK_GBS}
 
@@ -407,7 +415,7 @@ def main():
     # against the same batch's eager steps (the step launches only kernels)
     graph = None
     if not args.no_graph:
-        i0 = args.warmup
+        i0 = t0_batch
         reps = 20
         ge = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         torch.cuda.synchronize()
@@ -435,11 +443,11 @@ def main():
             graph = {"error": str(e)[:200]}
 
     check_status("after the serial, phase-timed and cold steps")
-    n_lookups = sum(dev_batches[i][2] for i in range(args.warmup, total))
+    n_lookups = sum(dev_batches[i][2] for i in range(t0_batch, total))
 
     # unique counts of the timed batches (for the byte models)
     us = []
-    for i in range(args.warmup, total):
+    for i in range(t0_batch, total):
         b = batches[i]
         us.append(len(np.unique(global_keys(w.row_offset, w.bags_per_table, b.offsets, b.indices))))
     N_avg = n_lookups / args.steps
@@ -474,7 +482,7 @@ def main():
                    "group": args.group if args.schedule == "pipelined" else None,
                    "side_streams": args.side_streams if args.schedule == "pipelined" else None,
                    "overlapped_steps": args.steps if args.schedule == "pipelined" else
-                   sum(1 for i in range(args.warmup, total)
+                   sum(1 for i in range(t0_batch, total)
                        if clayer is not None and clayer.overlaps(dev_batches[i][2]))},
         "roofline": {"bound": "hbm", "phase": dom, "kernel": d["kernels"], "model": "logical",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,

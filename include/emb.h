@@ -205,9 +205,14 @@ typedef struct {
  * All of the side streams' work precedes the end of the work enqueued on
  * main_stream, so one synchronisation of main_stream completes every step.
  * The side streams must differ from main_stream; calls that share sets,
- * events or side streams must be ordered.  Host-checkable errors return
- * before anything is enqueued; an error of a later step (a batch larger than
- * the sets' buffers) returns with the earlier steps enqueued. */
+ * events or side streams must be ordered.  With more than one group, each
+ * side stream's work is enqueued by a host thread of its own, started and
+ * joined within the call, while the calling thread enqueues main_stream's
+ * (the device order is the same as from one thread).  Every step's
+ * arguments are checked before anything is enqueued (EMB_EINVAL,
+ * EMB_EWORKSPACE, EMB_EUNSUPPORTED as the per-step calls would return, and
+ * EMB_EUNSUPPORTED for n_side > 16); EMB_EHIP (a failed launch or event
+ * call) returns with part of the schedule enqueued. */
 emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_update* update, int32_t n_steps,
                               const emb_batch* batches, float* const* outs, const float* const* grads,
                               int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,

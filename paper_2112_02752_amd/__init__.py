@@ -191,7 +191,12 @@ class Batch:
     indices: object
     bags_per_table: int
 
+    def __post_init__(self):
+        # the C descriptor is built with the batch, not on its first use
+        self.c()
+
     def c(self) -> CBatch:
+        """The C descriptor; rebuilt if a tensor was replaced or reallocated."""
         key = (_ptr(self.offsets), _ptr(self.indices), int(self.indices.numel()), self.bags_per_table,
                int(self.indices.element_size()))
         if getattr(self, "_ckey", None) != key:
@@ -538,8 +543,8 @@ class Pipeline:
                  max_indices: int = 0, max_bags: int = 0, group: int = 6, side_streams: int = 3,
                  rounding: str = "nearest", seed: int = 0):
         import torch
-        if group < 1 or side_streams < 1:
-            raise ValueError("group and side_streams must be >= 1")
+        if group < 1 or not 1 <= side_streams <= 16:
+            raise ValueError("group must be >= 1 and side_streams in 1..16")
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
         dev = tables.weights.device
         D = int(tables.weights.shape[1])
@@ -579,13 +584,13 @@ class Pipeline:
         step's results are complete when ``stream`` reaches the end of the
         enqueued work; the side streams' work all precedes it."""
         steps = list(steps)
-        for b, _, _ in steps:
-            if int(b.indices.numel()) > self.max_indices:
-                raise ValueError("batch larger than the pipeline's buffers")
         n = len(steps)
         if n == 0:
             return
-        batches = (CBatch * n)(*[b.c() for b, _, _ in steps])
+        cbs = [b.c() for b, _, _ in steps]
+        if max(c.num_indices for c in cbs) > self.max_indices:
+            raise ValueError("batch larger than the pipeline's buffers")
+        batches = (CBatch * n)(*cbs)
         outs = (ctypes.c_void_p * n)(*[_ptr(o) for _, o, _ in steps])
         grads = (ctypes.c_void_p * n)(*[_ptr(g) for _, _, g in steps])
         self._updc.seed = self.seed + self.steps_done

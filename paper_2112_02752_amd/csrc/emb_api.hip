@@ -134,6 +134,34 @@ emb_status route_prepare(const emb_tables* tables, const emb_batch* batch, int32
 
 }  // namespace
 
+namespace emb {
+
+// Every host check that emb_pool_fwd, emb_unique_ids (or _concurrent) and a
+// fused emb_grad_reduce would make for one step of the pipelined schedule,
+// so that the schedule can reject a bad step before it enqueues anything.
+emb_status check_pipeline_step(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* out,
+                               const float* grad, const emb_update* update, const emb_dedup_set* d) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  if ((st = check_batch(batch, tables->num_tables, &M)) != EMB_OK) return st;
+  if (pool != EMB_POOL_SUM && pool != EMB_POOL_MEAN) return EMB_EINVAL;
+  if ((st = check_update(update)) != EMB_OK) return st;
+  if ((int64_t)tables->dim * dtype_bytes(tables->dtype) / 16 > fwd_max_row_vectors()) return EMB_EUNSUPPORTED;
+  if (tables->dim > reduce_max_dim()) return EMB_EUNSUPPORTED;
+  if (M > 0 && out == nullptr) return EMB_EINVAL;
+  if (d->seg_offsets == nullptr || d->num_unique == nullptr) return EMB_EINVAL;
+  if (batch->num_indices > 0 && (d->unique_keys == nullptr || d->counts == nullptr || d->sort_perm == nullptr ||
+                                 grad == nullptr))
+    return EMB_EINVAL;
+  WsLayout lay;
+  return check_ws(d->ws, d->ws_bytes, batch->num_indices, M, tables->dim, &lay);
+}
+
+}  // namespace emb
+
 extern "C" {
 
 const char* emb_status_string(int32_t status) {

@@ -125,4 +125,8 @@ hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_workspace_status(const void* ws, int32_t* status, hipStream_t s);
 
+// host checks of one step of emb_pipeline_steps (defined with the C ABI)
+emb_status check_pipeline_step(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* out,
+                               const float* grad, const emb_update* update, const emb_dedup_set* d);
+
 }  // namespace emb

@@ -3,9 +3,184 @@
 // forward and the fused update of the current group.  The dedup reads only a
 // batch's ids and offsets, never the table, so running it early changes no
 // result.  Everything here is host code that only enqueues work through the
-// library's entry points and HIP events (no allocation, no synchronisation).
+// library's entry points and HIP events (no allocation, no synchronisation
+// with the device).
+//
+// Enqueueing a dedup costs the host tens of microseconds (a dozen kernel
+// launches for the wait-free dedup), about as long as the device takes for a
+// whole step, so with more than one group each side stream's work is
+// enqueued by a helper thread of its own while the calling thread enqueues
+// the main stream's (kernel launches on different streams proceed in
+// parallel from different threads).  Counters keep every cross-stream wait
+// attached to the same event record as in a single-threaded enqueue:
+//   side_done[s]: groups whose dedups and record on side stream s are
+//     enqueued; the main stream's waits for group g are enqueued only once
+//     every side_done[s] > g.
+//   main_done: groups whose main-stream record is enqueued; the dedups of
+//     group g >= 2 (which reuse the buffer sets of group g - 2) are enqueued
+//     only once main_done >= g - 1, after their wait for that record.
+// The side thread re-records the events of a parity only after the main
+// thread has enqueued its wait on the previous record (main_done >= g - 1
+// implies the main stream's wait for group g - 2 is enqueued), so no wait
+// ever attaches to a later record, which could make the two streams wait
+// for each other.
+#include <atomic>
+#include <system_error>
+#include <thread>
+
 #include "emb_common.h"
 #include "kernels.h"
+
+namespace {
+
+constexpr int kMaxSideStreams = 16;  // one host thread each
+
+struct Schedule {
+  const emb_tables* tables;
+  int32_t pool;
+  const emb_update* update;
+  int32_t n_steps, K, ngroups, n_side;
+  const emb_batch* batches;
+  float* const* outs;
+  const float* const* grads;
+  const emb_dedup_set* sets;
+  hipStream_t main;
+  void* const* sides;
+  hipEvent_t ev_start, ev_main[2];
+  void* const* events;
+
+  hipEvent_t ev_side(int parity, int s) const { return (hipEvent_t)events[3 + parity * n_side + s]; }
+  hipStream_t side(int s) const { return (hipStream_t)sides[s]; }
+};
+
+emb_status hip_ok(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; }
+
+// one dedup in flight per side stream at most with emb_unique_ids (which may
+// make the workgroups of a pass wait for one another); several side streams
+// use emb_unique_ids_concurrent, whose workgroups never wait for one another
+emb_status dedup_one(const Schedule& c, int k, const emb_dedup_set& d, void* stream) {
+  auto fn = c.n_side > 1 ? emb_unique_ids_concurrent : emb_unique_ids;
+  return fn(c.tables, &c.batches[k], d.unique_keys, d.counts, d.seg_offsets, d.sort_perm, d.num_unique, d.ws,
+            d.ws_bytes, stream);
+}
+
+// side stream s's part of group g: (for g >= 2) its wait for the main
+// stream's group g - 2, the dedups of the group dealt to it (i % n_side == s)
+// into the buffer sets of parity g % 2, and its record
+emb_status side_group(const Schedule& c, int g, int s) {
+  const int par = g % 2;
+  if (g >= 2 && hipStreamWaitEvent(c.side(s), c.ev_main[par], 0) != hipSuccess) return EMB_EHIP;
+  for (int i = s; i < c.K && g * c.K + i < c.n_steps; i += c.n_side) {
+    const emb_status r = dedup_one(c, g * c.K + i, c.sets[par * c.K + i], c.sides[s]);
+    if (r != EMB_OK) return r;
+  }
+  return hip_ok(hipEventRecord(c.ev_side(par, s), c.side(s)));
+}
+
+emb_status side_group_all(const Schedule& c, int g) {
+  for (int s = 0; s < c.n_side; ++s) {
+    const emb_status r = side_group(c, g, s);
+    if (r != EMB_OK) return r;
+  }
+  return EMB_OK;
+}
+
+// the main stream's part of group g: the wait for the group's dedups, then
+// each step's forward and fused backward + update, then the group's record
+emb_status main_group(const Schedule& c, int g) {
+  const int par = g % 2;
+  for (int s = 0; s < c.n_side; ++s)
+    if (hipStreamWaitEvent(c.main, c.ev_side(par, s), 0) != hipSuccess) return EMB_EHIP;
+  emb_update u = *c.update;
+  for (int i = 0; i < c.K && g * c.K + i < c.n_steps; ++i) {
+    const int k = g * c.K + i;
+    const emb_dedup_set& d = c.sets[par * c.K + i];
+    u.seed = c.update->seed + (uint64_t)k;  // bf16 stochastic rounding draws fresh bits every step
+    emb_status st = emb_pool_fwd(c.tables, &c.batches[k], c.pool, c.outs[k], c.main);
+    if (st == EMB_OK)
+      st = emb_grad_reduce(c.tables, &c.batches[k], c.pool, c.grads[k], d.sort_perm, d.seg_offsets, d.unique_keys,
+                           d.num_unique, nullptr, &u, d.ws, d.ws_bytes, c.main);
+    if (st != EMB_OK) return st;
+  }
+  return hip_ok(hipEventRecord(c.ev_main[par], c.main));
+}
+
+// single thread: the side streams' part of group g + 1 is enqueued before the
+// main stream's part of group g
+emb_status run_single(const Schedule& c) {
+  emb_status st = side_group_all(c, 0);
+  for (int g = 0; g < c.ngroups && st == EMB_OK; ++g) {
+    if (g + 1 < c.ngroups && (st = side_group_all(c, g + 1)) != EMB_OK) break;
+    st = main_group(c, g);
+  }
+  return st;
+}
+
+bool await_count(const std::atomic<int>& n, int v, const std::atomic<int>& failed) {
+  while (n.load(std::memory_order_acquire) < v) {
+    if (failed.load(std::memory_order_acquire)) return false;
+    std::this_thread::yield();
+  }
+  return true;
+}
+
+emb_status run_threaded(const Schedule& c) {
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess) return EMB_EHIP;
+  std::atomic<int> side_done[kMaxSideStreams], main_done{0}, failed{0};
+  emb_status side_st[kMaxSideStreams];
+  for (int s = 0; s < c.n_side; ++s) {
+    side_done[s].store(0);
+    side_st[s] = EMB_OK;
+  }
+  auto side_work = [&](int s) {
+    // the current device is per thread: the caller's
+    if (hipSetDevice(device) != hipSuccess) {
+      side_st[s] = EMB_EHIP;
+      failed.store(1, std::memory_order_release);
+      return;
+    }
+    for (int g = 0; g < c.ngroups; ++g) {
+      if (failed.load(std::memory_order_acquire)) return;
+      if (g >= 2 && !await_count(main_done, g - 1, failed)) return;
+      side_st[s] = side_group(c, g, s);
+      if (side_st[s] != EMB_OK) {
+        failed.store(1, std::memory_order_release);
+        return;
+      }
+      side_done[s].store(g + 1, std::memory_order_release);
+    }
+  };
+  std::thread helpers[kMaxSideStreams];
+  int started = 0;
+  try {
+    for (; started < c.n_side; ++started) helpers[started] = std::thread(side_work, started);
+  } catch (const std::system_error&) {
+    failed.store(1, std::memory_order_release);
+    for (int s = 0; s < started; ++s) helpers[s].join();
+    // with no thread started nothing is enqueued yet: the same schedule from
+    // this thread; otherwise the started ones may have enqueued dedups of
+    // the first groups (which nothing waits on) and the call fails
+    return started == 0 ? run_single(c) : EMB_EHIP;
+  }
+  emb_status st = EMB_OK;
+  for (int g = 0; g < c.ngroups && st == EMB_OK; ++g) {
+    for (int s = 0; s < c.n_side; ++s)
+      if (!await_count(side_done[s], g + 1, failed)) st = EMB_EHIP;
+    if (st != EMB_OK) break;
+    if ((st = main_group(c, g)) != EMB_OK) {
+      failed.store(1, std::memory_order_release);
+      break;
+    }
+    main_done.store(g + 1, std::memory_order_release);
+  }
+  for (int s = 0; s < c.n_side; ++s) helpers[s].join();
+  for (int s = 0; s < c.n_side; ++s)
+    if (side_st[s] != EMB_OK) return side_st[s];
+  return st;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -15,6 +190,7 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
                               void* const* side_streams, void* const* events) {
   if (tables == nullptr || update == nullptr || n_steps < 0 || group < 1 || n_side < 1 || n_side > group)
     return EMB_EINVAL;
+  if (n_side > kMaxSideStreams) return EMB_EUNSUPPORTED;
   if (n_steps == 0) return EMB_OK;
   if (batches == nullptr || outs == nullptr || grads == nullptr || sets == nullptr || side_streams == nullptr ||
       events == nullptr)
@@ -23,64 +199,35 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
     if (events[i] == nullptr) return EMB_EINVAL;
   for (int s = 0; s < n_side; ++s)
     if (side_streams[s] == nullptr || side_streams[s] == main_stream) return EMB_EINVAL;
-  const hipStream_t main = (hipStream_t)main_stream;
-  hipEvent_t ev_start = (hipEvent_t)events[0];
-  hipEvent_t ev_main[2] = {(hipEvent_t)events[1], (hipEvent_t)events[2]};
-  auto ev_side = [&](int parity, int s) { return (hipEvent_t)events[3 + parity * n_side + s]; };
-  auto hip_ok = [](hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; };
-  const int K = group;
-  const int ngroups = (n_steps + K - 1) / K;
-  // one dedup in flight per side stream at most with emb_unique_ids (which may
-  // make the workgroups of a pass wait for one another); several side
-  // streams use emb_unique_ids_concurrent, whose workgroups never wait
-  auto dedup = n_side > 1 ? emb_unique_ids_concurrent : emb_unique_ids;
-  emb_status st = hip_ok(hipEventRecord(ev_start, main));
-  for (int s = 0; s < n_side && st == EMB_OK; ++s) st = hip_ok(hipStreamWaitEvent((hipStream_t)side_streams[s], ev_start, 0));
-  if (st != EMB_OK) return st;
-
-  // the dedups of group g into the buffer sets of parity g % 2
-  auto dedups = [&](int g) -> emb_status {
-    const int par = g % 2;
-    for (int i = 0; i < K && g * K + i < n_steps; ++i) {
-      const int k = g * K + i;
-      const emb_dedup_set& d = sets[par * K + i];
-      const emb_status r = dedup(tables, &batches[k], d.unique_keys, d.counts, d.seg_offsets, d.sort_perm,
-                                 d.num_unique, d.ws, d.ws_bytes, side_streams[i % n_side]);
-      if (r != EMB_OK) return r;
-    }
-    for (int s = 0; s < n_side; ++s) {
-      const emb_status r = hip_ok(hipEventRecord(ev_side(par, s), (hipStream_t)side_streams[s]));
-      if (r != EMB_OK) return r;
-    }
-    return EMB_OK;
-  };
-
-  if ((st = dedups(0)) != EMB_OK) return st;
-  emb_update u = *update;
-  for (int g = 0; g < ngroups; ++g) {
-    if (g + 1 < ngroups) {
-      if (g >= 1) {
-        // the sets of group g + 1 were read by the main stream's group g - 1
-        for (int s = 0; s < n_side; ++s)
-          if ((st = hip_ok(hipStreamWaitEvent((hipStream_t)side_streams[s], ev_main[(g + 1) % 2], 0))) != EMB_OK)
-            return st;
-      }
-      if ((st = dedups(g + 1)) != EMB_OK) return st;
-    }
-    for (int s = 0; s < n_side; ++s)
-      if ((st = hip_ok(hipStreamWaitEvent(main, ev_side(g % 2, s), 0))) != EMB_OK) return st;
-    for (int i = 0; i < K && g * K + i < n_steps; ++i) {
-      const int k = g * K + i;
-      const emb_dedup_set& d = sets[(g % 2) * K + i];
-      u.seed = update->seed + (uint64_t)k;  // bf16 stochastic rounding draws fresh bits every step
-      if ((st = emb_pool_fwd(tables, &batches[k], pool, outs[k], main_stream)) != EMB_OK) return st;
-      if ((st = emb_grad_reduce(tables, &batches[k], pool, grads[k], d.sort_perm, d.seg_offsets, d.unique_keys,
-                                d.num_unique, nullptr, &u, d.ws, d.ws_bytes, main_stream)) != EMB_OK)
-        return st;
-    }
-    if ((st = hip_ok(hipEventRecord(ev_main[g % 2], main))) != EMB_OK) return st;
+  // every step is checked before anything is enqueued
+  for (int k = 0; k < n_steps; ++k) {
+    const emb_status st =
+        emb::check_pipeline_step(tables, &batches[k], pool, outs[k], grads[k], update, &sets[((k / group) % 2) * group + k % group]);
+    if (st != EMB_OK) return st;
   }
-  return EMB_OK;
+  Schedule c{};
+  c.tables = tables;
+  c.pool = pool;
+  c.update = update;
+  c.n_steps = n_steps;
+  c.K = group;
+  c.ngroups = (n_steps + group - 1) / group;
+  c.n_side = n_side;
+  c.batches = batches;
+  c.outs = outs;
+  c.grads = grads;
+  c.sets = sets;
+  c.main = (hipStream_t)main_stream;
+  c.sides = side_streams;
+  c.ev_start = (hipEvent_t)events[0];
+  c.ev_main[0] = (hipEvent_t)events[1];
+  c.ev_main[1] = (hipEvent_t)events[2];
+  c.events = events;
+  // the side streams start after the work already on the main stream
+  if (hipEventRecord(c.ev_start, c.main) != hipSuccess) return EMB_EHIP;
+  for (int s = 0; s < n_side; ++s)
+    if (hipStreamWaitEvent(c.side(s), c.ev_start, 0) != hipSuccess) return EMB_EHIP;
+  return c.ngroups > 1 ? run_threaded(c) : run_single(c);
 }
 
 }  // extern "C"

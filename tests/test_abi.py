@@ -214,8 +214,34 @@ def test_pipeline_steps_argument_checks():
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 0, sets, None, 1, sides, events) == emb.EMB_EINVAL      # group 0
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 2, sides, events) == emb.EMB_EINVAL      # sides > group
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 2, sets, None, 0, sides, events) == emb.EMB_EINVAL      # no side stream
+    many = (ctypes.c_void_p * 17)(*range(0x10, 0x10 + 17))
+    ev17 = (ctypes.c_void_p * 37)(*([0x40] * 37))
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 17, sets, None, 17, many, ev17) == emb.EMB_EUNSUPPORTED  # > 16 sides
     assert f(tb, 0, ub, 1, None, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_EINVAL
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, None, None, 1, sides, events) == emb.EMB_EINVAL
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 2, sets, None, 2, sides, no_events) == emb.EMB_EINVAL   # a null event
     same = (ctypes.c_void_p * 2)(0x10, 0x77)
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 2, sets, 0x77, 2, same, events) == emb.EMB_EINVAL       # side == main
+
+    # every step is checked before anything is enqueued: four steps in two
+    # groups of two, the last one bad in turn (a valid list would go on to
+    # enqueue, so it is not called here)
+    n = 4
+    wsb = L.emb_workspace_size(10, 1, t.dim)
+    good = emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000, wsb)
+    sets4 = (emb.CDedupSet * 4)(*([good] * 4))
+    b4 = (emb.CBatch * n)(*([emb.CBatch(1, 0x1000, 0x2000, 10, 4)] * n))
+    outs4 = (ctypes.c_void_p * n)(*([0x3000] * n))
+    grads4 = (ctypes.c_void_p * n)(*([0x3000] * n))
+    no_grad = (ctypes.c_void_p * n)(*([0x3000] * (n - 1) + [0]))
+    no_out = (ctypes.c_void_p * n)(*([0x3000] * (n - 1) + [0]))
+    assert f(tb, 0, ub, n, b4, outs4, no_grad, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, n, b4, no_out, grads4, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL
+    assert f(tb, 7, ub, n, b4, outs4, grads4, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL    # pool
+    small = (emb.CDedupSet * 4)(*([good] * 3 + [emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000,
+                                                              wsb - 256)]))
+    assert f(tb, 0, ub, n, b4, outs4, grads4, 2, small, None, 1, sides, events) == emb.EMB_EWORKSPACE
+    bad_b = (emb.CBatch * n)(*([emb.CBatch(1, 0x1000, 0x2000, 10, 4)] * (n - 1) + [emb.CBatch(1, 0x1000, 0, 10, 4)]))
+    assert f(tb, 0, ub, n, bad_b, outs4, grads4, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL
+    bad_upd = emb.CUpdate(9, 0.1, 0.0, None, 0, 0)
+    assert f(tb, 0, ctypes.byref(bad_upd), n, b4, outs4, grads4, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL

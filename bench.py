@@ -55,12 +55,15 @@ def parse():
     ap.add_argument("--bags", type=int, default=None, help="bags per table instead of the workload's own")
     ap.add_argument("--opt", choices=("sgd", "adagrad", "adagrad_ew"), default=None,
                     help="optimizer instead of the workload's own (adagrad_ew: element-wise, state [R][D])")
-    ap.add_argument("--schedule", choices=("pipelined", "auto", "serial", "concurrent"), default="pipelined",
+    ap.add_argument("--schedule", choices=("pipelined", "auto", "serial", "concurrent", "stale"),
+                    default="pipelined",
                     help="pipelined: the dedups of the next group of batches on side streams while the main "
                          "stream runs the forward and update of the current group; concurrent: the forward of a "
                          "batch on a side stream at the same time as its id dedup; serial: forward, dedup, "
                          "reduce + update one after another on one stream; auto: concurrent for batches of at "
-                         "least a million lookups, else serial")
+                         "least a million lookups, else serial; stale: the asynchronous schedule with "
+                         "staleness one (the forward of batch k+1 on a side stream, reading the table before "
+                         "the update of batch k, alongside the dedup of batch k)")
     ap.add_argument("--group", type=int, default=6, help="batches per group of the pipelined schedule")
     ap.add_argument("--side-streams", type=int, default=3,
                     help="side streams of the pipelined schedule (more than one: the dedups of a group run "
@@ -102,17 +105,23 @@ def file_sha(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def counter_traffic():
+def counter_traffic(workload: str):
     """HBM bytes per step of each phase from the committed rocprofv3 counter
     summary (FETCH_SIZE and WRITE_SIZE scaled by the copy-kernel calibration);
-    None for a phase whose kernel sources changed since the counters were taken."""
+    None for every phase of another workload than the one the counters were
+    taken on, and for a phase whose kernel sources changed since."""
     if not os.path.exists(COUNTERS):
         return None
     kv = {}
+    measured_on = None
     for line in open(COUNTERS):
+        if line.startswith("Workload: "):
+            measured_on = line[len("Workload: "):].strip()
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
+    if measured_on != workload:
+        return {phase: None for phase in PHASE_SOURCES}
     out = {}
     for phase, src in PHASE_SOURCES.items():
         try:
@@ -234,10 +243,12 @@ def main():
     n_warm = args.warmup
     t0_batch = n_warm
     total = n_warm + args.steps
+    # the stale schedule's last timed step runs the forward of one more batch
+    n_batches = total + (1 if args.schedule == "stale" else 0)
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
     t0 = time.time()
-    batches = [synth.make_batch(w, s) for s in range(total)]
-    print(f"[bench] generated {total} batches in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    batches = [synth.make_batch(w, s) for s in range(n_batches)]
+    print(f"[bench] generated {n_batches} batches in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
     W = torch.empty((w.total_rows, w.dim), dtype=torch.float32 if w.dtype == "fp32" else torch.bfloat16,
                     device=dev)
     synth.fill_device_weights(w, W.data_ptr(), int(torch.cuda.current_stream().cuda_stream))
@@ -290,6 +301,21 @@ def main():
 
         def run_steps(idx):
             pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in idx], sp)
+    elif args.schedule == "stale":
+        clayer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
+                           concurrent=True)
+
+        def run_steps(idx):
+            # step i: the forward of batch i + 1 (stale by the update of batch
+            # i) and the backward + update of batch i.  The warm-up starts with
+            # the forward of batch 0 and ends with that of the first timed
+            # batch, so every timed step is one whole forward and one whole
+            # backward + update.
+            idx = list(idx)
+            if idx and idx[0] == 0:
+                clayer.forward(dev_batches[0][0], out, sp)
+            for i in idx:
+                clayer.step_stale(dev_batches[i + 1][0], out, dev_batches[i][0], dev_batches[i][1], sp)
     else:
         def run_steps(idx):
             for i in idx:
@@ -454,7 +480,7 @@ def main():
     U_avg = float(np.mean(us))
     models = byte_models(w, N_avg, U_avg)
     t_phase = {k: float(np.mean(v)) for k, v in ph.items()}
-    traffic = counter_traffic()
+    traffic = counter_traffic(f"{w.name}: {w.description}")
     phases = {}
     for name, kern in (("fwd", "k_pool_fwd (emb_pool_fwd)"),
                        ("dedup", "k_sort_pass x passes + k_unique (emb_unique_ids)"),
@@ -479,6 +505,7 @@ def main():
         "config": {"workload": f"{w.name}: {w.description}", "rows": w.total_rows, "dim": w.dim,
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
                    "table_bytes": w.weight_bytes, "schedule": args.schedule,
+                   "staleness": 1 if args.schedule == "stale" else 0,
                    "group": args.group if args.schedule == "pipelined" else None,
                    "side_streams": args.side_streams if args.schedule == "pipelined" else None,
                    "overlapped_steps": args.steps if args.schedule == "pipelined" else

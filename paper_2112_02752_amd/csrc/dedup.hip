@@ -1132,6 +1132,10 @@ const void* pass_kernel(int it, int bits) {
 
 }  // namespace
 
+// the wait-free dedup uses 2048-key tiles up to this many tiles (about a
+// million keys), 4096-key tiles beyond
+constexpr int kWaitfreeSmallTiles = 512;
+
 hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   char* ws = static_cast<char*>(p.ws);
   const WsLayout& L = p.lay;
@@ -1182,14 +1186,25 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
     }
   }
   const int sort_cores = sort_it > 0 ? 1 : 0;
-  const int tile_keys = kSortThreads * (sort_cores ? sort_it : kSortItemsWide);
+  // Passes that read their offsets (reduce-then-scan): 4096-key tiles, or
+  // for the wait-free dedup of a batch of at most kWaitfreeSmallTiles
+  // 2048-key tiles (twice the workgroups, each ranking half as many keys:
+  // the pass is latency-bound, not bound by its column scan)
+  int rts_it = kSortItemsWide;
+  if (!sort_cores && p.waitfree &&
+      (N + kSortThreads * kSortItemsCore - 1) / (kSortThreads * kSortItemsCore) <= kWaitfreeSmallTiles)
+    rts_it = kSortItemsCore;
+  const int tile_keys = kSortThreads * (sort_cores ? sort_it : rts_it);
   const int sort_tiles = (N + tile_keys - 1) / tile_keys;
+  // int32 ids of one table are the keys: the first pass then reads them and
+  // finds each position's bag itself, with no prepare kernel
+  const bool first_pass_bags = p.T == 1 && !p.idx64;
   const int uniq_cores =
       !p.waitfree && uniq_tiles <= resident_blocks(reinterpret_cast<const void*>(&k_unique), kUniqThreads);
   uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
   hipError_t e = hipSuccess;
 
-  if (!sort_cores) {
+  if (!sort_cores && !first_pass_bags) {
     PrepArgs pa{};
     pa.offsets = p.offsets;
     pa.idx = p.idx;
@@ -1241,7 +1256,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
       xa.pass_shift[i] = p.plan.shift[i];
       xa.pass_bits[i] = p.plan.bits[i];
     }
-    xa.search_bags = sort_cores && ps == 0;
+    xa.search_bags = ps == 0 && (sort_cores || first_pass_bags);
     xa.offsets = p.offsets;
     xa.idx = p.idx;
     xa.idx64 = p.idx64;
@@ -1269,7 +1284,10 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
       ca.bits = xa.bits;
       ca.stride = status_stride;
       ca.counts = counts;
-      hipLaunchKernelGGL(k_tile_counts<kSortItemsWide>, dim3((unsigned)sort_tiles), dim3(kSortThreads), 0, s, ca);
+      if (rts_it == kSortItemsCore)
+        hipLaunchKernelGGL(k_tile_counts<kSortItemsCore>, dim3((unsigned)sort_tiles), dim3(kSortThreads), 0, s, ca);
+      else
+        hipLaunchKernelGGL(k_tile_counts<kSortItemsWide>, dim3((unsigned)sort_tiles), dim3(kSortThreads), 0, s, ca);
       if ((e = hipGetLastError()) != hipSuccess) return e;
       ColScanArgs sa{};
       sa.counts = counts;
@@ -1282,10 +1300,11 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
       if ((e = hipGetLastError()) != hipSuccess) return e;
       xa.prefix = counts;
     }
-    switch (sort_cores ? sort_it : kSortItemsWide) {
-      case kSortItemsCore: e = launch_pass_bits<kSortItemsCore>(xa, sort_tiles + prefix_blocks(ps), s); break;
-      case kSortItemsMid: e = launch_pass_bits<kSortItemsMid>(xa, sort_tiles + prefix_blocks(ps), s); break;
-      default: e = launch_pass_bits<kSortItemsWide>(xa, sort_tiles + (sort_cores ? prefix_blocks(ps) : 0), s);
+    const int extra = sort_cores ? prefix_blocks(ps) : 0;
+    switch (sort_cores ? sort_it : rts_it) {
+      case kSortItemsCore: e = launch_pass_bits<kSortItemsCore>(xa, sort_tiles + extra, s); break;
+      case kSortItemsMid: e = launch_pass_bits<kSortItemsMid>(xa, sort_tiles + extra, s); break;
+      default: e = launch_pass_bits<kSortItemsWide>(xa, sort_tiles + extra, s);
     }
     if (e != hipSuccess) return e;
     kin = xa.keys_out;

@@ -130,11 +130,10 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   L.uniq_status = off;
   off = align256(off + sizeof(uint64_t) * L.uniq_tiles);
   // plain digit counts of the passes whose tiles are not all resident at
-  // once (tiles of kSortThreads * kSortItemsWide keys); never shares bytes
-  // with the call-tagged words of the back region
+  // once (tiles of at least kSortTileMin keys); never shares bytes with the
+  // call-tagged words of the back region
   L.tile_counts = off;
-  off = align256(off + sizeof(uint32_t) * (size_t)((n + kSortThreads * kSortItemsWide - 1) / (kSortThreads * kSortItemsWide)) *
-                           kMaxDigits);
+  off = align256(off + sizeof(uint32_t) * (size_t)L.sort_tiles * kMaxDigits);
   L.chunk_seg = off;
   off = align256(off + sizeof(int32_t) * (L.chunks + 1));
   L.partials = off;

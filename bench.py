@@ -64,10 +64,13 @@ def parse():
                          "least a million lookups, else serial; stale: the asynchronous schedule with "
                          "staleness one (the forward of batch k+1 on a side stream, reading the table before "
                          "the update of batch k, alongside the dedup of batch k)")
-    ap.add_argument("--group", type=int, default=6, help="batches per group of the pipelined schedule")
+    ap.add_argument("--group", type=int, default=8, help="batches per group of the pipelined schedule")
     ap.add_argument("--side-streams", type=int, default=3,
-                    help="side streams of the pipelined schedule (more than one: the dedups of a group run "
-                         "concurrently with emb_unique_ids_concurrent)")
+                    help="side streams of the pipelined schedule with --dedup per-batch (more than one: the "
+                         "dedups of a group run concurrently with emb_unique_ids_concurrent)")
+    ap.add_argument("--dedup", choices=("group", "per-batch"), default="group",
+                    help="pipelined schedule: each group's dedups as one emb_unique_ids_batched call on one side "
+                         "stream (group), or one dedup per batch on the side streams (per-batch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
@@ -297,7 +300,7 @@ def main():
                 clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
     elif args.schedule == "pipelined":
         pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
-                            group=args.group, side_streams=args.side_streams)
+                            group=args.group, side_streams=args.side_streams, group_dedup=args.dedup == "group")
 
         def run_steps(idx):
             pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in idx], sp)
@@ -507,7 +510,8 @@ def main():
                    "table_bytes": w.weight_bytes, "schedule": args.schedule,
                    "staleness": 1 if args.schedule == "stale" else 0,
                    "group": args.group if args.schedule == "pipelined" else None,
-                   "side_streams": args.side_streams if args.schedule == "pipelined" else None,
+                   "dedup": args.dedup if args.schedule == "pipelined" else None,
+                   "side_streams": (pipe.S if pipe is not None else None),
                    "overlapped_steps": args.steps if args.schedule == "pipelined" else
                    sum(1 for i in range(t0_batch, total)
                        if clayer is not None and clayer.overlaps(dev_batches[i][2]))},

@@ -184,6 +184,28 @@ typedef struct {
   size_t ws_bytes;
 } emb_dedup_set;
 
+/* The dedups of n_batches batches (1..16) as one sort: each batch's key gets
+ * the batch's index above the key bits, so the sorted keys hold each batch's
+ * keys in turn, each in exactly the stable order of its own sort; each
+ * batch's share is then split off and its unique scan runs on it.  sets[i]
+ * receives, bit for bit, what emb_unique_ids(tables, &batches[i], sets[i]'s
+ * buffers) would leave there -- outputs, and in sets[i].ws the bag ids,
+ * chunk map and call record that emb_grad_reduce reads -- so each batch's
+ * gradient reduce follows as usual.  Same dedup as above (paper: Section
+ * "Multi-mode Execution", heterogeneous pipeline paragraph), one sort for a
+ * group of upcoming batches instead of one per batch: fewer, wider kernels.
+ * No workgroup waits for another (as emb_unique_ids_concurrent).
+ *   ws:  device, 256-byte aligned, ws_bytes >= emb_workspace_size(sum of
+ *        the batches' num_indices, sum of their bags, dim), initialised by
+ *        emb_workspace_init; used for this call only (its own state: pass
+ *        the same ws_bytes every call), distinct from every sets[i].ws.
+ *   sets[i].ws: as for emb_unique_ids, one per batch, all distinct.
+ * EMB_EUNSUPPORTED: more than 16 batches, a total of 2^30 ids or more, or
+ * key bits plus batch-index bits above 32 (tables of more than 2^(32 - b)
+ * rows for 2^b batches). */
+emb_status emb_unique_ids_batched(const emb_tables* tables, int32_t n_batches, const emb_batch* batches,
+                                  const emb_dedup_set* sets, void* ws, size_t ws_bytes, void* stream);
+
 /* n_steps training steps of the layer enqueued with the pipelined schedule:
  * step k pools batches[k] into outs[k] (device fp32 [M][D]) and applies the
  * fused backward and optimizer step with grads[k] (device fp32 [M][D]), in
@@ -196,7 +218,11 @@ typedef struct {
  * Execution", heterogeneous pipeline paragraph), here with no staleness.
  * With n_side = 1 the dedups are emb_unique_ids, one at a time; with
  * n_side > 1 they are emb_unique_ids_concurrent (no workgroup waits for
- * another), several at a time.
+ * another), several at a time.  With group_ws non-NULL (n_side must be 1,
+ * group at most 16) the dedups of a group are one emb_unique_ids_batched
+ * call with group_ws as its workspace (device, group_ws_bytes >=
+ * emb_workspace_size of a whole group's ids and bags, initialised by
+ * emb_workspace_init); NULL otherwise.
  *   sets:    host [2 * group] buffer sets, used alternately by groups
  *   events:  host [3 + 2 * n_side] hipEvent_t created by the caller (no
  *            timing needed); the library only records and waits on them
@@ -216,7 +242,8 @@ typedef struct {
 emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_update* update, int32_t n_steps,
                               const emb_batch* batches, float* const* outs, const float* const* grads,
                               int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,
-                              void* const* side_streams, void* const* events);
+                              void* const* side_streams, void* const* events, void* group_ws,
+                              size_t group_ws_bytes);
 
 /* Backward segment-reduce (the gradient the embedding stage pushes back,
  * paper: Section "Multi-mode Execution", heterogeneous pipeline paragraph),

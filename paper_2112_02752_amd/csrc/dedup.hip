@@ -61,6 +61,7 @@ struct PrepArgs {
   int32_t B, M, bags_per_block;
   uint32_t* keys_out;  // null for int32 ids of one table (the ids are the keys)
   int32_t* bag_of;
+  uint32_t key_hi;     // or-ed into every key (a group dedup's batch index bits; 0 otherwise)
 };
 
 // Used when the tiles of a pass are not all resident at once.  A block owns a
@@ -68,11 +69,13 @@ struct PrepArgs {
 // staged in LDS; every thread takes positions of the range in strides, finds
 // each one's bag by a binary search in LDS, and writes the bag id (and the key
 // for several tables).
-__global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
+// `a` supplies offsets, idx, idx64, ro, B, M, bags_per_block, keys_out,
+// bag_of and key_hi (one batch's, with keys_out and bag_of at its positions)
+template <typename A>
+__device__ __forceinline__ void prepare_block(const A& a, int block, int32_t* s_off) {
   constexpr int UN = 8;
-  __shared__ int32_t s_off[kPrepMaxBags + 1];
   const int tid = threadIdx.x;
-  const int m0 = blockIdx.x * a.bags_per_block;
+  const int m0 = block * a.bags_per_block;
   const int nb = min(a.M - m0, a.bags_per_block);
   for (int i = tid; i <= nb; i += kPrepThreads) s_off[i] = a.offsets[m0 + i];
   __syncthreads();
@@ -95,12 +98,17 @@ __global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
           if (s_off[mid] <= j) lo = mid; else hi = mid - 1;
         }
         const int m = m0 + lo;
-        const uint32_t key = a.ro.off[m / a.B] + (uint32_t)id[u];
+        const uint32_t key = (a.ro.off[m / a.B] + (uint32_t)id[u]) | a.key_hi;
         a.bag_of[j] = m;
         if (a.keys_out) a.keys_out[j] = key;
       }
     }
   }
+}
+
+__global__ __launch_bounds__(kPrepThreads) void k_prepare(PrepArgs a) {
+  __shared__ int32_t s_off[kPrepMaxBags + 1];
+  prepare_block(a, blockIdx.x, s_off);
 }
 
 // ------------------------------------------------------------- sort pass
@@ -798,6 +806,7 @@ struct UniqArgs {
   const uint64_t* prefix;  // reduce-then-scan: each tile's (heads, last head position + 1) over the
                            // tiles before it, from k_uniq_counts and k_uniq_scan; null: look-back
   WsHeader* hdr;
+  uint32_t key_mask;       // applied to the keys written out (a group dedup drops the batch index bits)
 };
 
 // status word: flag [63:62], head count [61:31], last head position + 1 [30:0]
@@ -816,11 +825,10 @@ struct UniqCountArgs {
   uint64_t* out;  // [tiles]: pack_uniq(0, heads, last head position + 1)
 };
 
-__global__ __launch_bounds__(kUniqThreads) void k_uniq_counts(UniqCountArgs a) {
+__device__ __forceinline__ void uniq_counts_tile(const UniqCountArgs& a, int tile, uint32_t* s_c, uint32_t* s_q) {
   constexpr int NW = kUniqThreads / kWave;
-  __shared__ uint32_t s_c[NW], s_q[NW];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  const int64_t tbase = (int64_t)blockIdx.x * kUniqTile;
+  const int64_t tbase = (int64_t)tile * kUniqTile;
   uint32_t cur[kUniqItems], prv[kUniqItems];
 #pragma unroll
   for (int i = 0; i < kUniqItems; ++i) {
@@ -853,14 +861,17 @@ __global__ __launch_bounds__(kUniqThreads) void k_uniq_counts(UniqCountArgs a) {
       tc += s_c[ww];
       tq = max(tq, s_q[ww]);
     }
-    a.out[blockIdx.x] = pack_uniq(0, tc, tq);
+    a.out[tile] = pack_uniq(0, tc, tq);
   }
 }
 
+__global__ __launch_bounds__(kUniqThreads) void k_uniq_counts(UniqCountArgs a) {
+  __shared__ uint32_t s_c[kUniqThreads / kWave], s_q[kUniqThreads / kWave];
+  uniq_counts_tile(a, blockIdx.x, s_c, s_q);
+}
+
 constexpr int kUniqScanThreads = 1024;
-__global__ __launch_bounds__(kUniqScanThreads) void k_uniq_scan(uint64_t* words, int32_t tiles) {
-  constexpr int NW = kUniqScanThreads / kWave;
-  __shared__ uint32_t s_c[NW], s_q[NW];
+__device__ __forceinline__ void uniq_scan_block(uint64_t* words, int32_t tiles, uint32_t* s_c, uint32_t* s_q) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
   const int per = (tiles + kUniqScanThreads - 1) / kUniqScanThreads;
   const int t0 = min(tiles, tid * per), t1 = min(tiles, t0 + per);
@@ -891,13 +902,17 @@ __global__ __launch_bounds__(kUniqScanThreads) void k_uniq_scan(uint64_t* words,
   }
 }
 
-__global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
+__global__ __launch_bounds__(kUniqScanThreads) void k_uniq_scan(uint64_t* words, int32_t tiles) {
+  __shared__ uint32_t s_c[kUniqScanThreads / kWave], s_q[kUniqScanThreads / kWave];
+  uniq_scan_block(words, tiles, s_c, s_q);
+}
+
+__device__ __forceinline__ void unique_tile(const UniqArgs& a, const int tile) {
   constexpr int NW = kUniqThreads / kWave;
   __shared__ uint32_t s_keys[kUniqTile];
   __shared__ uint32_t s_wc[NW], s_wq[NW];
   __shared__ uint32_t s_pc, s_pq, s_prev, s_fail;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
-  const int tile = blockIdx.x;
   const int64_t tbase = (int64_t)tile * kUniqTile;
   const bool last_tile = tbase + kUniqTile >= (int64_t)a.N;
   // this call's generation (its first sort pass recorded it); the sort is
@@ -1059,7 +1074,7 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     const int64_t pos = tbase + s;
     if (pos < a.N) {
       if (heads & (1u << i)) {
-        a.ukeys[u] = s_keys[s];
+        a.ukeys[u] = s_keys[s] & a.key_mask;
         a.seg[u] = (int32_t)pos;
         if (u > 0) a.counts[u - 1] = (int32_t)pos - (int32_t)(lastq - 1u);
         lastq = (uint32_t)pos + 1u;
@@ -1075,6 +1090,8 @@ __global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) {
     }
   }
 }
+
+__global__ __launch_bounds__(kUniqThreads) void k_unique(UniqArgs a) { unique_tile(a, blockIdx.x); }
 
 __global__ void k_unique_empty(int32_t* num_unique, int32_t* seg) {
   if (threadIdx.x == 0) {
@@ -1324,6 +1341,7 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   ua.chunk_seg = reinterpret_cast<int32_t*>(ws + L.chunk_seg);
   ua.status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
   ua.prev_totals = reinterpret_cast<uint32_t*>(ws + L.totals) + (p.plan.passes - 1) * kMaxDigits;
+  ua.key_mask = 0xffffffffu;
   if (!uniq_cores) {
     // reduce-then-scan: tile head counts, then their scan over the tiles
     UniqCountArgs uc{};
@@ -1338,6 +1356,340 @@ hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s) {
   }
   ua.hdr = hdr;
   hipLaunchKernelGGL(k_unique, dim3((unsigned)uniq_tiles), dim3(kUniqThreads), 0, s, ua);
+  return hipGetLastError();
+}
+
+}  // namespace emb
+
+// ------------------------------------------------------------ group dedup
+//
+// The batches of a group are sorted as one: every key carries its batch's
+// index above the key bits, so the sorted keys hold batch 0's keys first,
+// then batch 1's, and within each batch exactly the stable order of its own
+// sort.  Each batch's share (its positions [P_i, P_i + N_i) of the sorted
+// order) is then split off into its own permutation and bag ids, and its
+// unique scan runs on its share alone, into its own outputs and workspace.
+// No workgroup of any of these kernels waits for another.
+
+namespace emb {
+
+namespace {
+
+// the member a block belongs to: the last i with first[i] <= blk
+__device__ __forceinline__ int group_member(const int32_t* first, int n, int blk) {
+  int i = 0;
+  while (i + 1 < n && first[i + 1] <= blk) ++i;
+  return i;
+}
+
+struct PrepView {  // one batch's prepare arguments, in the form prepare_block reads
+  const int32_t* offsets;
+  const void* idx;
+  int32_t idx64;
+  const TableOffsets& ro;
+  int32_t B, M, bags_per_block;
+  uint32_t* keys_out;
+  int32_t* bag_of;
+  uint32_t key_hi;
+};
+
+struct PrepMember {
+  const int32_t* offsets;
+  const void* idx;
+  int64_t P;
+  int32_t idx64, B, M, bags_per_block;
+};
+
+struct PrepGroupArgs {
+  int32_t n, key_bits;
+  int32_t first[kMaxGroup + 1];  // first block of each member; first[n] = grid
+  PrepMember b[kMaxGroup];
+  uint32_t* keys_out;            // the group's keys, all members' positions
+  int32_t* bag_of;               // the group's bag ids (each member's own bag numbers)
+  TableOffsets ro;
+};
+
+__global__ __launch_bounds__(kPrepThreads) void k_prepare_group(PrepGroupArgs a) {
+  __shared__ int32_t s_off[kPrepMaxBags + 1];
+  const int i = group_member(a.first, a.n, (int)blockIdx.x);
+  const PrepMember& m = a.b[i];
+  const PrepView v{m.offsets, m.idx, m.idx64, a.ro, m.B, m.M, m.bags_per_block, a.keys_out + m.P, a.bag_of + m.P,
+                   i == 0 ? 0u : (uint32_t)i << a.key_bits};
+  prepare_block(v, (int)blockIdx.x - a.first[i], s_off);
+}
+
+struct SplitMember {
+  int64_t P;
+  int32_t N;
+  int32_t* sort_perm;
+  int32_t* sorted_bag;
+  int32_t* num_unique;
+  int32_t* seg_offsets;
+  WsHeader* hdr;
+};
+
+struct SplitGroupArgs {
+  int32_t n, sorted;             // sorted: the group's passes ran
+  int32_t first[kMaxGroup + 1];
+  SplitMember b[kMaxGroup];
+  const int32_t* perm;           // the group's sort permutation (group positions)
+  const int32_t* bags;           // bag ids of the group's sorted positions
+  WsHeader* ghdr;                // the group's workspace header
+};
+
+constexpr int kSplitThreads = 256;
+constexpr int kSplitItems = 8;
+
+__global__ __launch_bounds__(kSplitThreads) void k_split_group(SplitGroupArgs a) {
+  const int i = group_member(a.first, a.n, (int)blockIdx.x);
+  const SplitMember& m = a.b[i];
+  const int lb = (int)blockIdx.x - a.first[i];
+  const int tid = threadIdx.x;
+  if (lb == 0 && tid == 0) {
+    if (m.N == 0) {
+      m.num_unique[0] = 0;
+      m.seg_offsets[0] = 0;
+    } else {
+      // the member's own call generation; the group sort's error bits become
+      // its own, so that its unique scan and gradient reduce see them
+      const uint32_t g = next_gen(m.hdr->gen);
+      m.hdr->cur = g;
+      const uint32_t bits = call_errors(a.ghdr, a.ghdr->cur) & kDedupErrors;
+      if (bits) flag_error(m.hdr, g, bits);
+    }
+  }
+  // the group call is complete: its generation becomes the group header's
+  if (blockIdx.x == 0 && tid == 0 && a.sorted) a.ghdr->gen = a.ghdr->cur;
+  const int64_t base = (int64_t)lb * (kSplitThreads * kSplitItems);
+#pragma unroll
+  for (int k = 0; k < kSplitItems; ++k) {
+    const int64_t j = base + k * kSplitThreads + tid;
+    if (j < m.N) {
+      m.sort_perm[j] = a.perm[m.P + j] - (int32_t)m.P;
+      m.sorted_bag[j] = a.bags[m.P + j];
+    }
+  }
+}
+
+struct UniqMember {
+  int64_t P;
+  int32_t N, ntiles, nchunks;
+  uint32_t* unique_keys;
+  int32_t* counts;
+  int32_t* seg_offsets;
+  int32_t* num_unique;
+  int32_t* chunk_seg;
+  uint64_t* words;
+  uint32_t* totals;
+  WsHeader* hdr;
+};
+
+struct UniqGroupArgs {
+  int32_t n;
+  uint32_t key_mask;
+  int32_t first[kMaxGroup + 1];  // first unique tile block of each member
+  UniqMember b[kMaxGroup];
+  const uint32_t* skeys;         // the group's sorted keys
+};
+
+__global__ __launch_bounds__(kUniqThreads) void k_uniq_counts_group(UniqGroupArgs a) {
+  __shared__ uint32_t s_c[kUniqThreads / kWave], s_q[kUniqThreads / kWave];
+  const int i = group_member(a.first, a.n, (int)blockIdx.x);
+  const UniqMember& m = a.b[i];
+  const UniqCountArgs c{a.skeys + m.P, m.N, m.words};
+  uniq_counts_tile(c, (int)blockIdx.x - a.first[i], s_c, s_q);
+}
+
+__global__ __launch_bounds__(kUniqScanThreads) void k_uniq_scan_group(UniqGroupArgs a) {
+  __shared__ uint32_t s_c[kUniqScanThreads / kWave], s_q[kUniqScanThreads / kWave];
+  const UniqMember& m = a.b[blockIdx.x];
+  if (m.N > 0) uniq_scan_block(m.words, m.ntiles, s_c, s_q);
+}
+
+__global__ __launch_bounds__(kUniqThreads) void k_unique_group(UniqGroupArgs a) {
+  const int i = group_member(a.first, a.n, (int)blockIdx.x);
+  const UniqMember& m = a.b[i];
+  UniqArgs u{};
+  u.skeys = a.skeys + m.P;
+  u.N = m.N;
+  u.ntiles = m.ntiles;
+  u.nchunks = m.nchunks;
+  u.ukeys = m.unique_keys;
+  u.counts = m.counts;
+  u.seg = m.seg_offsets;
+  u.num_unique = m.num_unique;
+  u.chunk_seg = m.chunk_seg;
+  u.status = m.words;
+  u.prev_totals = m.totals;
+  u.prefix = m.words;
+  u.hdr = m.hdr;
+  u.key_mask = a.key_mask;
+  unique_tile(u, (int)blockIdx.x - a.first[i]);
+}
+
+}  // namespace
+
+hipError_t launch_dedup_group(const GroupDedupLaunch& p, hipStream_t s) {
+  char* ws = static_cast<char*>(p.ws);
+  const WsLayout& L = p.lay;
+  char* back = ws_back(p.ws, p.ws_bytes, L);
+  WsHeader* ghdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+  const int n = p.n;
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  hipError_t e = hipSuccess;
+  uint32_t* keys_built = reinterpret_cast<uint32_t*>(ws + L.keys_built);
+  int32_t* bag_of = reinterpret_cast<int32_t*>(ws + L.bag_of);
+  uint32_t* sorted_keys = reinterpret_cast<uint32_t*>(ws + L.sorted_keys);
+  int32_t* group_perm = reinterpret_cast<int32_t*>(ws + L.group_perm);
+  int32_t* sorted_bag = reinterpret_cast<int32_t*>(ws + L.sorted_bag);
+
+  if (p.N > 0) {
+    const int N = (int)p.N;
+    // keys (with the member index above the key bits) and bag ids of all positions
+    PrepGroupArgs pa{};
+    pa.n = n;
+    pa.key_bits = p.key_bits;
+    pa.keys_out = keys_built;
+    pa.bag_of = bag_of;
+    pa.ro = p.ro;
+    int blocks = 0;
+    for (int i = 0; i < n; ++i) {
+      const GroupMember& m = p.m[i];
+      pa.first[i] = blocks;
+      pa.b[i] = PrepMember{m.offsets, m.idx, m.P, m.idx64, m.B, m.M, m.bags_per_block};
+      if (m.N > 0 && m.M > 0) blocks += (m.M + m.bags_per_block - 1) / m.bags_per_block;
+    }
+    pa.first[n] = blocks;
+    if (blocks > 0) {
+      hipLaunchKernelGGL(k_prepare_group, dim3((unsigned)blocks), dim3(kPrepThreads), 0, s, pa);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+
+    // the radix passes over all positions: reduce-then-scan, tile offsets
+    // computed before each pass (no workgroup waits for another)
+    const int it = (N + kSortThreads * kSortItemsCore - 1) / (kSortThreads * kSortItemsCore) <= kWaitfreeSmallTiles
+                       ? kSortItemsCore
+                       : kSortItemsWide;
+    const int tile_keys = kSortThreads * it;
+    const int sort_tiles = (N + tile_keys - 1) / tile_keys;
+    int max_bits = 1;
+    for (int i = 0; i < p.plan.passes; ++i) max_bits = p.plan.bits[i] > max_bits ? p.plan.bits[i] : max_bits;
+    const int status_stride = 1 << max_bits;
+    const uint32_t* kin = keys_built;
+    const int32_t* vin = nullptr;
+    const int32_t* bin = bag_of;
+    uint32_t* keys_a = reinterpret_cast<uint32_t*>(ws + L.keys_a);
+    uint32_t* keys_b = reinterpret_cast<uint32_t*>(ws + L.keys_b);
+    int32_t* vals_a = reinterpret_cast<int32_t*>(ws + L.vals_a);
+    int32_t* vals_b = reinterpret_cast<int32_t*>(ws + L.vals_b);
+    int32_t* bags_a = reinterpret_cast<int32_t*>(ws + L.bags_a);
+    int32_t* bags_b = reinterpret_cast<int32_t*>(ws + L.bags_b);
+    uint32_t* counts = reinterpret_cast<uint32_t*>(ws + L.tile_counts);
+    for (int ps = 0; ps < p.plan.passes; ++ps) {
+      const bool last = ps == p.plan.passes - 1;
+      PassArgs xa{};
+      xa.keys_in = kin;
+      xa.vals_in = vin;
+      xa.bags_in = bin;
+      xa.keys_out = last ? sorted_keys : ((ps % 2 == 0) ? keys_a : keys_b);
+      xa.vals_out = last ? group_perm : ((ps % 2 == 0) ? vals_a : vals_b);
+      xa.bags_out = last ? sorted_bag : ((ps % 2 == 0) ? bags_a : bags_b);
+      xa.totals = reinterpret_cast<uint32_t*>(ws + L.totals) + ps * kMaxDigits;
+      xa.prev_totals = ps > 0 ? reinterpret_cast<uint32_t*>(ws + L.totals) + (ps - 1) * kMaxDigits : nullptr;
+      xa.status = reinterpret_cast<uint64_t*>(back + L.pass_status);
+      xa.rows = reinterpret_cast<uint64_t*>(back + L.rows);
+      xa.grp = reinterpret_cast<uint64_t*>(back + L.grp);
+      xa.coresident = 0;
+      xa.prefix_mode = kPrefixGroups;
+      xa.later = nullptr;
+      xa.totals_all = reinterpret_cast<uint32_t*>(ws + L.totals);
+      xa.npass = p.plan.passes;
+      for (int i = 0; i < kMaxPasses; ++i) {
+        xa.pass_shift[i] = p.plan.shift[i];
+        xa.pass_bits[i] = p.plan.bits[i];
+      }
+      xa.search_bags = 0;
+      xa.T = p.T;
+      xa.uniq_status = reinterpret_cast<uint64_t*>(ws + L.uniq_status);
+      xa.uniq_tiles = 0;  // the members' unique scans use their own words
+      xa.hdr = ghdr;
+      xa.N = N;
+      xa.ntiles = sort_tiles;
+      xa.shift = p.plan.shift[ps];
+      xa.bits = p.plan.bits[ps];
+      xa.pass = ps;
+      xa.status_stride = status_stride;
+      CountArgs ca{};
+      ca.keys = kin;
+      ca.N = N;
+      ca.shift = xa.shift;
+      ca.bits = xa.bits;
+      ca.stride = status_stride;
+      ca.counts = counts;
+      if (it == kSortItemsCore)
+        hipLaunchKernelGGL(k_tile_counts<kSortItemsCore>, dim3((unsigned)sort_tiles), dim3(kSortThreads), 0, s, ca);
+      else
+        hipLaunchKernelGGL(k_tile_counts<kSortItemsWide>, dim3((unsigned)sort_tiles), dim3(kSortThreads), 0, s, ca);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      ColScanArgs sa{};
+      sa.counts = counts;
+      sa.totals = xa.totals;
+      sa.tiles = sort_tiles;
+      sa.nd = 1 << xa.bits;
+      sa.stride = status_stride;
+      hipLaunchKernelGGL(k_column_scan, dim3((unsigned)((sa.nd + kColDigits - 1) / kColDigits)),
+                         dim3(kColDigits * kColChunks), 0, s, sa);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      xa.prefix = counts;
+      e = it == kSortItemsCore ? launch_pass_bits<kSortItemsCore>(xa, sort_tiles, s)
+                               : launch_pass_bits<kSortItemsWide>(xa, sort_tiles, s);
+      if (e != hipSuccess) return e;
+      kin = xa.keys_out;
+      vin = xa.vals_out;
+      bin = xa.bags_out;
+    }
+  }
+
+  // each member's share of the sorted order, and its call generation
+  SplitGroupArgs sa{};
+  sa.n = n;
+  sa.sorted = p.N > 0 ? 1 : 0;
+  sa.perm = group_perm;
+  sa.bags = sorted_bag;
+  sa.ghdr = ghdr;
+  int sblocks = 0;
+  for (int i = 0; i < n; ++i) {
+    const GroupMember& m = p.m[i];
+    sa.first[i] = sblocks;
+    sa.b[i] = SplitMember{m.P, m.N, m.sort_perm, m.sorted_bag, m.num_unique, m.seg_offsets, m.hdr};
+    const int per = kSplitThreads * kSplitItems;
+    sblocks += m.N > 0 ? (m.N + per - 1) / per : 1;
+  }
+  sa.first[n] = sblocks;
+  hipLaunchKernelGGL(k_split_group, dim3((unsigned)sblocks), dim3(kSplitThreads), 0, s, sa);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (p.N == 0) return hipSuccess;
+
+  // each member's unique scan on its share
+  UniqGroupArgs ua{};
+  ua.n = n;
+  ua.key_mask = p.key_bits >= 32 ? 0xffffffffu : ((1u << p.key_bits) - 1u);
+  ua.skeys = sorted_keys;
+  int tiles = 0;
+  for (int i = 0; i < n; ++i) {
+    const GroupMember& m = p.m[i];
+    ua.first[i] = tiles;
+    const int nt = (m.N + kUniqTile - 1) / kUniqTile;
+    ua.b[i] = UniqMember{m.P, m.N, nt, (m.N + kChunk - 1) / kChunk, m.unique_keys, m.counts, m.seg_offsets,
+                         m.num_unique, m.chunk_seg, m.uniq_words, m.totals, m.hdr};
+    tiles += nt;
+  }
+  ua.first[n] = tiles;
+  hipLaunchKernelGGL(k_uniq_counts_group, dim3((unsigned)tiles), dim3(kUniqThreads), 0, s, ua);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_uniq_scan_group, dim3((unsigned)n), dim3(kUniqScanThreads), 0, s, ua);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_unique_group, dim3((unsigned)tiles), dim3(kUniqThreads), 0, s, ua);
   return hipGetLastError();
 }
 

@@ -136,6 +136,29 @@ emb_status route_prepare(const emb_tables* tables, const emb_batch* batch, int32
 
 namespace emb {
 
+emb_status check_dedup_group(const emb_tables* tables, int32_t n_batches, const emb_batch* batches, const void* ws,
+                             size_t ws_bytes) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  if (n_batches < 1 || batches == nullptr) return EMB_EINVAL;
+  if (n_batches > kMaxGroup) return EMB_EUNSUPPORTED;
+  int gb = 0;
+  while ((1 << gb) < n_batches) ++gb;
+  if (key_bits_for(R) + gb > 32) return EMB_EUNSUPPORTED;
+  int64_t N = 0, M = 0;
+  for (int i = 0; i < n_batches; ++i) {
+    int32_t m = 0;
+    if ((st = check_batch(&batches[i], tables->num_tables, &m)) != EMB_OK) return st;
+    N += batches[i].num_indices;
+    M += m;
+  }
+  if (N >= kMaxIndices) return EMB_EUNSUPPORTED;
+  WsLayout lay;
+  return check_ws(ws, ws_bytes, N, M, tables->dim, &lay);
+}
+
 // Every host check that emb_pool_fwd, emb_unique_ids (or _concurrent) and a
 // fused emb_grad_reduce would make for one step of the pipelined schedule,
 // so that the schedule can reject a bad step before it enqueues anything.
@@ -257,6 +280,72 @@ static emb_status unique_ids(const emb_tables* tables, const emb_batch* batch, u
   p.num_unique = num_unique;
   p.waitfree = waitfree;
   return hip_status(launch_dedup(p, (hipStream_t)stream));
+}
+
+emb_status emb_unique_ids_batched(const emb_tables* tables, int32_t n_batches, const emb_batch* batches,
+                                  const emb_dedup_set* sets, void* ws, size_t ws_bytes, void* stream) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  if (n_batches < 1 || batches == nullptr || sets == nullptr) return EMB_EINVAL;
+  if (n_batches > kMaxGroup) return EMB_EUNSUPPORTED;
+  const int kb = key_bits_for(R);
+  int gb = 0;
+  while ((1 << gb) < n_batches) ++gb;
+  if (kb + gb > 32) return EMB_EUNSUPPORTED;  // the batch index must fit above the key bits
+  GroupDedupLaunch p{};
+  p.n = n_batches;
+  p.ro = ro;
+  p.T = tables->num_tables;
+  p.key_bits = kb;
+  int64_t Ntot = 0, Mtot = 0;
+  for (int i = 0; i < n_batches; ++i) {
+    const emb_batch* b = &batches[i];
+    const emb_dedup_set& d = sets[i];
+    int32_t M = 0;
+    if ((st = check_batch(b, tables->num_tables, &M)) != EMB_OK) return st;
+    if (d.seg_offsets == nullptr || d.num_unique == nullptr) return EMB_EINVAL;
+    if (b->num_indices > 0 && (d.unique_keys == nullptr || d.counts == nullptr || d.sort_perm == nullptr))
+      return EMB_EINVAL;
+    WsLayout li;
+    if ((st = check_ws(d.ws, d.ws_bytes, b->num_indices, M, tables->dim, &li)) != EMB_OK) return st;
+    // each batch's workspace is its own: not the group's, not another batch's
+    if (d.ws == ws) return EMB_EINVAL;
+    for (int j = 0; j < i; ++j)
+      if (sets[j].ws == d.ws) return EMB_EINVAL;
+    GroupMember& m = p.m[i];
+    m.offsets = b->offsets;
+    m.idx = b->indices;
+    m.idx64 = b->index_bytes == 8;
+    m.B = b->bags_per_table;
+    m.M = M;
+    m.N = (int32_t)b->num_indices;
+    m.P = Ntot;
+    // about kPrepPositions positions per prepare block, as for one batch
+    const int64_t want = m.N > 0 ? (int64_t)kPrepPositions * M / m.N : 1;
+    m.bags_per_block = (int32_t)(want < 1 ? 1 : (want > kPrepMaxBags ? kPrepMaxBags : want));
+    char* w = static_cast<char*>(d.ws);
+    m.unique_keys = d.unique_keys;
+    m.counts = d.counts;
+    m.seg_offsets = d.seg_offsets;
+    m.sort_perm = d.sort_perm;
+    m.num_unique = d.num_unique;
+    m.sorted_bag = reinterpret_cast<int32_t*>(w + li.sorted_bag);
+    m.chunk_seg = reinterpret_cast<int32_t*>(w + li.chunk_seg);
+    m.uniq_words = reinterpret_cast<uint64_t*>(w + li.uniq_status);
+    m.totals = reinterpret_cast<uint32_t*>(w + li.totals);
+    m.hdr = reinterpret_cast<WsHeader*>(w + li.hdr);
+    Ntot += m.N;
+    Mtot += M;
+  }
+  if (Ntot >= kMaxIndices) return EMB_EUNSUPPORTED;
+  if ((st = check_ws(ws, ws_bytes, Ntot, Mtot, tables->dim, &p.lay)) != EMB_OK) return st;
+  p.N = Ntot;
+  p.plan = make_sort_plan(kb + gb);
+  p.ws = ws;
+  p.ws_bytes = ws_bytes;
+  return hip_status(launch_dedup_group(p, (hipStream_t)stream));
 }
 
 emb_status emb_unique_ids(const emb_tables* tables, const emb_batch* batch, uint32_t* unique_keys, int32_t* counts,

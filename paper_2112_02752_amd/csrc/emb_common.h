@@ -83,8 +83,8 @@ static_assert(sizeof(WsHeader) == 256, "header is one 256-byte block");
 // tags differ.
 struct WsLayout {
   // front (offsets from the workspace base)
-  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_keys, sorted_bag, uniq_status,
-      tile_counts, chunk_seg, partials, level2, arrivals, front;
+  size_t hdr, totals, keys_built, keys_a, keys_b, vals_a, vals_b, bags_a, bags_b, bag_of, sorted_keys, sorted_bag,
+      group_perm, uniq_status, tile_counts, chunk_seg, partials, level2, arrivals, front;
   // back (offsets from the back base)
   size_t pass_status, rows, grp, later, back;
   size_t total;
@@ -126,6 +126,10 @@ inline WsLayout ws_layout(int64_t N, int64_t M, int32_t D) {
   L.sorted_keys = off;
   off = align256(off + n4);
   L.sorted_bag = off;
+  off = align256(off + n4);
+  // a group dedup's sort permutation (positions of all its batches), before
+  // each batch's share is split off
+  L.group_perm = off;
   off = align256(off + n4);
   L.uniq_status = off;
   off = align256(off + sizeof(uint64_t) * L.uniq_tiles);

@@ -49,6 +49,41 @@ struct DedupLaunch {
 };
 hipError_t launch_dedup(const DedupLaunch& p, hipStream_t s);
 
+// A group dedup: the batches of a group sorted as one, each key carrying its
+// batch's index above the key bits, then each batch's share split off into
+// its own outputs and workspace, exactly as its own dedup would leave them.
+constexpr int kMaxGroup = 16;
+struct GroupMember {
+  const int32_t* offsets;
+  const void* idx;
+  int32_t idx64, B, M, N;
+  int64_t P;                   // first position of this batch among the group's positions
+  int32_t bags_per_block;      // of its prepare blocks
+  uint32_t* unique_keys;       // its outputs, as emb_unique_ids fills them
+  int32_t* counts;
+  int32_t* seg_offsets;
+  int32_t* sort_perm;
+  int32_t* num_unique;
+  int32_t* sorted_bag;         // in its own workspace (what its gradient reduce reads)
+  int32_t* chunk_seg;
+  uint64_t* uniq_words;        // its unique scan's per-tile words
+  uint32_t* totals;            // a row of its workspace's digit totals (cleared by its unique scan)
+  WsHeader* hdr;
+};
+struct GroupDedupLaunch {
+  int32_t n;
+  GroupMember m[kMaxGroup];
+  TableOffsets ro;
+  int32_t T;
+  int32_t key_bits;            // bits of a key without the batch index
+  int64_t N;                   // positions of all the batches
+  SortPlan plan;               // over key_bits + the batch index bits
+  void* ws;                    // the group's own workspace
+  size_t ws_bytes;
+  WsLayout lay;
+};
+hipError_t launch_dedup_group(const GroupDedupLaunch& p, hipStream_t s);
+
 struct ReduceLaunch {
   const float* grad_out;
   const int32_t* perm;
@@ -124,6 +159,11 @@ struct ValidateLaunch {
 hipError_t launch_validate(const ValidateLaunch& p, hipStream_t s);
 hipError_t launch_zero_bytes(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_workspace_status(const void* ws, int32_t* status, hipStream_t s);
+
+// host checks of a group of batches for emb_unique_ids_batched's group
+// workspace: the number of batches, key bits, total ids and workspace size
+emb_status check_dedup_group(const emb_tables* tables, int32_t n_batches, const emb_batch* batches, const void* ws,
+                             size_t ws_bytes);
 
 // host checks of one step of emb_pipeline_steps (defined with the C ABI)
 emb_status check_pipeline_step(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* out,

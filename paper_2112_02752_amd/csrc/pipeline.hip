@@ -48,6 +48,8 @@ struct Schedule {
   void* const* sides;
   hipEvent_t ev_start, ev_main[2];
   void* const* events;
+  void* group_ws;  // non-null: each group's dedups as one emb_unique_ids_batched call
+  size_t group_ws_bytes;
 
   hipEvent_t ev_side(int parity, int s) const { return (hipEvent_t)events[3 + parity * n_side + s]; }
   hipStream_t side(int s) const { return (hipStream_t)sides[s]; }
@@ -70,6 +72,13 @@ emb_status dedup_one(const Schedule& c, int k, const emb_dedup_set& d, void* str
 emb_status side_group(const Schedule& c, int g, int s) {
   const int par = g % 2;
   if (g >= 2 && hipStreamWaitEvent(c.side(s), c.ev_main[par], 0) != hipSuccess) return EMB_EHIP;
+  if (c.group_ws != nullptr) {
+    const int count = c.n_steps - g * c.K < c.K ? c.n_steps - g * c.K : c.K;
+    const emb_status r = emb_unique_ids_batched(c.tables, count, &c.batches[g * c.K], &c.sets[par * c.K], c.group_ws,
+                                                c.group_ws_bytes, c.sides[s]);
+    if (r != EMB_OK) return r;
+    return hip_ok(hipEventRecord(c.ev_side(par, s), c.side(s)));
+  }
   for (int i = s; i < c.K && g * c.K + i < c.n_steps; i += c.n_side) {
     const emb_status r = dedup_one(c, g * c.K + i, c.sets[par * c.K + i], c.sides[s]);
     if (r != EMB_OK) return r;
@@ -187,10 +196,12 @@ extern "C" {
 emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_update* update, int32_t n_steps,
                               const emb_batch* batches, float* const* outs, const float* const* grads,
                               int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,
-                              void* const* side_streams, void* const* events) {
+                              void* const* side_streams, void* const* events, void* group_ws,
+                              size_t group_ws_bytes) {
   if (tables == nullptr || update == nullptr || n_steps < 0 || group < 1 || n_side < 1 || n_side > group)
     return EMB_EINVAL;
   if (n_side > kMaxSideStreams) return EMB_EUNSUPPORTED;
+  if (group_ws != nullptr && n_side != 1) return EMB_EINVAL;  // a group's one dedup runs on one stream
   if (n_steps == 0) return EMB_OK;
   if (batches == nullptr || outs == nullptr || grads == nullptr || sets == nullptr || side_streams == nullptr ||
       events == nullptr)
@@ -205,6 +216,12 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
         emb::check_pipeline_step(tables, &batches[k], pool, outs[k], grads[k], update, &sets[((k / group) % 2) * group + k % group]);
     if (st != EMB_OK) return st;
   }
+  if (group_ws != nullptr)
+    for (int g = 0; g * group < n_steps; ++g) {
+      const int count = n_steps - g * group < group ? n_steps - g * group : group;
+      const emb_status st = emb::check_dedup_group(tables, count, &batches[g * group], group_ws, group_ws_bytes);
+      if (st != EMB_OK) return st;
+    }
   Schedule c{};
   c.tables = tables;
   c.pool = pool;
@@ -223,6 +240,8 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
   c.ev_main[0] = (hipEvent_t)events[1];
   c.ev_main[1] = (hipEvent_t)events[2];
   c.events = events;
+  c.group_ws = group_ws;
+  c.group_ws_bytes = group_ws_bytes;
   // the side streams start after the work already on the main stream
   if (hipEventRecord(c.ev_start, c.main) != hipSuccess) return EMB_EHIP;
   for (int s = 0; s < n_side; ++s)

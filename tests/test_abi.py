@@ -205,7 +205,9 @@ def test_pipeline_steps_argument_checks():
     sides = (ctypes.c_void_p * 2)(0x10, 0x20)
     events = (ctypes.c_void_p * 7)(*([0x40] * 7))
     no_events = (ctypes.c_void_p * 7)(*([0x40] * 6 + [0]))
-    f = L.emb_pipeline_steps
+    def f(*a, group_ws=None, group_ws_bytes=0):
+        return L.emb_pipeline_steps(*a, group_ws, group_ws_bytes)
+
     tb, ub = ctypes.byref(t), ctypes.byref(upd)
     assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_OK   # nothing to do
     assert f(None, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_EINVAL
@@ -245,3 +247,50 @@ def test_pipeline_steps_argument_checks():
     assert f(tb, 0, ub, n, bad_b, outs4, grads4, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL
     bad_upd = emb.CUpdate(9, 0.1, 0.0, None, 0, 0)
     assert f(tb, 0, ctypes.byref(bad_upd), n, b4, outs4, grads4, 2, sets4, None, 1, sides, events) == emb.EMB_EINVAL
+    # one batched dedup per group: one side stream only, and a group workspace
+    # large enough for every group (checked before anything is enqueued)
+    gws = L.emb_workspace_size(20, 2, t.dim)
+    assert f(tb, 0, ub, n, b4, outs4, grads4, 2, sets4, None, 2, sides, events,
+             group_ws=0x200000, group_ws_bytes=gws) == emb.EMB_EINVAL                                    # 2 sides
+    assert f(tb, 0, ub, n, b4, outs4, grads4, 2, sets4, None, 1, sides, events,
+             group_ws=0x200000, group_ws_bytes=gws - 256) == emb.EMB_EWORKSPACE                           # too small
+    many_sets = (emb.CDedupSet * 34)(*([good] * 34))
+    b17 = (emb.CBatch * 17)(*([emb.CBatch(1, 0x1000, 0x2000, 10, 4)] * 17))
+    o17 = (ctypes.c_void_p * 17)(*([0x3000] * 17))
+    assert f(tb, 0, ub, 17, b17, o17, o17, 17, many_sets, None, 1, sides, events,
+             group_ws=0x200000, group_ws_bytes=1 << 30) == emb.EMB_EUNSUPPORTED                           # > 16
+
+
+def test_unique_ids_batched_argument_checks():
+    """Host checks of emb_unique_ids_batched return before anything is enqueued."""
+    L = emb.lib()
+    t = _tables()
+    n = 3
+    b = (emb.CBatch * n)(*([emb.CBatch(1, 0x1000, 0x2000, 10, 4)] * n))
+    need = L.emb_workspace_size(10, 1, t.dim)
+    gneed = L.emb_workspace_size(30, 3, t.dim)
+    sets = (emb.CDedupSet * n)(*[emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000 * (i + 1), need)
+                                 for i in range(n)])
+    f = L.emb_unique_ids_batched
+    tb = ctypes.byref(t)
+    assert f(tb, 0, b, sets, 0x800000, gneed, None) == emb.EMB_EINVAL          # no batch
+    assert f(tb, n, None, sets, 0x800000, gneed, None) == emb.EMB_EINVAL
+    assert f(tb, n, b, None, 0x800000, gneed, None) == emb.EMB_EINVAL
+    assert f(tb, n, b, sets, 0x800000, gneed - 256, None) == emb.EMB_EWORKSPACE  # group workspace too small
+    assert f(tb, n, b, sets, 0x800010, gneed, None) == emb.EMB_EWORKSPACE      # misaligned
+    assert f(tb, n, b, sets, 0x100000, gneed, None) == emb.EMB_EINVAL          # a set's workspace is the group's
+    same = (emb.CDedupSet * n)(*[emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000, need)] * n)
+    assert f(tb, n, b, same, 0x800000, gneed, None) == emb.EMB_EINVAL          # two sets share a workspace
+    small = (emb.CDedupSet * n)(*[emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000 * (i + 1), need - 256)
+                                  for i in range(n)])
+    assert f(tb, n, b, small, 0x800000, gneed, None) == emb.EMB_EWORKSPACE
+    no_perm = (emb.CDedupSet * n)(*[emb.CDedupSet(0x5000, 0x5100, 0x5200, None, 0x5400, 0x100000 * (i + 1), need)
+                                    for i in range(n)])
+    assert f(tb, n, b, no_perm, 0x800000, gneed, None) == emb.EMB_EINVAL
+    b17 = (emb.CBatch * 17)(*([emb.CBatch(1, 0x1000, 0x2000, 10, 4)] * 17))
+    s17 = (emb.CDedupSet * 17)(*[emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000 * (i + 1), need)
+                                 for i in range(17)])
+    assert f(tb, 17, b17, s17, 0x800000, 1 << 30, None) == emb.EMB_EUNSUPPORTED  # more than 16 batches
+    # 2^31 + 1 rows need 32 key bits: no room for a batch index
+    wide = _tables(row_offset=(0, (1 << 31) + 1))
+    assert f(ctypes.byref(wide), 2, b, sets, 0x800000, gneed, None) == emb.EMB_EUNSUPPORTED

@@ -141,19 +141,21 @@ def test_failed_dedup_unfused_path():
     _say("  ok")
 
 
-def test_failed_dedup_in_pipeline_is_reported():
+@pytest.mark.parametrize("group_dedup", [True, False])
+def test_failed_dedup_in_pipeline_is_reported(group_dedup):
     """The pipelined schedule: a failure preset in one buffer set's workspace
     makes that step write nothing and Pipeline.check raise; the other steps
-    of the run equal serial steps of the same batches minus the failed one."""
+    of the run equal serial steps of the same batches minus the failed one
+    (with each group's dedups as one batched call, and one call per batch)."""
     import torch
     import paper_2112_02752_amd as emb
     w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
-    _say(f"case failed dedup in pipeline {w.name}")
+    _say(f"case failed dedup in pipeline {w.name} group dedup={group_dedup}")
     bs = [_batch(w, s) for s in range(4)]
     nmax = max(len(b.indices) for b, _, _ in bs)
     dl_p = parity.device_layer_from_workload(w)
     pipe = emb.Pipeline(dl_p.tables, w.pool, w.opt, w.lr, w.eps, dl_p.state, max_indices=nmax,
-                        max_bags=w.num_bags, group=2)
+                        max_bags=w.num_bags, group=2, side_streams=1, group_dedup=group_dedup)
     # set index of step 1 in the first group is 1
     _preset_failure(pipe.sets[1].ws)
     outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in bs]
@@ -173,4 +175,49 @@ def test_failed_dedup_in_pipeline_is_reported():
         assert torch.equal(o, outs[k]), f"pooled output of step {k}"
     assert torch.equal(dl_s.W, dl_p.W)
     assert torch.equal(dl_s.state, dl_p.state)
+    _say("  ok")
+
+
+def test_failed_group_dedup_reaches_every_batch():
+    """A failure preset in a group dedup's own workspace (the error bits of its
+    next call) becomes every batch's: each batch's fused gradient reduce
+    writes nothing and each set reports the failure; the next group call on
+    the same workspaces is clean and every batch's step then equals a serial
+    step of it."""
+    import torch
+    import paper_2112_02752_amd as emb
+    w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
+    _say(f"case failed group dedup {w.name}")
+    bs = [_batch(w, s) for s in range(3)]
+    nmax = max(len(b.indices) for b, _, _ in bs)
+    dl = parity.device_layer_from_workload(w)
+    sets = [emb.DedupBuffers("cuda", nmax, w.num_bags, w.dim) for _ in bs]
+    gws = torch.empty(emb.workspace_size(3 * nmax, 3 * w.num_bags, w.dim), dtype=torch.uint8, device="cuda")
+    emb.workspace_init(gws)
+
+    def steps():
+        emb.unique_ids_batched(dl.tables, [db for _, db, _ in bs], sets, gws)
+        for (_, db, g), d in zip(bs, sets):
+            emb.grad_reduce(dl.tables, db, w.pool, g, d.sort_perm, d.seg_offsets, d.unique_keys, d.num_unique, d.ws,
+                            opt=w.opt, lr=w.lr, eps=w.eps, state=dl.state)
+        torch.cuda.synchronize()
+
+    W0, S0 = dl.W.clone(), dl.state.clone()
+    _preset_failure(gws)
+    steps()
+    assert torch.equal(dl.W, W0)
+    assert torch.equal(dl.state, S0)
+    for d in sets:
+        assert emb.read_status(d.ws)[0] & 1
+        assert int(d.num_unique.cpu().item()) == 0
+    steps()
+    for d in sets:
+        assert emb.read_status(d.ws)[0] == 0
+    dl_s = parity.device_layer_from_workload(w)
+    layer = emb.Layer(dl_s.tables, w.pool, w.opt, w.lr, w.eps, dl_s.state, max_indices=nmax, max_bags=w.num_bags)
+    for _, db, g in bs:
+        layer.backward(db, g)
+    torch.cuda.synchronize()
+    assert torch.equal(dl_s.W, dl.W)
+    assert torch.equal(dl_s.state, dl.state)
     _say("  ok")

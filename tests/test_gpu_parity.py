@@ -647,13 +647,16 @@ def test_stale_schedule_matches_oracle_replay(name, concurrent):
     parity.check_rows(dl, store, touched, w.opt)
 
 
-@pytest.mark.parametrize("group,sides,nsteps", [(1, 1, 5), (2, 1, 7), (4, 1, 10), (2, 2, 7), (6, 3, 13)])
-def test_pipelined_schedule_equals_serial(group, sides, nsteps):
+@pytest.mark.parametrize("group,sides,nsteps,gd", [(1, 1, 5, False), (2, 1, 7, False), (4, 1, 10, False),
+                                                   (2, 2, 7, False), (6, 3, 13, False), (1, 1, 5, True),
+                                                   (2, 1, 7, True), (6, 1, 13, True), (16, 1, 20, True)])
+def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd):
     """The dedups of the next group of batches on a side stream while the main
     stream runs the forward and update of the current group change nothing:
     tables, state and pooled outputs equal those of serial steps bit for bit
-    (step counts that leave a partial last group included)."""
-    _say(f"case pipelined vs serial group={group} side streams={sides} steps={nsteps}")
+    (step counts that leave a partial last group included; gd: each group's
+    dedups as one emb_unique_ids_batched call)."""
+    _say(f"case pipelined vs serial group={group} side streams={sides} steps={nsteps} group dedup={gd}")
     import torch
     import paper_2112_02752_amd as emb
     w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
@@ -671,7 +674,7 @@ def test_pipelined_schedule_equals_serial(group, sides, nsteps):
                 layer.step(b, out, g)
         else:
             pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
-                                max_bags=w.num_bags, group=group, side_streams=sides)
+                                max_bags=w.num_bags, group=group, side_streams=sides, group_dedup=gd)
             # two runs: the second starts after everything the first enqueued
             half = nsteps // 2
             pipe.run([(b, o, g) for (b, g), o in zip(dev_b[:half], outs[:half])])
@@ -687,13 +690,14 @@ def test_pipelined_schedule_equals_serial(group, sides, nsteps):
         np.testing.assert_array_equal(a, b)
 
 
-@pytest.mark.parametrize("name,nsteps,group,sides", [("c3", 6, 4, 1), ("c3", 13, 6, 3), ("c2", 3, 2, 1),
-                                                     ("c2", 5, 4, 2)])
-def test_pipelined_schedule_full_size(name, nsteps, group, sides):
+@pytest.mark.parametrize("name,nsteps,group,sides,gd", [("c3", 6, 4, 1, False), ("c3", 13, 6, 3, False),
+                                                        ("c2", 3, 2, 1, False), ("c2", 5, 4, 2, False),
+                                                        ("c3", 13, 6, 1, True), ("c2", 5, 4, 1, True)])
+def test_pipelined_schedule_full_size(name, nsteps, group, sides, gd):
     """Full-size pipelined steps against the oracle replaying the same steps on
     the rows they touch: every pooled output, the final rows and state, rows
     no step touched unchanged."""
-    _say(f"case pipelined full size {name} steps={nsteps} group={group} side streams={sides}")
+    _say(f"case pipelined full size {name} steps={nsteps} group={group} side streams={sides} group dedup={gd}")
     import oracle
     import torch
     import paper_2112_02752_amd as emb
@@ -704,7 +708,7 @@ def test_pipelined_schedule_full_size(name, nsteps, group, sides):
               torch.from_numpy(b.grad).cuda()) for b in batches]
     dl = parity.device_layer_from_workload(w)
     pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
-                        group=group, side_streams=sides)
+                        group=group, side_streams=sides, group_dedup=gd)
     outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in dev_b]
     pipe.run([(b, o, g) for (b, g), o in zip(dev_b, outs)])
     torch.cuda.synchronize()
@@ -834,6 +838,97 @@ def test_workspace_shared_by_both_dedups_and_all_sizes():
         o_gr, _ = oracle.grad_reduce(len(ro) - 1, B, np.ascontiguousarray(off, np.int32), G, pool, ref)
         r = parity.rel_rownorm(gr[:U].cpu().numpy(), o_gr)
         assert r <= parity.TOL_FP32, f"call {k} ({name}): gradient rows rel err {r}"
+
+
+def _batched_case(case):
+    """(row_offset, dim, [(offsets, indices, bags_per_table)]) of a group."""
+    rng = np.random.default_rng(17)
+    if case in ("c3x6", "c3x1", "c3x2_int64"):
+        w = synth.workload("c3")
+        k = {"c3x6": 6, "c3x1": 1, "c3x2_int64": 2}[case]
+        bs = [synth.make_batch(w, s, with_grad=False) for s in range(k)]
+        dt = np.int64 if case.endswith("int64") else np.int32
+        return w.row_offset, w.dim, [(b.offsets, b.indices.astype(dt), w.bags_per_table) for b in bs]
+    if case == "c2_mixed":
+        w = synth.workload("c2")
+        bs = [synth.make_batch(w, s, with_grad=False) for s in range(3)]
+        out = [(b.offsets, b.indices, w.bags_per_table) for b in bs]
+        B = 4
+        out.insert(1, (np.zeros(w.num_tables * B + 1, np.int32), np.zeros(0, np.int32), B))  # every bag empty
+        one = np.zeros(w.num_tables * B + 1, np.int32)
+        one[B * 3 + 2:] = 1  # one id, in bag 13 (the second bag of table 3)
+        out.append((one, np.array([w.row_offset[4] - w.row_offset[3] - 1], np.int32), B))
+        return w.row_offset, w.dim, out
+    if case == "k16":
+        rows = [1 << 20]
+        out = []
+        for i in range(16):
+            off, idx = _rand_batch(rng, rows, 200 + 37 * i, 40, empty_frac=0.05, zipf=1.2)
+            out.append((off, idx, 200 + 37 * i))
+        return _row_offset(rows), 16, out
+    raise ValueError(case)
+
+
+@pytest.mark.parametrize("case", ["c3x6", "c3x1", "c3x2_int64", "c2_mixed", "k16"])
+def test_unique_ids_batched_matches_single(case):
+    """emb_unique_ids_batched leaves in every batch's buffers, bit for bit,
+    what that batch's own emb_unique_ids leaves: the outputs, and (through
+    the unfused gradient reduce that reads them) the bag ids, chunk map and
+    call record in its workspace; twice in a row on the same workspaces, the
+    batches' order reversed the second time.  The first batch of the first
+    call is also checked against the oracle."""
+    import oracle
+    import torch
+    import paper_2112_02752_amd as emb
+    _say(f"case unique_ids_batched {case}")
+    ro, D, group = _batched_case(case)
+    dev = "cuda"
+    tables = emb.Tables(torch.empty((1, D), dtype=torch.float32, device=dev), [int(x) for x in ro])
+    T = len(ro) - 1
+    bt = [emb.Batch(torch.from_numpy(np.ascontiguousarray(o, np.int32)).to(dev), torch.from_numpy(i).to(dev), B)
+          for o, i, B in group]
+    Ns = [len(i) for _, i, _ in group]
+    Ms = [len(o) - 1 for o, _, _ in group]
+    rng = np.random.default_rng(3)
+    grads = [torch.from_numpy(rng.standard_normal((m, D)).astype(np.float32)).to(dev) for m in Ms]
+    nmax, mmax = max(max(Ns), 1), max(Ms)
+    sets_b = [emb.DedupBuffers(dev, nmax, mmax, D) for _ in group]
+    sets_s = [emb.DedupBuffers(dev, nmax, mmax, D) for _ in group]
+    gws = torch.empty(emb.workspace_size(max(sum(Ns), 1), sum(Ms), D), dtype=torch.uint8, device=dev)
+    emb.workspace_init(gws)
+    gr_b = torch.zeros((nmax, D), dtype=torch.float32, device=dev)
+    gr_s = torch.zeros((nmax, D), dtype=torch.float32, device=dev)
+    pool = "sum"
+    for rnd, order in enumerate((list(range(len(group))), list(reversed(range(len(group)))))):
+        emb.unique_ids_batched(tables, [bt[i] for i in order], [sets_b[i] for i in order], gws)
+        for i in order:
+            emb.unique_ids(tables, bt[i], sets_s[i].unique_keys, sets_s[i].counts, sets_s[i].seg_offsets,
+                           sets_s[i].sort_perm, sets_s[i].num_unique, sets_s[i].ws)
+        torch.cuda.synchronize()
+        for i in order:
+            n = Ns[i]
+            a, b = sets_b[i], sets_s[i]
+            assert emb.read_status(a.ws)[0] == 0, (rnd, i)
+            U = int(b.num_unique.cpu().item())
+            assert int(a.num_unique.cpu().item()) == U, (rnd, i)
+            np.testing.assert_array_equal(a.unique_keys[:U].cpu().numpy(), b.unique_keys[:U].cpu().numpy())
+            np.testing.assert_array_equal(a.counts[:U].cpu().numpy(), b.counts[:U].cpu().numpy())
+            np.testing.assert_array_equal(a.seg_offsets[:U + 1].cpu().numpy(), b.seg_offsets[:U + 1].cpu().numpy())
+            np.testing.assert_array_equal(a.sort_perm[:n].cpu().numpy(), b.sort_perm[:n].cpu().numpy())
+            if n == 0:
+                continue
+            for sset, gr in ((a, gr_b), (b, gr_s)):
+                emb.grad_reduce(tables, bt[i], pool, grads[i], sset.sort_perm, sset.seg_offsets, sset.unique_keys,
+                                sset.num_unique, sset.ws, grad_rows=gr)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(gr_b[:U].cpu().numpy(), gr_s[:U].cpu().numpy())
+            if rnd == 0 and i == 0:
+                o, idx, B = group[0]
+                ref = oracle.unique_ids(T, np.asarray(ro, np.int64), B, np.ascontiguousarray(o, np.int32),
+                                        np.ascontiguousarray(idx, np.int32))
+                assert U == ref.num_unique
+                np.testing.assert_array_equal(a.unique_keys[:U].cpu().numpy().view(np.uint32), ref.unique_keys)
+                np.testing.assert_array_equal(a.sort_perm[:n].cpu().numpy(), ref.perm)
 
 
 # ------------------------------------------------------------------ routing

@@ -64,7 +64,7 @@ def parse():
                          "least a million lookups, else serial; stale: the asynchronous schedule with "
                          "staleness one (the forward of batch k+1 on a side stream, reading the table before "
                          "the update of batch k, alongside the dedup of batch k)")
-    ap.add_argument("--group", type=int, default=8, help="batches per group of the pipelined schedule")
+    ap.add_argument("--group", type=int, default=4, help="batches per group of the pipelined schedule")
     ap.add_argument("--side-streams", type=int, default=3,
                     help="side streams of the pipelined schedule with --dedup per-batch (more than one: the "
                          "dedups of a group run concurrently with emb_unique_ids_concurrent)")

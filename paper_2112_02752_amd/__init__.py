@@ -548,8 +548,10 @@ class Pipeline:
     equal those of serial steps bit for bit.  By default (``group_dedup``)
     the dedups of a group are one emb_unique_ids_batched call on one side
     stream: one sort of all the group's keys, each batch's share then split
-    off into its own buffers (no workgroup waits for another; about 35 us of
-    device time per c3 batch against 52 for emb_unique_ids alone).  Without
+    off into its own buffers (no workgroup waits for another; about 30 us of
+    device time per c3 batch in a group of 8, 39 in a group of 4, against 55
+    for emb_unique_ids alone).  The group's first forward runs before the
+    wait for its dedups, which it does not read.  Without
     it, with one side stream the dedups run one after another with
     emb_unique_ids (whose sort may make the workgroups of a pass wait for one
     another, which is safe with one dedup in flight next to kernels that
@@ -567,7 +569,7 @@ class Pipeline:
     staleness: only the dedup, which the table never feeds, runs early."""
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
-                 max_indices: int = 0, max_bags: int = 0, group: int = 8, side_streams: int = 3,
+                 max_indices: int = 0, max_bags: int = 0, group: int = 4, side_streams: int = 3,
                  rounding: str = "nearest", seed: int = 0, group_dedup: bool = True):
         import torch
         if group < 1 or not 1 <= side_streams <= 16:

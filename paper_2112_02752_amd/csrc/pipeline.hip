@@ -53,6 +53,8 @@ struct Schedule {
 
   hipEvent_t ev_side(int parity, int s) const { return (hipEvent_t)events[3 + parity * n_side + s]; }
   hipStream_t side(int s) const { return (hipStream_t)sides[s]; }
+  int start(int g) const { return g * K; }
+  int count(int g) const { return n_steps - g * K < K ? n_steps - g * K : K; }
 };
 
 emb_status hip_ok(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; }
@@ -73,14 +75,20 @@ emb_status side_group(const Schedule& c, int g, int s) {
   const int par = g % 2;
   if (g >= 2 && hipStreamWaitEvent(c.side(s), c.ev_main[par], 0) != hipSuccess) return EMB_EHIP;
   if (c.group_ws != nullptr) {
-    const int count = c.n_steps - g * c.K < c.K ? c.n_steps - g * c.K : c.K;
-    const emb_status r = emb_unique_ids_batched(c.tables, count, &c.batches[g * c.K], &c.sets[par * c.K], c.group_ws,
-                                                c.group_ws_bytes, c.sides[s]);
+    // a group of one batch: its own dedup (one dedup in flight on this
+    // stream, beside kernels that never wait)
+    const emb_status r = c.count(g) == 1
+                             ? emb_unique_ids(c.tables, &c.batches[c.start(g)], c.sets[par * c.K].unique_keys,
+                                              c.sets[par * c.K].counts, c.sets[par * c.K].seg_offsets,
+                                              c.sets[par * c.K].sort_perm, c.sets[par * c.K].num_unique,
+                                              c.sets[par * c.K].ws, c.sets[par * c.K].ws_bytes, c.sides[s])
+                             : emb_unique_ids_batched(c.tables, c.count(g), &c.batches[c.start(g)], &c.sets[par * c.K],
+                                                      c.group_ws, c.group_ws_bytes, c.sides[s]);
     if (r != EMB_OK) return r;
     return hip_ok(hipEventRecord(c.ev_side(par, s), c.side(s)));
   }
-  for (int i = s; i < c.K && g * c.K + i < c.n_steps; i += c.n_side) {
-    const emb_status r = dedup_one(c, g * c.K + i, c.sets[par * c.K + i], c.sides[s]);
+  for (int i = s; i < c.count(g); i += c.n_side) {
+    const emb_status r = dedup_one(c, c.start(g) + i, c.sets[par * c.K + i], c.sides[s]);
     if (r != EMB_OK) return r;
   }
   return hip_ok(hipEventRecord(c.ev_side(par, s), c.side(s)));
@@ -98,17 +106,20 @@ emb_status side_group_all(const Schedule& c, int g) {
 // each step's forward and fused backward + update, then the group's record
 emb_status main_group(const Schedule& c, int g) {
   const int par = g % 2;
-  for (int s = 0; s < c.n_side; ++s)
-    if (hipStreamWaitEvent(c.main, c.ev_side(par, s), 0) != hipSuccess) return EMB_EHIP;
   emb_update u = *c.update;
-  for (int i = 0; i < c.K && g * c.K + i < c.n_steps; ++i) {
-    const int k = g * c.K + i;
+  for (int i = 0; i < c.count(g); ++i) {
+    const int k = c.start(g) + i;
     const emb_dedup_set& d = c.sets[par * c.K + i];
     u.seed = c.update->seed + (uint64_t)k;  // bf16 stochastic rounding draws fresh bits every step
     emb_status st = emb_pool_fwd(c.tables, &c.batches[k], c.pool, c.outs[k], c.main);
-    if (st == EMB_OK)
-      st = emb_grad_reduce(c.tables, &c.batches[k], c.pool, c.grads[k], d.sort_perm, d.seg_offsets, d.unique_keys,
-                           d.num_unique, nullptr, &u, d.ws, d.ws_bytes, c.main);
+    if (st != EMB_OK) return st;
+    // the group's first forward needs no dedup output: the wait for the
+    // group's dedups comes after it, before the first gradient reduce
+    if (i == 0)
+      for (int s = 0; s < c.n_side; ++s)
+        if (hipStreamWaitEvent(c.main, c.ev_side(par, s), 0) != hipSuccess) return EMB_EHIP;
+    st = emb_grad_reduce(c.tables, &c.batches[k], c.pool, c.grads[k], d.sort_perm, d.seg_offsets, d.unique_keys,
+                         d.num_unique, nullptr, &u, d.ws, d.ws_bytes, c.main);
     if (st != EMB_OK) return st;
   }
   return hip_ok(hipEventRecord(c.ev_main[par], c.main));
@@ -202,6 +213,7 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
     return EMB_EINVAL;
   if (n_side > kMaxSideStreams) return EMB_EUNSUPPORTED;
   if (group_ws != nullptr && n_side != 1) return EMB_EINVAL;  // a group's one dedup runs on one stream
+  if (group_ws != nullptr && group > emb::kMaxGroup) return EMB_EUNSUPPORTED;
   if (n_steps == 0) return EMB_OK;
   if (batches == nullptr || outs == nullptr || grads == nullptr || sets == nullptr || side_streams == nullptr ||
       events == nullptr)
@@ -212,8 +224,8 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
     if (side_streams[s] == nullptr || side_streams[s] == main_stream) return EMB_EINVAL;
   // every step is checked before anything is enqueued
   for (int k = 0; k < n_steps; ++k) {
-    const emb_status st =
-        emb::check_pipeline_step(tables, &batches[k], pool, outs[k], grads[k], update, &sets[((k / group) % 2) * group + k % group]);
+    const emb_status st = emb::check_pipeline_step(tables, &batches[k], pool, outs[k], grads[k], update,
+                                                   &sets[((k / group) % 2) * group + k % group]);
     if (st != EMB_OK) return st;
   }
   if (group_ws != nullptr)

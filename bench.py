@@ -65,6 +65,9 @@ def parse():
                          "staleness one (the forward of batch k+1 on a side stream, reading the table before "
                          "the update of batch k, alongside the dedup of batch k)")
     ap.add_argument("--group", type=int, default=4, help="batches per group of the pipelined schedule")
+    ap.add_argument("--no-chain", action="store_true",
+                    help="pipelined: time one call on its own (its first group's dedups and its last group's "
+                         "forward and update not overlapped) instead of a call in a chain of calls")
     ap.add_argument("--side-streams", type=int, default=3,
                     help="side streams of the pipelined schedule with --dedup per-batch (more than one: the "
                          "dedups of a group run concurrently with emb_unique_ids_concurrent)")
@@ -246,8 +249,16 @@ def main():
     n_warm = args.warmup
     t0_batch = n_warm
     total = n_warm + args.steps
-    # the stale schedule's last timed step runs the forward of one more batch
-    n_batches = total + (1 if args.schedule == "stale" else 0)
+    # the stale schedule's last timed step runs the forward of one more batch;
+    # the chained pipelined schedule's timed call dedups the group after its
+    # steps, and its own first group is deduplicated at the end of the
+    # warm-up: the timed region holds exactly `steps` dedups and `steps`
+    # forwards, backwards and updates.  The pipelined schedule also runs one
+    # call on its own over `steps` batches of their own (isolated_call).
+    chain = args.schedule == "pipelined" and not args.no_chain
+    n_ahead = args.group if chain else 0
+    n_iso = args.steps if args.schedule == "pipelined" else 0
+    n_batches = total + (1 if args.schedule == "stale" else 0) + n_ahead + n_iso
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
     t0 = time.time()
     batches = [synth.make_batch(w, s) for s in range(n_batches)]
@@ -302,8 +313,9 @@ def main():
         pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
                             group=args.group, side_streams=args.side_streams, group_dedup=args.dedup == "group")
 
-        def run_steps(idx):
-            pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in idx], sp)
+        def run_steps(idx, ahead=None):
+            pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in idx], sp,
+                     ahead=[dev_batches[i][0] for i in ahead] if ahead else None)
     elif args.schedule == "stale":
         clayer = emb.Layer(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
                            concurrent=True)
@@ -336,7 +348,10 @@ def main():
             print(f"bench.py: {where}: {e}", file=sys.stderr, flush=True)
             sys.exit(3)
 
-    run_steps(range(n_warm))
+    if chain and n_warm > 0:
+        run_steps(range(n_warm), ahead=range(t0_batch, t0_batch + n_ahead))
+    else:
+        run_steps(range(n_warm))
     torch.cuda.synchronize()
     check_status("warm-up")
 
@@ -346,13 +361,32 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     e_all[0].record(stream)
-    run_steps(range(t0_batch, total))
+    if chain:
+        run_steps(range(t0_batch, total), ahead=range(total, total + n_ahead))
+    else:
+        run_steps(range(t0_batch, total))
     e_all[1].record(stream)
     t_enq = time.perf_counter() - t_start
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     gpu_all_s = e_all[0].elapsed_time(e_all[1]) * 1e-3
     check_status("timed region")
+    isolated = None
+    if n_iso:
+        # the same schedule as one call on its own over batches of its own
+        pipe.discard()
+        iso = range(total + n_ahead, total + n_ahead + n_iso)
+        torch.cuda.synchronize()
+        t_iso = time.perf_counter()
+        run_steps(iso)
+        torch.cuda.synchronize()
+        t_iso = time.perf_counter() - t_iso
+        check_status("isolated call")
+        isolated = {"us_per_step": t_iso / n_iso * 1e6,
+                    "lookups_per_s": sum(dev_batches[i][2] for i in iso) / t_iso,
+                    "note": "one pipelined call on its own over `steps` batches of their own, after the timed "
+                            "region: its first group's dedups and its last group's forward and update overlap "
+                            "nothing"}
 
     # the same batches again as serial steps with an event pair around each
     # step: the distribution of serial step times
@@ -510,6 +544,11 @@ def main():
                    "table_bytes": w.weight_bytes, "schedule": args.schedule,
                    "staleness": 1 if args.schedule == "stale" else 0,
                    "group": args.group if args.schedule == "pipelined" else None,
+                   "chained": chain,
+                   "step_accounting": ("chained calls (a training loop's look-ahead): the warm-up call ends with "
+                                       "the dedups of the first timed group, the timed call with those of the "
+                                       "group after it; the timed region holds exactly `steps` dedups and `steps` "
+                                       "forwards, backwards and updates") if chain else None,
                    "dedup": args.dedup if args.schedule == "pipelined" else None,
                    "side_streams": (pipe.S if pipe is not None else None),
                    "overlapped_steps": args.steps if args.schedule == "pipelined" else
@@ -533,6 +572,7 @@ def main():
                     "p90": float(np.percentile(step_s, 90)) * 1e6,
                     "host_enqueue_us": t_enq / args.steps * 1e6,
                     "with_phase_events_median": float(np.median(phased_step_s)) * 1e6},
+        "isolated_call": isolated,
         "cold": None if cold is None else dict(cold, lookups_per_s=N_avg * 1e6 / cold["median_us"]),
         "achievable_copy_GBs": copy_gbs,
         "routing": routing,

@@ -124,7 +124,7 @@ def lib():
         PV = ctypes.POINTER(vp)
         L.emb_pipeline_steps.restype = i32
         L.emb_pipeline_steps.argtypes = [T, i32, Up, i32, B, PV, PV, i32, ctypes.POINTER(CDedupSet), vp, i32, PV, PV,
-                                         vp, sz]
+                                         vp, sz, i32, i32, i32]
         L.emb_unique_ids_batched.restype = i32
         L.emb_unique_ids_batched.argtypes = [T, i32, B, ctypes.POINTER(CDedupSet), vp, sz, vp]
         L.emb_route_ids_noalloc.restype = i32
@@ -607,6 +607,10 @@ class Pipeline:
         self.rounding, self.seed, self.steps_done = rounding, seed, 0
         self._updc = _update(opt, lr, eps, state, rounding, seed)
         self._pool = POOL[pool]
+        # chained calls: groups numbered across calls, and the batches whose
+        # dedups the last call enqueued for the next one
+        self._group_base = 0
+        self._primed = None
 
     def __del__(self):
         try:
@@ -616,21 +620,39 @@ class Pipeline:
         except Exception:
             pass
 
-    def run(self, steps, stream=None) -> None:
+    def run(self, steps, stream=None, ahead=None) -> None:
         """Enqueue one training step per ``(batch, out, grad_out)`` of
         ``steps``, in order, on ``stream`` (the forward of each batch into its
         ``out``, then its backward with ``grad_out`` and the optimizer step),
         through one call of the native schedule (emb_pipeline_steps).  Every
         step's results are complete when ``stream`` reaches the end of the
-        enqueued work; the side streams' work all precedes it."""
+        enqueued work; the side streams' work all precedes it.
+
+        ``ahead``: the next call's first ``group`` batches (a training loop's
+        look-ahead).  Their dedups are enqueued at the end of this call,
+        beside its last group's forward and update, and the next call, whose
+        first steps must use exactly these batches (unchanged), starts with
+        them done.  A call that starts with other batches raises; ``discard``
+        drops the look-ahead instead."""
         steps = list(steps)
         n = len(steps)
+        if ahead is not None:
+            ahead = list(ahead)
+            if n == 0 or len(ahead) != self.K:
+                raise ValueError(f"ahead takes the next call's first {self.K} batches, after at least one step")
         if n == 0:
             return
-        cbs = [b.c() for b, _, _ in steps]
+        primed = 0
+        if self._primed is not None:
+            first = [b for b, _, _ in steps[:self.K]]
+            if len(first) != len(self._primed) or any(x is not y for x, y in zip(first, self._primed)):
+                raise ValueError("the first steps are not the batches deduplicated ahead by the last call "
+                                 "(call discard() to drop them)")
+            primed = 1
+        cbs = [b.c() for b, _, _ in steps] + ([b.c() for b in ahead] if ahead else [])
         if max(c.num_indices for c in cbs) > self.max_indices:
             raise ValueError("batch larger than the pipeline's buffers")
-        batches = (CBatch * n)(*cbs)
+        batches = (CBatch * len(cbs))(*cbs)
         outs = (ctypes.c_void_p * n)(*[_ptr(o) for _, o, _ in steps])
         grads = (ctypes.c_void_p * n)(*[_ptr(g) for _, _, g in steps])
         self._updc.seed = self.seed + self.steps_done
@@ -638,8 +660,15 @@ class Pipeline:
         _check("emb_pipeline_steps", lib().emb_pipeline_steps(
             self._ct, self._pool, ctypes.byref(self._updc), n, batches, outs, grads, self.K, self._sets_c,
             _stream(stream), self.S, self._sides_c, self._events_c, _ptr(gws),
-            gws.numel() if gws is not None else 0))
+            gws.numel() if gws is not None else 0, self._group_base % 2, primed, 1 if ahead else 0))
         self.steps_done += n
+        self._group_base += (n + self.K - 1) // self.K
+        self._primed = ahead
+
+    def discard(self) -> None:
+        """Drop the look-ahead dedups of the last call: the next call starts
+        with its own."""
+        self._primed = None
 
     def status(self, stream=None):
         """Per buffer set, the status of its last step (emb_workspace_status);

@@ -175,9 +175,19 @@ emb_status check_pipeline_step(const emb_tables* tables, const emb_batch* batch,
   if ((int64_t)tables->dim * dtype_bytes(tables->dtype) / 16 > fwd_max_row_vectors()) return EMB_EUNSUPPORTED;
   if (tables->dim > reduce_max_dim()) return EMB_EUNSUPPORTED;
   if (M > 0 && out == nullptr) return EMB_EINVAL;
+  if (batch->num_indices > 0 && grad == nullptr) return EMB_EINVAL;
+  return check_dedup_step(tables, batch, d);
+}
+
+emb_status check_dedup_step(const emb_tables* tables, const emb_batch* batch, const emb_dedup_set* d) {
+  TableOffsets ro;
+  int64_t R = 0;
+  emb_status st = check_tables(tables, &ro, &R);
+  if (st != EMB_OK) return st;
+  int32_t M = 0;
+  if ((st = check_batch(batch, tables->num_tables, &M)) != EMB_OK) return st;
   if (d->seg_offsets == nullptr || d->num_unique == nullptr) return EMB_EINVAL;
-  if (batch->num_indices > 0 && (d->unique_keys == nullptr || d->counts == nullptr || d->sort_perm == nullptr ||
-                                 grad == nullptr))
+  if (batch->num_indices > 0 && (d->unique_keys == nullptr || d->counts == nullptr || d->sort_perm == nullptr))
     return EMB_EINVAL;
   WsLayout lay;
   return check_ws(d->ws, d->ws_bytes, batch->num_indices, M, tables->dim, &lay);

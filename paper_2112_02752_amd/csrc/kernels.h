@@ -168,5 +168,7 @@ emb_status check_dedup_group(const emb_tables* tables, int32_t n_batches, const 
 // host checks of one step of emb_pipeline_steps (defined with the C ABI)
 emb_status check_pipeline_step(const emb_tables* tables, const emb_batch* batch, int32_t pool, const float* out,
                                const float* grad, const emb_update* update, const emb_dedup_set* d);
+// the dedup part alone (a look-ahead batch, deduplicated for the next call)
+emb_status check_dedup_step(const emb_tables* tables, const emb_batch* batch, const emb_dedup_set* d);
 
 }  // namespace emb

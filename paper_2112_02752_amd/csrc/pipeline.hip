@@ -24,6 +24,17 @@
 // implies the main stream's wait for group g - 2 is enqueued), so no wait
 // ever attaches to a later record, which could make the two streams wait
 // for each other.
+//
+// Calls can be chained (a training loop's look-ahead): a call may end with
+// the dedups of the group of batches after its steps (ahead), into the
+// buffer sets the next call's first group reads, and the next call then
+// starts with those dedups already enqueued (primed).  Groups are numbered
+// across calls (group_base) so that buffer parities alternate across the
+// boundary; the look-ahead dedups wait like any others for the main stream's
+// group of the same parity, and the next call's first group waits for them
+// through the same event.  Every side stream of a call still starts after
+// the work already on the main stream, so the batches it reads may be
+// written there until the call that dedups them.
 #include <atomic>
 #include <system_error>
 #include <thread>
@@ -50,11 +61,19 @@ struct Schedule {
   void* const* events;
   void* group_ws;  // non-null: each group's dedups as one emb_unique_ids_batched call
   size_t group_ws_bytes;
+  int32_t group_base;  // this call's first group in the numbering across calls (buffer parity)
+  int32_t primed;      // 1: the first group's dedups were enqueued by the previous call
+  int32_t ahead;       // 1: also dedup the group of K batches after the steps (batches[n_steps...])
 
   hipEvent_t ev_side(int parity, int s) const { return (hipEvent_t)events[3 + parity * n_side + s]; }
   hipStream_t side(int s) const { return (hipStream_t)sides[s]; }
-  int start(int g) const { return g * K; }
-  int count(int g) const { return n_steps - g * K < K ? n_steps - g * K : K; }
+  int parity(int g) const { return (group_base + g) & 1; }
+  // group g < ngroups: steps [g K, min(g K + K, n_steps)); group ngroups
+  // (with ahead): the K look-ahead batches
+  int start(int g) const { return g < ngroups ? g * K : n_steps; }
+  int count(int g) const { return g < ngroups ? (n_steps - g * K < K ? n_steps - g * K : K) : K; }
+  int side_first() const { return primed ? 1 : 0; }
+  int side_end() const { return ngroups + ahead; }
 };
 
 emb_status hip_ok(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_EHIP; }
@@ -70,9 +89,10 @@ emb_status dedup_one(const Schedule& c, int k, const emb_dedup_set& d, void* str
 
 // side stream s's part of group g: (for g >= 2) its wait for the main
 // stream's group g - 2, the dedups of the group dealt to it (i % n_side == s)
-// into the buffer sets of parity g % 2, and its record
+// into the buffer sets of the group's parity, and its record (groups 0 and 1
+// follow the call's start, and so every earlier group of the main stream)
 emb_status side_group(const Schedule& c, int g, int s) {
-  const int par = g % 2;
+  const int par = c.parity(g);
   if (g >= 2 && hipStreamWaitEvent(c.side(s), c.ev_main[par], 0) != hipSuccess) return EMB_EHIP;
   if (c.group_ws != nullptr) {
     // a group of one batch: its own dedup (one dedup in flight on this
@@ -105,7 +125,7 @@ emb_status side_group_all(const Schedule& c, int g) {
 // the main stream's part of group g: the wait for the group's dedups, then
 // each step's forward and fused backward + update, then the group's record
 emb_status main_group(const Schedule& c, int g) {
-  const int par = g % 2;
+  const int par = c.parity(g);
   emb_update u = *c.update;
   for (int i = 0; i < c.count(g); ++i) {
     const int k = c.start(g) + i;
@@ -125,15 +145,24 @@ emb_status main_group(const Schedule& c, int g) {
   return hip_ok(hipEventRecord(c.ev_main[par], c.main));
 }
 
+// the main stream's last wait of a call with look-ahead dedups: for them, so
+// that the end of the main stream's work is the end of all the call's work
+emb_status main_join_ahead(const Schedule& c) {
+  if (!c.ahead) return EMB_OK;
+  for (int s = 0; s < c.n_side; ++s)
+    if (hipStreamWaitEvent(c.main, c.ev_side(c.parity(c.ngroups), s), 0) != hipSuccess) return EMB_EHIP;
+  return EMB_OK;
+}
+
 // single thread: the side streams' part of group g + 1 is enqueued before the
 // main stream's part of group g
 emb_status run_single(const Schedule& c) {
-  emb_status st = side_group_all(c, 0);
+  emb_status st = c.side_first() == 0 ? side_group_all(c, 0) : EMB_OK;
   for (int g = 0; g < c.ngroups && st == EMB_OK; ++g) {
-    if (g + 1 < c.ngroups && (st = side_group_all(c, g + 1)) != EMB_OK) break;
+    if (g + 1 < c.side_end() && (st = side_group_all(c, g + 1)) != EMB_OK) break;
     st = main_group(c, g);
   }
-  return st;
+  return st == EMB_OK ? main_join_ahead(c) : st;
 }
 
 bool await_count(const std::atomic<int>& n, int v, const std::atomic<int>& failed) {
@@ -150,7 +179,7 @@ emb_status run_threaded(const Schedule& c) {
   std::atomic<int> side_done[kMaxSideStreams], main_done{0}, failed{0};
   emb_status side_st[kMaxSideStreams];
   for (int s = 0; s < c.n_side; ++s) {
-    side_done[s].store(0);
+    side_done[s].store(c.side_first());
     side_st[s] = EMB_OK;
   }
   auto side_work = [&](int s) {
@@ -160,7 +189,7 @@ emb_status run_threaded(const Schedule& c) {
       failed.store(1, std::memory_order_release);
       return;
     }
-    for (int g = 0; g < c.ngroups; ++g) {
+    for (int g = c.side_first(); g < c.side_end(); ++g) {
       if (failed.load(std::memory_order_acquire)) return;
       if (g >= 2 && !await_count(main_done, g - 1, failed)) return;
       side_st[s] = side_group(c, g, s);
@@ -194,6 +223,11 @@ emb_status run_threaded(const Schedule& c) {
     }
     main_done.store(g + 1, std::memory_order_release);
   }
+  if (st == EMB_OK && c.ahead) {
+    for (int s = 0; s < c.n_side; ++s)
+      if (!await_count(side_done[s], c.ngroups + 1, failed)) st = EMB_EHIP;
+    if (st == EMB_OK) st = main_join_ahead(c);
+  }
   for (int s = 0; s < c.n_side; ++s) helpers[s].join();
   for (int s = 0; s < c.n_side; ++s)
     if (side_st[s] != EMB_OK) return side_st[s];
@@ -208,13 +242,14 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
                               const emb_batch* batches, float* const* outs, const float* const* grads,
                               int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,
                               void* const* side_streams, void* const* events, void* group_ws,
-                              size_t group_ws_bytes) {
-  if (tables == nullptr || update == nullptr || n_steps < 0 || group < 1 || n_side < 1 || n_side > group)
+                              size_t group_ws_bytes, int32_t group_base, int32_t primed, int32_t ahead) {
+  if (tables == nullptr || update == nullptr || n_steps < 0 || group < 1 || n_side < 1 || n_side > group ||
+      group_base < 0 || (primed != 0 && primed != 1) || (ahead != 0 && ahead != 1))
     return EMB_EINVAL;
   if (n_side > kMaxSideStreams) return EMB_EUNSUPPORTED;
   if (group_ws != nullptr && n_side != 1) return EMB_EINVAL;  // a group's one dedup runs on one stream
   if (group_ws != nullptr && group > emb::kMaxGroup) return EMB_EUNSUPPORTED;
-  if (n_steps == 0) return EMB_OK;
+  if (n_steps == 0) return ahead ? EMB_EINVAL : EMB_OK;
   if (batches == nullptr || outs == nullptr || grads == nullptr || sets == nullptr || side_streams == nullptr ||
       events == nullptr)
     return EMB_EINVAL;
@@ -222,18 +257,6 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
     if (events[i] == nullptr) return EMB_EINVAL;
   for (int s = 0; s < n_side; ++s)
     if (side_streams[s] == nullptr || side_streams[s] == main_stream) return EMB_EINVAL;
-  // every step is checked before anything is enqueued
-  for (int k = 0; k < n_steps; ++k) {
-    const emb_status st = emb::check_pipeline_step(tables, &batches[k], pool, outs[k], grads[k], update,
-                                                   &sets[((k / group) % 2) * group + k % group]);
-    if (st != EMB_OK) return st;
-  }
-  if (group_ws != nullptr)
-    for (int g = 0; g * group < n_steps; ++g) {
-      const int count = n_steps - g * group < group ? n_steps - g * group : group;
-      const emb_status st = emb::check_dedup_group(tables, count, &batches[g * group], group_ws, group_ws_bytes);
-      if (st != EMB_OK) return st;
-    }
   Schedule c{};
   c.tables = tables;
   c.pool = pool;
@@ -254,11 +277,30 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
   c.events = events;
   c.group_ws = group_ws;
   c.group_ws_bytes = group_ws_bytes;
+  c.group_base = group_base;
+  c.primed = primed;
+  c.ahead = ahead;
+  // every step, and every look-ahead batch's dedup, is checked before
+  // anything is enqueued
+  for (int g = 0; g < c.side_end(); ++g) {
+    for (int i = 0; i < c.count(g); ++i) {
+      const int k = c.start(g) + i;
+      const emb_dedup_set* d = &sets[c.parity(g) * group + i];
+      const emb_status st = g < c.ngroups
+                                ? emb::check_pipeline_step(tables, &batches[k], pool, outs[k], grads[k], update, d)
+                                : emb::check_dedup_step(tables, &batches[k], d);
+      if (st != EMB_OK) return st;
+    }
+    if (group_ws != nullptr && g >= c.side_first()) {
+      const emb_status st = emb::check_dedup_group(tables, c.count(g), &batches[c.start(g)], group_ws, group_ws_bytes);
+      if (st != EMB_OK) return st;
+    }
+  }
   // the side streams start after the work already on the main stream
   if (hipEventRecord(c.ev_start, c.main) != hipSuccess) return EMB_EHIP;
   for (int s = 0; s < n_side; ++s)
     if (hipStreamWaitEvent(c.side(s), c.ev_start, 0) != hipSuccess) return EMB_EHIP;
-  return c.ngroups > 1 ? run_threaded(c) : run_single(c);
+  return c.ngroups + c.ahead > 1 ? run_threaded(c) : run_single(c);
 }
 
 }  // extern "C"

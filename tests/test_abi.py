@@ -205,8 +205,8 @@ def test_pipeline_steps_argument_checks():
     sides = (ctypes.c_void_p * 2)(0x10, 0x20)
     events = (ctypes.c_void_p * 7)(*([0x40] * 7))
     no_events = (ctypes.c_void_p * 7)(*([0x40] * 6 + [0]))
-    def f(*a, group_ws=None, group_ws_bytes=0):
-        return L.emb_pipeline_steps(*a, group_ws, group_ws_bytes)
+    def f(*a, group_ws=None, group_ws_bytes=0, group_base=0, primed=0, ahead=0):
+        return L.emb_pipeline_steps(*a, group_ws, group_ws_bytes, group_base, primed, ahead)
 
     tb, ub = ctypes.byref(t), ctypes.byref(upd)
     assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_OK   # nothing to do
@@ -259,6 +259,25 @@ def test_pipeline_steps_argument_checks():
     o17 = (ctypes.c_void_p * 17)(*([0x3000] * 17))
     assert f(tb, 0, ub, 17, b17, o17, o17, 17, many_sets, None, 1, sides, events,
              group_ws=0x200000, group_ws_bytes=1 << 30) == emb.EMB_EUNSUPPORTED                           # > 16
+    # chained calls: flags 0 or 1, a group base >= 0, a look-ahead only after
+    # steps, and the look-ahead batches' dedups checked before anything is
+    # enqueued (two steps in one group of two, then a look-ahead group of two
+    # in the sets of the other parity, its last batch or set bad in turn)
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, group_base=-1) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, primed=2) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, ahead=2) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events, ahead=1) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events, primed=1) == emb.EMB_OK
+    assert f(tb, 0, ub, 2, bad_b, outs4, grads4, 2, sets4, None, 1, sides, events, ahead=1) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 2, b4, outs4, grads4, 2, small, None, 1, sides, events, ahead=1) == emb.EMB_EWORKSPACE
+    # with group base 1 the steps take the last two sets and the look-ahead
+    # group the first two: the small first set is a look-ahead batch's
+    small0 = (emb.CDedupSet * 4)(*([emb.CDedupSet(0x5000, 0x5100, 0x5200, 0x5300, 0x5400, 0x100000, wsb - 256)]
+                                   + [good] * 3))
+    assert f(tb, 0, ub, 2, b4, outs4, grads4, 2, small0, None, 1, sides, events, ahead=1,
+             group_base=1) == emb.EMB_EWORKSPACE
+    assert f(tb, 0, ub, 2, b4, outs4, grads4, 2, sets4, None, 1, sides, events, ahead=1,
+             group_ws=0x200000, group_ws_bytes=L.emb_workspace_size(20, 2, t.dim) - 256) == emb.EMB_EWORKSPACE
 
 
 def test_unique_ids_batched_argument_checks():

@@ -690,6 +690,67 @@ def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd):
         np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("group,sides,gd,chunks", [(2, 1, True, (3, 4, 2)), (4, 1, True, (5, 8, 4)),
+                                                   (1, 1, False, (2, 3, 1)), (2, 2, False, (4, 3, 2)),
+                                                   (6, 3, False, (7, 6, 6)), (4, 1, True, (4, "discard", 5))])
+def test_pipelined_chained_calls_equal_serial(group, sides, gd, chunks):
+    """Chained calls: each call but the last also dedups the next call's
+    first group of batches, and the next call starts with those dedups done
+    (a training loop's look-ahead).  Tables, state and pooled outputs equal
+    those of serial steps bit for bit; a call that starts with other batches
+    than the ones deduplicated ahead is refused; after discard() the next
+    call dedups its own first group."""
+    _say(f"case pipelined chained group={group} side streams={sides} group dedup={gd} chunks={chunks}")
+    import torch
+    import paper_2112_02752_amd as emb
+    sizes = [c for c in chunks if c != "discard"]
+    nsteps = sum(sizes)
+    w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
+    batches = [synth.make_batch(w, s) for s in range(nsteps)]
+    nmax = max(len(b.indices) for b in batches)
+    dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
+              torch.from_numpy(b.grad).cuda()) for b in batches]
+    results = []
+    for mode in ("serial", "chained"):
+        dl = parity.device_layer_from_workload(w)
+        outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in dev_b]
+        if mode == "serial":
+            layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags)
+            for (b, g), out in zip(dev_b, outs):
+                layer.step(b, out, g)
+        else:
+            pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
+                                max_bags=w.num_bags, group=group, side_streams=sides, group_dedup=gd)
+            k = 0
+            for i, c in enumerate(chunks):
+                if c == "discard":
+                    pipe.discard()
+                    continue
+                nxt = chunks[i + 1] if i + 1 < len(chunks) else None
+                ahead = None
+                if isinstance(nxt, int):
+                    ahead = [b for b, _ in dev_b[k + c:k + c + group]]
+                elif nxt == "discard":
+                    # dedups ahead of batches that the next call will not start with
+                    ahead = [b for b, _ in dev_b[k + c + 1:k + c + 1 + group]]
+                steps = [(b, o, g) for (b, g), o in zip(dev_b[k:k + c], outs[k:k + c])]
+                if k > 0 and pipe._primed is not None:
+                    with pytest.raises(ValueError):
+                        # batch 0 is never among the batches deduplicated ahead
+                        pipe.run([(dev_b[0][0], outs[0], dev_b[0][1])])
+                pipe.run(steps, ahead=ahead)
+                k += c
+        torch.cuda.synchronize()
+        if mode == "chained":
+            pipe.check()
+        results.append((dl.W.cpu().numpy(), dl.state.cpu().numpy(), [o.cpu().numpy() for o in outs]))
+    (w0, s0, o0), (w1, s1, o1) = results
+    np.testing.assert_array_equal(w0, w1)
+    np.testing.assert_array_equal(s0, s1)
+    for a, b in zip(o0, o1):
+        np.testing.assert_array_equal(a, b)
+
+
 @pytest.mark.parametrize("name,nsteps,group,sides,gd", [("c3", 6, 4, 1, False), ("c3", 13, 6, 3, False),
                                                         ("c2", 3, 2, 1, False), ("c2", 5, 4, 2, False),
                                                         ("c3", 13, 6, 1, True), ("c2", 5, 4, 1, True)])

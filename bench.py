@@ -77,6 +77,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache repeat (for counter runs)")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--counters-run", action="store_true",
+                    help="only the warm-up, the timed region and the phase timings (the kernels of the timed "
+                         "configuration and nothing else, for rocprofv3 counter runs)")
     ap.add_argument("--route-ranks", type=int, default=8,
                     help="also time emb_route_ids of the same batches over this many equal row ranges (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget of the CPU oracle sample")
@@ -111,18 +114,22 @@ def file_sha(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def counter_traffic(workload: str):
+def counter_traffic(workload: str, dedup_kind: str):
     """HBM bytes per step of each phase from the committed rocprofv3 counter
     summary (FETCH_SIZE and WRITE_SIZE scaled by the copy-kernel calibration);
     None for every phase of another workload than the one the counters were
-    taken on, and for a phase whose kernel sources changed since."""
+    taken on, for the dedup phase of another dedup than theirs (one call per
+    batch, or batched calls over groups of K), and for a phase whose kernel
+    sources changed since."""
     if not os.path.exists(COUNTERS):
         return None
     kv = {}
-    measured_on = None
+    measured_on = dedup_on = None
     for line in open(COUNTERS):
         if line.startswith("Workload: "):
             measured_on = line[len("Workload: "):].strip()
+        if line.startswith("Dedup: "):
+            dedup_on = line[len("Dedup: "):].strip()
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
@@ -132,6 +139,7 @@ def counter_traffic(workload: str):
     for phase, src in PHASE_SOURCES.items():
         try:
             ok = all(kv.get(f"sha_{os.path.basename(f)}") == file_sha(f) for f in src)
+            ok = ok and (phase != "dedup" or dedup_on == dedup_kind)
             out[phase] = float(kv[f"hbm_bytes_{phase}"]) if ok else None
         except (KeyError, ValueError):
             out[phase] = None
@@ -372,7 +380,7 @@ def main():
     gpu_all_s = e_all[0].elapsed_time(e_all[1]) * 1e-3
     check_status("timed region")
     isolated = None
-    if n_iso:
+    if n_iso and not args.counters_run:
         # the same schedule as one call on its own over batches of its own
         pipe.discard()
         iso = range(total + n_ahead, total + n_ahead + n_iso)
@@ -390,34 +398,76 @@ def main():
 
     # the same batches again as serial steps with an event pair around each
     # step: the distribution of serial step times
-    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
-    for k, i in enumerate(range(t0_batch, total)):
-        sev[k][0].record(stream)
-        layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
-        sev[k][1].record(stream)
-    torch.cuda.synchronize()
-    step_s = [e[0].elapsed_time(e[1]) * 1e-3 for e in sev]
-    gpu_step_s = float(np.mean(step_s))
+    step_s = None
+    if not args.counters_run:
+        sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for k, i in enumerate(range(t0_batch, total)):
+            sev[k][0].record(stream)
+            layer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
+            sev[k][1].record(stream)
+        torch.cuda.synchronize()
+        step_s = [e[0].elapsed_time(e[1]) * 1e-3 for e in sev]
 
-    # the same batches again as serial steps with events between the phases:
-    # per-phase times for the roofline
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for k, i in enumerate(range(t0_batch, total)):
-        step(i, evs[k])
-    torch.cuda.synchronize()
+    # per-phase times for the roofline: the same batches again, one phase at a
+    # time with events between, through the kernels of the timed
+    # configuration.  With group dedups (the pipelined schedule's default)
+    # each group's dedups are one batched call and a batch's dedup time is its
+    # group's over the group's size; otherwise serial steps.
+    group_phases = pipe is not None and pipe.group_ws is not None
     ph = {"fwd": [], "dedup": [], "bwd_update": []}
-    for e in evs:
-        ph["fwd"].append(e[0].elapsed_time(e[1]) * 1e-3)
-        ph["dedup"].append(e[1].elapsed_time(e[2]) * 1e-3)
-        ph["bwd_update"].append(e[2].elapsed_time(e[3]) * 1e-3)
-    phased_step_s = [e[0].elapsed_time(e[3]) * 1e-3 for e in evs]
+    torch.cuda.synchronize()
+    if group_phases:
+        pipe.discard()
+        idx = list(range(t0_batch, total))
+        recs = []
+        for g0 in range(0, len(idx), pipe.K):
+            grp = idx[g0:g0 + pipe.K]
+            # the device spins while the host enqueues the group (a batched
+            # dedup and two calls per batch take the host longer than the
+            # device), so that the events time the kernels and not the host
+            torch.cuda._sleep(1 << 20)
+            eg = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            eg[0].record(stream)
+            emb.unique_ids_batched(tables, [dev_batches[i][0] for i in grp], pipe.sets[:len(grp)], pipe.group_ws,
+                                   sp)
+            eg[1].record(stream)
+            es = []
+            for j, i in enumerate(grp):
+                d = pipe.sets[j]
+                e3 = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                e3[0].record(stream)
+                emb.pool_fwd(tables, dev_batches[i][0], w.pool, out, sp)
+                e3[1].record(stream)
+                emb.grad_reduce(tables, dev_batches[i][0], w.pool, dev_batches[i][1], d.sort_perm, d.seg_offsets,
+                                d.unique_keys, d.num_unique, d.ws, opt=w.opt, lr=w.lr, eps=w.eps, state=state,
+                                stream=sp)
+                e3[2].record(stream)
+                es.append(e3)
+            recs.append((eg, es))
+        torch.cuda.synchronize()
+        check_status("phase timings")
+        for eg, es in recs:
+            dd = eg[0].elapsed_time(eg[1]) * 1e-3 / len(es)
+            for e3 in es:
+                ph["fwd"].append(e3[0].elapsed_time(e3[1]) * 1e-3)
+                ph["dedup"].append(dd)
+                ph["bwd_update"].append(e3[1].elapsed_time(e3[2]) * 1e-3)
+    else:
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+        for k, i in enumerate(range(t0_batch, total)):
+            step(i, evs[k])
+        torch.cuda.synchronize()
+        for e in evs:
+            ph["fwd"].append(e[0].elapsed_time(e[1]) * 1e-3)
+            ph["dedup"].append(e[1].elapsed_time(e[2]) * 1e-3)
+            ph["bwd_update"].append(e[2].elapsed_time(e[3]) * 1e-3)
+    phased_step_s = [a + b + c for a, b, c in zip(ph["fwd"], ph["dedup"], ph["bwd_update"])]
 
     # cold steps: the same batches again, with the L2s and the last-level
     # cache flushed by writing 1 GiB before each step (outside the events)
     flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     cold = None
-    if not args.no_cold:
+    if not args.no_cold and not args.counters_run:
         cold_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
         for k, i in enumerate(range(t0_batch, total)):
             flush.fill_(k & 0xff)
@@ -449,7 +499,7 @@ def main():
     # routing of the same batches to the owners of equal row ranges: the step
     # before the forward when the table is sharded over that many devices
     routing = None
-    if args.route_ranks > 0:
+    if args.route_ranks > 0 and not args.counters_run:
         Wr = args.route_ranks
         shard = [w.total_rows * r // Wr for r in range(Wr + 1)]
         i32 = dict(dtype=torch.int32, device=dev)
@@ -477,7 +527,7 @@ def main():
     # the serial step captured in a HIP graph: one batch, replayed back to back,
     # against the same batch's eager steps (the step launches only kernels)
     graph = None
-    if not args.no_graph:
+    if not args.no_graph and not args.counters_run:
         i0 = t0_batch
         reps = 20
         ge = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
@@ -517,10 +567,15 @@ def main():
     U_avg = float(np.mean(us))
     models = byte_models(w, N_avg, U_avg)
     t_phase = {k: float(np.mean(v)) for k, v in ph.items()}
-    traffic = counter_traffic(f"{w.name}: {w.description}")
+    dedup_kind = f"emb_unique_ids_batched, groups of {pipe.K}" if group_phases else "emb_unique_ids"
+    traffic = counter_traffic(f"{w.name}: {w.description}", dedup_kind)
+    dedup_kernels = ("per group of batches: k_prepare_group, then per pass k_tile_counts + k_column_scan + "
+                     "k_sort_pass, then k_split_group, k_uniq_counts_group, k_uniq_scan_group, k_unique_group "
+                     f"(emb_unique_ids_batched over groups of {pipe.K}; per batch: the group's time over its "
+                     "size)") if group_phases else "k_sort_pass x passes + k_unique (emb_unique_ids)"
     phases = {}
     for name, kern in (("fwd", "k_pool_fwd (emb_pool_fwd)"),
-                       ("dedup", "k_sort_pass x passes + k_unique (emb_unique_ids)"),
+                       ("dedup", dedup_kernels),
                        ("bwd_update", "k_reduce_main + k_reduce_combine (emb_grad_reduce, fused update)")):
         log_b, comp_b = models[name]
         t = t_phase[name]
@@ -566,10 +621,10 @@ def main():
         "step_us": {"schedule": args.schedule, "timed_region_gpu_per_step": gpu_all_s / args.steps * 1e6,
                     "serial_note": "mean / median / p10 / p90: serial steps of the same batches, one event pair "
                                    "around each",
-                    "mean": gpu_step_s * 1e6,
-                    "median": float(np.median(step_s)) * 1e6,
-                    "p10": float(np.percentile(step_s, 10)) * 1e6,
-                    "p90": float(np.percentile(step_s, 90)) * 1e6,
+                    "mean": float(np.mean(step_s)) * 1e6 if step_s else None,
+                    "median": float(np.median(step_s)) * 1e6 if step_s else None,
+                    "p10": float(np.percentile(step_s, 10)) * 1e6 if step_s else None,
+                    "p90": float(np.percentile(step_s, 90)) * 1e6 if step_s else None,
                     "host_enqueue_us": t_enq / args.steps * 1e6,
                     "with_phase_events_median": float(np.median(phased_step_s)) * 1e6},
         "isolated_call": isolated,
@@ -579,7 +634,7 @@ def main():
         "graph": graph,
         "cost_model": cost_model_check(w, N_avg, U_avg, t_phase, ms),
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.counters_run:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(w, batches, args.cpu_seconds)
     print(json.dumps(line), flush=True)

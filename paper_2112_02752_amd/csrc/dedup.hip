@@ -151,6 +151,14 @@ struct PassArgs {
   uint32_t* totals_all;
   int32_t npass;
   int32_t pass_shift[kMaxPasses], pass_bits[kMaxPasses];
+  // the last pass of a group sort (split_n > 0): values and bags go straight
+  // to each member's own buffers instead of vals_out and bags_out; a key's
+  // member is key >> split_bits (0 with one member), its sorted position in
+  // the member dst - split_P[m] (< split_N[m]), its value less split_P[m]
+  int32_t split_n, split_bits;
+  int32_t split_P[kMaxGroup], split_N[kMaxGroup];
+  int32_t* split_perm[kMaxGroup];
+  int32_t* split_bag[kMaxGroup];
 };
 
 // Prefix blocks of a co-resident pass.  Groups: one block per kPrefixGroup
@@ -743,7 +751,8 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   __syncthreads();
 
   // write the tile out in digit runs: keys and values, then the bags
-  // through the keys' buffer, each slot to the destination found for it
+  // through the values' buffer, each slot to the destination found for it
+  // (in a group sort's last pass, values and bags to the key's member)
   const int64_t tstart = (int64_t)tile * TILE;
   const int nvalid = (int)min((int64_t)TILE, (int64_t)a.N - tstart);
   uint32_t dst[IT];
@@ -757,7 +766,14 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
       dst[j] = s_gbase[d] + (uint32_t)s - s_tstart[d];
       if (dst[j] < (uint32_t)a.N) {
         a.keys_out[dst[j]] = k;
-        a.vals_out[dst[j]] = s_vals[s];
+        if (a.split_n > 0) {
+          const uint32_t m = a.split_n > 1 ? k >> a.split_bits : 0u;
+          const uint32_t o = dst[j] - (uint32_t)a.split_P[m < (uint32_t)a.split_n ? m : 0];
+          if (m < (uint32_t)a.split_n && o < (uint32_t)a.split_N[m]) a.split_perm[m][o] = s_vals[s] - a.split_P[m];
+          else flag_error(a.hdr, gcall, 2u);  // a key outside its member's share
+        } else {
+          a.vals_out[dst[j]] = s_vals[s];
+        }
       } else {
         flag_error(a.hdr, gcall, 2u);  // digit totals inconsistent with the keys
       }
@@ -766,11 +782,22 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < IT; ++i)
-    if (lp[i] != 0xffffffffu) s_keys[lp[i]] = (uint32_t)bag[i];
+    if (lp[i] != 0xffffffffu) s_vals[lp[i]] = bag[i];
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < IT; ++j)
-    if (dst[j] < (uint32_t)a.N) a.bags_out[dst[j]] = (int32_t)s_keys[tid + j * kSortThreads];
+  for (int j = 0; j < IT; ++j) {
+    if (dst[j] >= (uint32_t)a.N) continue;
+    const int s = tid + j * kSortThreads;
+    if (a.split_n > 0) {
+      const uint32_t m = a.split_n > 1 ? s_keys[s] >> a.split_bits : 0u;
+      if (m < (uint32_t)a.split_n) {
+        const uint32_t o = dst[j] - (uint32_t)a.split_P[m];
+        if (o < (uint32_t)a.split_N[m]) a.split_bag[m][o] = s_vals[s];
+      }
+    } else {
+      a.bags_out[dst[j]] = s_vals[s];
+    }
+  }
 }
 
 // ------------------------------------------------- reduce-then-scan passes
@@ -1484,59 +1511,6 @@ __global__ __launch_bounds__(kPrepThreads) void k_prepare_group(PrepGroupArgs a)
   prepare_block(v, (int)blockIdx.x - a.first[i], s_off);
 }
 
-struct SplitMember {
-  int64_t P;
-  int32_t N;
-  int32_t* sort_perm;
-  int32_t* sorted_bag;
-  int32_t* num_unique;
-  int32_t* seg_offsets;
-  WsHeader* hdr;
-};
-
-struct SplitGroupArgs {
-  int32_t n, sorted;             // sorted: the group's passes ran
-  int32_t first[kMaxGroup + 1];
-  SplitMember b[kMaxGroup];
-  const int32_t* perm;           // the group's sort permutation (group positions)
-  const int32_t* bags;           // bag ids of the group's sorted positions
-  WsHeader* ghdr;                // the group's workspace header
-};
-
-constexpr int kSplitThreads = 256;
-constexpr int kSplitItems = 8;
-
-__global__ __launch_bounds__(kSplitThreads) void k_split_group(SplitGroupArgs a) {
-  const int i = group_member(a.first, a.n, (int)blockIdx.x);
-  const SplitMember& m = a.b[i];
-  const int lb = (int)blockIdx.x - a.first[i];
-  const int tid = threadIdx.x;
-  if (lb == 0 && tid == 0) {
-    if (m.N == 0) {
-      m.num_unique[0] = 0;
-      m.seg_offsets[0] = 0;
-    } else {
-      // the member's own call generation; the group sort's error bits become
-      // its own, so that its unique scan and gradient reduce see them
-      const uint32_t g = next_gen(m.hdr->gen);
-      m.hdr->cur = g;
-      const uint32_t bits = call_errors(a.ghdr, a.ghdr->cur) & kDedupErrors;
-      if (bits) flag_error(m.hdr, g, bits);
-    }
-  }
-  // the group call is complete: its generation becomes the group header's
-  if (blockIdx.x == 0 && tid == 0 && a.sorted) a.ghdr->gen = a.ghdr->cur;
-  const int64_t base = (int64_t)lb * (kSplitThreads * kSplitItems);
-#pragma unroll
-  for (int k = 0; k < kSplitItems; ++k) {
-    const int64_t j = base + k * kSplitThreads + tid;
-    if (j < m.N) {
-      m.sort_perm[j] = a.perm[m.P + j] - (int32_t)m.P;
-      m.sorted_bag[j] = a.bags[m.P + j];
-    }
-  }
-}
-
 struct UniqMember {
   int64_t P;
   int32_t N, ntiles, nchunks;
@@ -1556,6 +1530,8 @@ struct UniqGroupArgs {
   int32_t first[kMaxGroup + 1];  // first unique tile block of each member
   UniqMember b[kMaxGroup];
   const uint32_t* skeys;         // the group's sorted keys
+  WsHeader* ghdr;                // the group call's header
+  int32_t sorted;                // the group's passes ran
 };
 
 __global__ __launch_bounds__(kUniqThreads) void k_uniq_counts_group(UniqGroupArgs a) {
@@ -1566,9 +1542,26 @@ __global__ __launch_bounds__(kUniqThreads) void k_uniq_counts_group(UniqGroupArg
   uniq_counts_tile(c, (int)blockIdx.x - a.first[i], s_c, s_q);
 }
 
+// One block per member: its call generation (the group sort's error bits
+// become its own, so that its unique scan and gradient reduce see them; an
+// empty member's outputs instead), then its unique counts' scan.  Block 0
+// also makes the group call's generation the group header's (the call is
+// complete: no later kernel of it reads the group header).
 __global__ __launch_bounds__(kUniqScanThreads) void k_uniq_scan_group(UniqGroupArgs a) {
   __shared__ uint32_t s_c[kUniqScanThreads / kWave], s_q[kUniqScanThreads / kWave];
   const UniqMember& m = a.b[blockIdx.x];
+  if (threadIdx.x == 0) {
+    if (m.N == 0) {
+      m.num_unique[0] = 0;
+      m.seg_offsets[0] = 0;
+    } else {
+      const uint32_t g = next_gen(m.hdr->gen);
+      m.hdr->cur = g;
+      const uint32_t bits = call_errors(a.ghdr, a.ghdr->cur) & kDedupErrors;
+      if (bits) flag_error(m.hdr, g, bits);
+    }
+    if (blockIdx.x == 0 && a.sorted) a.ghdr->gen = a.ghdr->cur;
+  }
   if (m.N > 0) uniq_scan_block(m.words, m.ntiles, s_c, s_q);
 }
 
@@ -1686,6 +1679,17 @@ hipError_t launch_dedup_group(const GroupDedupLaunch& p, hipStream_t s) {
       xa.bits = p.plan.bits[ps];
       xa.pass = ps;
       xa.status_stride = status_stride;
+      if (last) {
+        // each member's values and bags straight to its own buffers
+        xa.split_n = n;
+        xa.split_bits = p.key_bits;
+        for (int i = 0; i < n; ++i) {
+          xa.split_P[i] = (int32_t)p.m[i].P;
+          xa.split_N[i] = p.m[i].N;
+          xa.split_perm[i] = p.m[i].sort_perm;
+          xa.split_bag[i] = p.m[i].sorted_bag;
+        }
+      }
       CountArgs ca{};
       ca.keys = kin;
       ca.N = N;
@@ -1717,26 +1721,6 @@ hipError_t launch_dedup_group(const GroupDedupLaunch& p, hipStream_t s) {
     }
   }
 
-  // each member's share of the sorted order, and its call generation
-  SplitGroupArgs sa{};
-  sa.n = n;
-  sa.sorted = p.N > 0 ? 1 : 0;
-  sa.perm = group_perm;
-  sa.bags = sorted_bag;
-  sa.ghdr = ghdr;
-  int sblocks = 0;
-  for (int i = 0; i < n; ++i) {
-    const GroupMember& m = p.m[i];
-    sa.first[i] = sblocks;
-    sa.b[i] = SplitMember{m.P, m.N, m.sort_perm, m.sorted_bag, m.num_unique, m.seg_offsets, m.hdr};
-    const int per = kSplitThreads * kSplitItems;
-    sblocks += m.N > 0 ? (m.N + per - 1) / per : 1;
-  }
-  sa.first[n] = sblocks;
-  hipLaunchKernelGGL(k_split_group, dim3((unsigned)sblocks), dim3(kSplitThreads), 0, s, sa);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (p.N == 0) return hipSuccess;
-
   // each member's unique scan on its share
   UniqGroupArgs ua{};
   ua.n = n;
@@ -1752,10 +1736,17 @@ hipError_t launch_dedup_group(const GroupDedupLaunch& p, hipStream_t s) {
     tiles += nt;
   }
   ua.first[n] = tiles;
-  hipLaunchKernelGGL(k_uniq_counts_group, dim3((unsigned)tiles), dim3(kUniqThreads), 0, s, ua);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  ua.ghdr = ghdr;
+  ua.sorted = p.N > 0 ? 1 : 0;
+  if (tiles > 0) {
+    hipLaunchKernelGGL(k_uniq_counts_group, dim3((unsigned)tiles), dim3(kUniqThreads), 0, s, ua);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  // every member's call generation (and an empty member's outputs), then
+  // the scan of the unique counts
   hipLaunchKernelGGL(k_uniq_scan_group, dim3((unsigned)n), dim3(kUniqScanThreads), 0, s, ua);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (tiles == 0) return hipSuccess;
   hipLaunchKernelGGL(k_unique_group, dim3((unsigned)tiles), dim3(kUniqThreads), 0, s, ua);
   return hipGetLastError();
 }

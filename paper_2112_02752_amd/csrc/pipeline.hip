@@ -122,27 +122,36 @@ emb_status side_group_all(const Schedule& c, int g) {
   return EMB_OK;
 }
 
-// the main stream's part of group g: the wait for the group's dedups, then
-// each step's forward and fused backward + update, then the group's record
-emb_status main_group(const Schedule& c, int g) {
+// The main stream's part of group g: each step's forward and fused backward
+// + update, then the group's record.  The group's first forward reads no
+// dedup output, so it comes before the wait for the group's dedups (and, in
+// the threaded enqueue, before the host waits for their record).
+emb_status main_first_forward(const Schedule& c, int g) {
+  const int k = c.start(g);
+  return emb_pool_fwd(c.tables, &c.batches[k], c.pool, c.outs[k], c.main);
+}
+
+emb_status main_group_rest(const Schedule& c, int g) {
   const int par = c.parity(g);
+  for (int s = 0; s < c.n_side; ++s)
+    if (hipStreamWaitEvent(c.main, c.ev_side(par, s), 0) != hipSuccess) return EMB_EHIP;
   emb_update u = *c.update;
   for (int i = 0; i < c.count(g); ++i) {
     const int k = c.start(g) + i;
     const emb_dedup_set& d = c.sets[par * c.K + i];
     u.seed = c.update->seed + (uint64_t)k;  // bf16 stochastic rounding draws fresh bits every step
-    emb_status st = emb_pool_fwd(c.tables, &c.batches[k], c.pool, c.outs[k], c.main);
-    if (st != EMB_OK) return st;
-    // the group's first forward needs no dedup output: the wait for the
-    // group's dedups comes after it, before the first gradient reduce
-    if (i == 0)
-      for (int s = 0; s < c.n_side; ++s)
-        if (hipStreamWaitEvent(c.main, c.ev_side(par, s), 0) != hipSuccess) return EMB_EHIP;
-    st = emb_grad_reduce(c.tables, &c.batches[k], c.pool, c.grads[k], d.sort_perm, d.seg_offsets, d.unique_keys,
-                         d.num_unique, nullptr, &u, d.ws, d.ws_bytes, c.main);
+    emb_status st = i > 0 ? emb_pool_fwd(c.tables, &c.batches[k], c.pool, c.outs[k], c.main) : EMB_OK;
+    if (st == EMB_OK)
+      st = emb_grad_reduce(c.tables, &c.batches[k], c.pool, c.grads[k], d.sort_perm, d.seg_offsets, d.unique_keys,
+                           d.num_unique, nullptr, &u, d.ws, d.ws_bytes, c.main);
     if (st != EMB_OK) return st;
   }
   return hip_ok(hipEventRecord(c.ev_main[par], c.main));
+}
+
+emb_status main_group(const Schedule& c, int g) {
+  const emb_status st = main_first_forward(c, g);
+  return st == EMB_OK ? main_group_rest(c, g) : st;
 }
 
 // the main stream's last wait of a call with look-ahead dedups: for them, so
@@ -156,13 +165,20 @@ emb_status main_join_ahead(const Schedule& c) {
 
 // single thread: the side streams' part of group g + 1 is enqueued before the
 // main stream's part of group g
-emb_status run_single(const Schedule& c) {
-  emb_status st = c.side_first() == 0 ? side_group_all(c, 0) : EMB_OK;
-  for (int g = 0; g < c.ngroups && st == EMB_OK; ++g) {
+// from group g_first on, the side streams' part of group g_first already
+// enqueued: each next group's side part, then this group's main part
+emb_status run_single_from(const Schedule& c, int g_first) {
+  emb_status st = EMB_OK;
+  for (int g = g_first; g < c.ngroups && st == EMB_OK; ++g) {
     if (g + 1 < c.side_end() && (st = side_group_all(c, g + 1)) != EMB_OK) break;
     st = main_group(c, g);
   }
   return st == EMB_OK ? main_join_ahead(c) : st;
+}
+
+emb_status run_single(const Schedule& c) {
+  const emb_status st = c.side_first() == 0 ? side_group_all(c, 0) : EMB_OK;
+  return st == EMB_OK ? run_single_from(c, 0) : st;
 }
 
 bool await_count(const std::atomic<int>& n, int v, const std::atomic<int>& failed) {
@@ -200,6 +216,18 @@ emb_status run_threaded(const Schedule& c) {
       side_done[s].store(g + 1, std::memory_order_release);
     }
   };
+  // With the first group's dedups enqueued by the previous call, its main
+  // stream work goes first, before any helper thread starts: the device then
+  // has work at once instead of after the helpers' first launches (launches
+  // from several threads take turns).  The helpers' first group (1) waits for
+  // nothing of the main stream's.
+  emb_status st = EMB_OK;
+  int g_first = 0;
+  if (c.primed) {
+    if ((st = main_group(c, 0)) != EMB_OK) return st;
+    main_done.store(1, std::memory_order_release);
+    g_first = 1;
+  }
   std::thread helpers[kMaxSideStreams];
   int started = 0;
   try {
@@ -207,17 +235,26 @@ emb_status run_threaded(const Schedule& c) {
   } catch (const std::system_error&) {
     failed.store(1, std::memory_order_release);
     for (int s = 0; s < started; ++s) helpers[s].join();
-    // with no thread started nothing is enqueued yet: the same schedule from
-    // this thread; otherwise the started ones may have enqueued dedups of
-    // the first groups (which nothing waits on) and the call fails
-    return started == 0 ? run_single(c) : EMB_EHIP;
+    // with no thread started, no dedup of this call is enqueued yet: the rest
+    // of the schedule from this thread (a primed call's first group is
+    // already enqueued); otherwise the started ones may have enqueued dedups
+    // of the next groups (which nothing waits on) and the call fails
+    if (started > 0) return EMB_EHIP;
+    if (g_first == 0) return run_single(c);
+    // the primed first group's main stream work is enqueued: the side
+    // streams' group 1, then the rest in the single-thread order
+    st = 1 < c.side_end() ? side_group_all(c, 1) : EMB_OK;
+    return st == EMB_OK ? run_single_from(c, 1) : st;
   }
-  emb_status st = EMB_OK;
-  for (int g = 0; g < c.ngroups && st == EMB_OK; ++g) {
+  for (int g = g_first; g < c.ngroups && st == EMB_OK; ++g) {
+    if ((st = main_first_forward(c, g)) != EMB_OK) {
+      failed.store(1, std::memory_order_release);
+      break;
+    }
     for (int s = 0; s < c.n_side; ++s)
       if (!await_count(side_done[s], g + 1, failed)) st = EMB_EHIP;
     if (st != EMB_OK) break;
-    if ((st = main_group(c, g)) != EMB_OK) {
+    if ((st = main_group_rest(c, g)) != EMB_OK) {
       failed.store(1, std::memory_order_release);
       break;
     }

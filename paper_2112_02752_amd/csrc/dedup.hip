@@ -553,8 +553,12 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
   uint32_t* s_hist = reinterpret_cast<uint32_t*>(s_arena);
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & (kWave - 1);
+  // co-resident: the histograms start from zero (the per-wave counters are
+  // cleared after them); otherwise the per-wave counters at once
   if (a.coresident)
     for (int i = tid; i < kMaxPasses * ND; i += kSortThreads) s_hist[i] = 0u;
+  else
+    for (int i = tid; i < NW * ND / 2; i += kSortThreads) reinterpret_cast<uint32_t*>(s_arena + Lds::kCnt)[i] = 0u;
   if (a.search_bags && a.T > 1)
     for (int t = tid; t < a.T; t += kSortThreads) s_toff[t] = a.ro.off[t];
   // the previous pass is complete: clear its totals for the next call
@@ -656,9 +660,11 @@ __global__ __launch_bounds__(kSortThreads, 4) void k_sort_pass(PassArgs a) {
     publish_counts();
   }
   // the histograms are out: the per-wave counters start from zero
-  __syncthreads();
-  for (int i = tid; i < NW * ND / 2; i += kSortThreads) reinterpret_cast<uint32_t*>(s_arena + Lds::kCnt)[i] = 0u;
-  __syncthreads();
+  if (a.coresident) {
+    __syncthreads();
+    for (int i = tid; i < NW * ND / 2; i += kSortThreads) reinterpret_cast<uint32_t*>(s_arena + Lds::kCnt)[i] = 0u;
+    __syncthreads();
+  }
 
   // rank each element among the earlier elements of its wave with its digit
 #pragma unroll

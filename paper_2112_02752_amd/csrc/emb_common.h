@@ -282,8 +282,9 @@ __device__ __forceinline__ void flag_error(WsHeader* h, uint32_t g, uint32_t bit
 
 // a wait of call g that started at t0 has run out (or another wait of the call has)
 __device__ __forceinline__ bool wait_over(const WsHeader* h, uint32_t g, uint64_t t0, uint32_t spins) {
-  // the call's error word is read on the first retry and every 32nd after it
-  if ((spins & 31u) == 1u && (call_errors(h, g) & 1u)) return true;
+  // the call's error word is read every 32nd retry (each read is a round
+  // trip of its own, which a poll that succeeds on its next load would pay)
+  if ((spins & 31u) == 0u && (call_errors(h, g) & 1u)) return true;
   return wait_clock() - t0 > kWaitTicks;
 }
 

@@ -87,9 +87,10 @@ def test_failed_dedup_writes_nothing_and_is_reported(name, bags_mult):
     assert torch.equal(dl.state, S0), "a failed step wrote optimizer state"
     bits, site, block, timeouts = layer.status()
     assert bits & 1, (bits, site, block, timeouts)
-    # co-resident sort passes: a wait that found a word not yet published
-    # gave up on its first retry and was recorded (whether any wait found
-    # one depends on timing: the published words may all be there in time)
+    # co-resident sort passes: a wait that kept finding a word not yet
+    # published gave up at its check of the error bits and was recorded
+    # (whether any wait retries that long depends on timing: the published
+    # words may all be there in time)
     assert (site != 0) == (timeouts > 0), (bits, site, block, timeouts)
     _say(f"  recorded waits that gave up: {timeouts} (first site {site:#x})")
     with pytest.raises(emb.StepFailed):

@@ -435,7 +435,8 @@ def main():
             # the device spins while the host enqueues the group (a batched
             # dedup and two calls per batch take the host longer than the
             # device), so that the events time the kernels and not the host
-            torch.cuda._sleep(1 << 20)
+            if hasattr(torch.cuda, "_sleep"):
+                torch.cuda._sleep(1 << 20)
             eg = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
             eg[0].record(stream)
             emb.unique_ids_batched(tables, [dev_batches[i][0] for i in grp], pipe.sets[:len(grp)], pipe.group_ws,

@@ -751,6 +751,48 @@ def test_pipelined_chained_calls_equal_serial(group, sides, gd, chunks):
         np.testing.assert_array_equal(a, b)
 
 
+def test_pipelined_chained_bf16_tables_stochastic_rounding():
+    """Chained pipelined calls on the 26-table bf16 workload (scaled down)
+    with stochastic rounding: each step draws its bits from seed + its step
+    index across the calls, as serial steps do, so tables, state and pooled
+    outputs equal those of serial steps bit for bit."""
+    _say("case pipelined chained c4-small bf16 stochastic rounding")
+    import torch
+    import paper_2112_02752_amd as emb
+    w = synth.scaled(synth.workload("c4"), rows_div=100, bags_div=64, name="c4-small")
+    chunks, group = (5, 4, 3), 2
+    batches = [synth.make_batch(w, s) for s in range(sum(chunks))]
+    nmax = max(len(b.indices) for b in batches)
+    dev_b = [(emb.Batch(torch.from_numpy(b.offsets).cuda(), torch.from_numpy(b.indices).cuda(), w.bags_per_table),
+              torch.from_numpy(b.grad).cuda()) for b in batches]
+    results = []
+    for mode in ("serial", "chained"):
+        dl = parity.device_layer_from_workload(w)
+        outs = [torch.empty((w.num_bags, w.dim), dtype=torch.float32, device="cuda") for _ in dev_b]
+        if mode == "serial":
+            layer = emb.Layer(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax, max_bags=w.num_bags,
+                              rounding="stochastic", seed=91)
+            for (b, g), out in zip(dev_b, outs):
+                layer.step(b, out, g)
+        else:
+            pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
+                                max_bags=w.num_bags, group=group, rounding="stochastic", seed=91)
+            k = 0
+            for i, c in enumerate(chunks):
+                ahead = [b for b, _ in dev_b[k + c:k + c + group]] if i + 1 < len(chunks) else None
+                pipe.run([(b, o, g) for (b, g), o in zip(dev_b[k:k + c], outs[k:k + c])], ahead=ahead)
+                k += c
+        torch.cuda.synchronize()
+        if mode == "chained":
+            pipe.check()
+        results.append((dl.W.view(torch.int16).cpu().numpy(), dl.state.cpu().numpy(), [o.cpu().numpy() for o in outs]))
+    (w0, s0, o0), (w1, s1, o1) = results
+    np.testing.assert_array_equal(w0, w1)
+    np.testing.assert_array_equal(s0, s1)
+    for a, b in zip(o0, o1):
+        np.testing.assert_array_equal(a, b)
+
+
 @pytest.mark.parametrize("name,nsteps,group,sides,gd", [("c3", 6, 4, 1, False), ("c3", 13, 6, 3, False),
                                                         ("c2", 3, 2, 1, False), ("c2", 5, 4, 2, False),
                                                         ("c3", 13, 6, 1, True), ("c2", 5, 4, 1, True)])

@@ -200,8 +200,8 @@ class Batch:
 
     def c(self) -> CBatch:
         """The C descriptor; rebuilt if a tensor was replaced or reallocated."""
-        key = (_ptr(self.offsets), _ptr(self.indices), int(self.indices.numel()), self.bags_per_table,
-               int(self.indices.element_size()))
+        idx = self.indices
+        key = (self.offsets.data_ptr(), idx.data_ptr(), idx.numel(), self.bags_per_table, idx.element_size())
         if getattr(self, "_ckey", None) != key:
             n = key[2]
             self._c = CBatch(self.bags_per_table, key[0], key[1] if n else None, n, key[4])
@@ -649,12 +649,21 @@ class Pipeline:
                 raise ValueError("the first steps are not the batches deduplicated ahead by the last call "
                                  "(call discard() to drop them)")
             primed = 1
-        cbs = [b.c() for b, _, _ in steps] + ([b.c() for b in ahead] if ahead else [])
+        cbs = [b.c() for b, _, _ in steps]
+        if ahead:
+            cbs += [b.c() for b in ahead]
         if max(c.num_indices for c in cbs) > self.max_indices:
             raise ValueError("batch larger than the pipeline's buffers")
         batches = (CBatch * len(cbs))(*cbs)
-        outs = (ctypes.c_void_p * n)(*[_ptr(o) for _, o, _ in steps])
-        grads = (ctypes.c_void_p * n)(*[_ptr(g) for _, _, g in steps])
+        ptrs = {}  # outputs are often one tensor for every step
+
+        def ptr(t):
+            v = ptrs.get(id(t))
+            if v is None and t is not None:
+                v = ptrs[id(t)] = t.data_ptr()
+            return v
+        outs = (ctypes.c_void_p * n)(*[ptr(o) for _, o, _ in steps])
+        grads = (ctypes.c_void_p * n)(*[ptr(g) for _, _, g in steps])
         self._updc.seed = self.seed + self.steps_done
         gws = self.group_ws
         _check("emb_pipeline_steps", lib().emb_pipeline_steps(

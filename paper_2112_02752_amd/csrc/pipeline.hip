@@ -176,7 +176,16 @@ emb_status run_single_from(const Schedule& c, int g_first) {
   return st == EMB_OK ? main_join_ahead(c) : st;
 }
 
+// side stream s's wait for the call's start record, enqueued just before its
+// first work by the thread that enqueues that work (the wait costs the host
+// 15-25 us, which stays off the main stream's first launches)
+emb_status side_wait_start(const Schedule& c, int s) {
+  return hip_ok(hipStreamWaitEvent(c.side(s), c.ev_start, 0));
+}
+
 emb_status run_single(const Schedule& c) {
+  for (int s = 0; s < c.n_side; ++s)
+    if (side_wait_start(c, s) != EMB_OK) return EMB_EHIP;
   const emb_status st = c.side_first() == 0 ? side_group_all(c, 0) : EMB_OK;
   return st == EMB_OK ? run_single_from(c, 0) : st;
 }
@@ -200,7 +209,7 @@ emb_status run_threaded(const Schedule& c) {
   }
   auto side_work = [&](int s) {
     // the current device is per thread: the caller's
-    if (hipSetDevice(device) != hipSuccess) {
+    if (hipSetDevice(device) != hipSuccess || side_wait_start(c, s) != EMB_OK) {
       side_st[s] = EMB_EHIP;
       failed.store(1, std::memory_order_release);
       return;
@@ -241,6 +250,8 @@ emb_status run_threaded(const Schedule& c) {
     // of the next groups (which nothing waits on) and the call fails
     if (started > 0) return EMB_EHIP;
     if (g_first == 0) return run_single(c);
+    for (int s = 0; s < c.n_side; ++s)
+      if (side_wait_start(c, s) != EMB_OK) return EMB_EHIP;
     // the primed first group's main stream work is enqueued: the side
     // streams' group 1, then the rest in the single-thread order
     st = 1 < c.side_end() ? side_group_all(c, 1) : EMB_OK;
@@ -333,10 +344,9 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
       if (st != EMB_OK) return st;
     }
   }
-  // the side streams start after the work already on the main stream
+  // the side streams start after the work already on the main stream (their
+  // waits for this record are enqueued by whichever thread enqueues their work)
   if (hipEventRecord(c.ev_start, c.main) != hipSuccess) return EMB_EHIP;
-  for (int s = 0; s < n_side; ++s)
-    if (hipStreamWaitEvent(c.side(s), c.ev_start, 0) != hipSuccess) return EMB_EHIP;
   return c.ngroups + c.ahead > 1 ? run_threaded(c) : run_single(c);
 }
 

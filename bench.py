@@ -65,6 +65,8 @@ def parse():
                          "staleness one (the forward of batch k+1 on a side stream, reading the table before "
                          "the update of batch k, alongside the dedup of batch k)")
     ap.add_argument("--group", type=int, default=4, help="batches per group of the pipelined schedule")
+    ap.add_argument("--depth", type=int, default=2,
+                    help="pipelined: buffer set parities; chained calls look ahead depth - 1 groups")
     ap.add_argument("--no-chain", action="store_true",
                     help="pipelined: time one call on its own (its first group's dedups and its last group's "
                          "forward and update not overlapped) instead of a call in a chain of calls")
@@ -268,13 +270,15 @@ def main():
     t0_batch = n_warm
     total = n_warm + args.steps
     # the stale schedule's last timed step runs the forward of one more batch;
-    # the chained pipelined schedule's timed call dedups the group after its
-    # steps, and its own first group is deduplicated at the end of the
-    # warm-up: the timed region holds exactly `steps` dedups and `steps`
-    # forwards, backwards and updates.  The pipelined schedule also runs one
-    # call on its own over `steps` batches of their own (isolated_call).
-    chain = args.schedule == "pipelined" and not args.no_chain
-    n_ahead = args.group if chain else 0
+    # the chained pipelined schedule's timed call dedups the groups after its
+    # steps (depth - 1 of them, as many as its steps hold), and its own first
+    # groups are deduplicated at the end of the warm-up: the timed region
+    # holds exactly `steps` dedups and `steps` forwards, backwards and
+    # updates.  The pipelined schedule also runs one call on its own over
+    # `steps` batches of their own (isolated_call).
+    look = min(args.depth - 1, args.steps // args.group) if args.schedule == "pipelined" else 0
+    chain = args.schedule == "pipelined" and not args.no_chain and look > 0
+    n_ahead = look * args.group if chain else 0
     n_iso = args.steps if args.schedule == "pipelined" else 0
     n_batches = total + (1 if args.schedule == "stale" else 0) + n_ahead + n_iso
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
@@ -329,7 +333,8 @@ def main():
                 clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
     elif args.schedule == "pipelined":
         pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
-                            group=args.group, side_streams=args.side_streams, group_dedup=args.dedup == "group")
+                            group=args.group, side_streams=args.side_streams, group_dedup=args.dedup == "group",
+                            depth=args.depth)
 
         def run_steps(idx, ahead=None):
             pipe.run([(dev_batches[i][0], out, dev_batches[i][1]) for i in idx], sp,
@@ -611,10 +616,12 @@ def main():
                    "staleness": 1 if args.schedule == "stale" else 0,
                    "group": args.group if args.schedule == "pipelined" else None,
                    "chained": chain,
+                   "depth": args.depth if args.schedule == "pipelined" else None,
+                   "look_ahead_groups": look if chain else 0,
                    "step_accounting": ("chained calls (a training loop's look-ahead): the warm-up call ends with "
-                                       "the dedups of the first timed group, the timed call with those of the "
-                                       "group after it; the timed region holds exactly `steps` dedups and `steps` "
-                                       "forwards, backwards and updates") if chain else None,
+                                       "the dedups of the first timed groups, the timed call with those of the "
+                                       "groups after it; the timed region holds exactly `steps` dedups and "
+                                       "`steps` forwards, backwards and updates") if chain else None,
                    "dedup": args.dedup if args.schedule == "pipelined" else None,
                    "side_streams": (pipe.S if pipe is not None else None),
                    "overlapped_steps": args.steps if args.schedule == "pipelined" else

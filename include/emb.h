@@ -223,20 +223,25 @@ emb_status emb_unique_ids_batched(const emb_tables* tables, int32_t n_batches, c
  * call with group_ws as its workspace (device, group_ws_bytes >=
  * emb_workspace_size of a whole group's ids and bags, initialised by
  * emb_workspace_init); NULL otherwise.
- *   sets:    host [2 * group] buffer sets, used alternately by groups
- *   events:  host [3 + 2 * n_side] hipEvent_t created by the caller (no
- *            timing needed); the library only records and waits on them
+ *   depth:   buffer set parities P (2..8): groups of steps whose dedup
+ *            buffers are in use at once (a group's dedups wait for the main
+ *            stream's group P earlier, whose buffers they reuse)
+ *   sets:    host [depth * group] buffer sets, group g of the call using
+ *            those of parity (group_base + g) % depth
+ *   events:  host [1 + depth + depth * n_side] hipEvent_t created by the
+ *            caller (no timing needed); the library only records and waits
+ *            on them
  *   update:  the optimizer; step k uses update->seed + k for bf16
  *            stochastic rounding
- * Chained calls (a training loop's look-ahead): with ahead = 1, batches
- * holds n_steps + group entries and the call also dedups the last `group`
- * of them (the next call's first group) on the side streams, overlapping
- * its own last group's forward and update; the next call, given primed = 1
- * and those same batches (unchanged) as its first group's, does not dedup
- * them again.  group_base numbers groups across chained calls (the buffer
- * sets of group g of the call are those of parity (group_base + g) % 2): a
- * call's group_base is the previous call's plus its number of groups,
- * ceil(n_steps / group); 0 and primed = ahead = 0 for a call on its own.
+ * Chained calls (a training loop's look-ahead): with ahead = A (0..depth-1),
+ * batches holds n_steps + A * group entries and the call also dedups the
+ * last A * group of them (the next call's first A groups) on the side
+ * streams, overlapping its own last groups' forwards and updates; the next
+ * call, given primed = A and those same batches (unchanged) as its first A
+ * groups' (n_steps >= A * group), does not dedup them again.  group_base
+ * numbers groups across chained calls: a call's group_base is the previous
+ * call's plus its number of groups, ceil(n_steps / group); 0 and
+ * primed = ahead = 0 for a call on its own.
  * All of the side streams' work precedes the end of the work enqueued on
  * main_stream (the look-ahead dedups too), so one synchronisation of
  * main_stream completes every step.
@@ -247,15 +252,16 @@ emb_status emb_unique_ids_batched(const emb_tables* tables, int32_t n_batches, c
  * (the device order is the same as from one thread).  Every step's
  * arguments are checked before anything is enqueued (EMB_EINVAL,
  * EMB_EWORKSPACE, EMB_EUNSUPPORTED as the per-step calls would return, and
- * EMB_EUNSUPPORTED for n_side > 16; EMB_EINVAL for ahead with n_steps =
- * 0); EMB_EHIP (a failed launch or event call) returns with part of the
- * schedule enqueued. */
+ * EMB_EUNSUPPORTED for n_side > 16 or depth > 8; EMB_EINVAL for ahead with
+ * n_steps = 0, depth < 2, primed or ahead outside 0..depth-1, or primed
+ * groups beyond the steps); EMB_EHIP (a failed launch or event call)
+ * returns with part of the schedule enqueued. */
 emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_update* update, int32_t n_steps,
                               const emb_batch* batches, float* const* outs, const float* const* grads,
                               int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,
                               void* const* side_streams, void* const* events, void* group_ws,
                               size_t group_ws_bytes,
-                              int32_t group_base, int32_t primed, int32_t ahead);
+                              int32_t group_base, int32_t primed, int32_t ahead, int32_t depth);
 
 /* Backward segment-reduce (the gradient the embedding stage pushes back,
  * paper: Section "Multi-mode Execution", heterogeneous pipeline paragraph),

@@ -124,7 +124,7 @@ def lib():
         PV = ctypes.POINTER(vp)
         L.emb_pipeline_steps.restype = i32
         L.emb_pipeline_steps.argtypes = [T, i32, Up, i32, B, PV, PV, i32, ctypes.POINTER(CDedupSet), vp, i32, PV, PV,
-                                         vp, sz, i32, i32, i32]
+                                         vp, sz, i32, i32, i32, i32]
         L.emb_unique_ids_batched.restype = i32
         L.emb_unique_ids_batched.argtypes = [T, i32, B, ctypes.POINTER(CDedupSet), vp, sz, vp]
         L.emb_route_ids_noalloc.restype = i32
@@ -558,11 +558,12 @@ class Pipeline:
     never wait); with several side streams the dedups of a group are dealt
     round-robin over them and run concurrently with
     emb_unique_ids_concurrent, in which no workgroup waits for another.
-    Two sets of ``group`` dedup buffers alternate; the side streams overwrite
-    a set only after the main stream's group that read it, so each group
-    costs one cross-stream wait per stream and direction (each costs the host
-    15-25 us on ROCm while its event is pending, hence groups rather than
-    single steps).
+    ``depth`` sets of ``group`` dedup buffers rotate; the side streams
+    overwrite a set only after the main stream's group that read it, so each
+    group costs one cross-stream wait per stream and direction (each costs
+    the host 15-25 us on ROCm while its event is pending, hence groups rather
+    than single steps), and chained calls may look ahead up to ``depth - 1``
+    groups.
 
     This is the paper's embedding stage run ahead of the dense stage
     (Section "Multi-mode Execution", heterogeneous pipeline) with no
@@ -570,10 +571,10 @@ class Pipeline:
 
     def __init__(self, tables: Tables, pool: str, opt: str, lr: float, eps: float = 1e-8, state=None,
                  max_indices: int = 0, max_bags: int = 0, group: int = 4, side_streams: int = 3,
-                 rounding: str = "nearest", seed: int = 0, group_dedup: bool = True):
+                 rounding: str = "nearest", seed: int = 0, group_dedup: bool = True, depth: int = 2):
         import torch
-        if group < 1 or not 1 <= side_streams <= 16:
-            raise ValueError("group must be >= 1 and side_streams in 1..16")
+        if group < 1 or not 1 <= side_streams <= 16 or not 2 <= depth <= 8:
+            raise ValueError("group must be >= 1, side_streams in 1..16 and depth in 2..8")
         if group_dedup and group > 16:
             raise ValueError("a group dedup takes at most 16 batches")
         self.tables, self.pool, self.opt, self.lr, self.eps, self.state = tables, pool, opt, lr, eps, state
@@ -589,14 +590,15 @@ class Pipeline:
                 raise ValueError("a group of batches too large for one dedup")
             self.group_ws = torch.empty(gb, dtype=torch.uint8, device=dev)
             workspace_init(self.group_ws)
-        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(2 * group)]
+        self.depth = depth
+        self.sets = [DedupBuffers(dev, max_indices, max_bags, D) for _ in range(depth * group)]
         self.max_indices = max(1, max_indices)
         self._side_streams = [torch.cuda.Stream(device=dev) for _ in range(self.S)]
         self.sides = [int(x.cuda_stream) for x in self._side_streams]
         # events the native schedule records and waits on: the start, the main
         # stream's group done (per set parity), each side stream's group done
         # (per parity and stream)
-        self._events = [_Hip.event() for _ in range(3 + 2 * self.S)]
+        self._events = [_Hip.event() for _ in range(1 + depth + depth * self.S)]
         self._events_c = (ctypes.c_void_p * len(self._events))(*self._events)
         self._sides_c = (ctypes.c_void_p * self.S)(*self.sides)
         self._sets_c = (CDedupSet * len(self.sets))(*[
@@ -628,27 +630,30 @@ class Pipeline:
         step's results are complete when ``stream`` reaches the end of the
         enqueued work; the side streams' work all precedes it.
 
-        ``ahead``: the next call's first ``group`` batches (a training loop's
-        look-ahead).  Their dedups are enqueued at the end of this call,
-        beside its last group's forward and update, and the next call, whose
-        first steps must use exactly these batches (unchanged), starts with
-        them done.  A call that starts with other batches raises; ``discard``
-        drops the look-ahead instead."""
+        ``ahead``: the next call's first batches, ``A * group`` of them for
+        A in 1..depth-1 (a training loop's look-ahead).  Their dedups are
+        enqueued at the end of this call, beside its last groups' forwards and
+        updates, and the next call, whose first steps must use exactly these
+        batches (unchanged), starts with them done.  A call that starts with
+        other batches raises; ``discard`` drops the look-ahead instead."""
         steps = list(steps)
         n = len(steps)
+        n_ahead = 0
         if ahead is not None:
             ahead = list(ahead)
-            if n == 0 or len(ahead) != self.K:
-                raise ValueError(f"ahead takes the next call's first {self.K} batches, after at least one step")
+            n_ahead = len(ahead) // self.K
+            if n == 0 or n_ahead < 1 or n_ahead >= self.depth or len(ahead) != n_ahead * self.K:
+                raise ValueError(f"ahead takes the next call's first A * {self.K} batches, A in 1..{self.depth - 1}, "
+                                 "after at least one step")
         if n == 0:
             return
         primed = 0
         if self._primed is not None:
-            first = [b for b, _, _ in steps[:self.K]]
+            first = [b for b, _, _ in steps[:len(self._primed)]]
             if len(first) != len(self._primed) or any(x is not y for x, y in zip(first, self._primed)):
                 raise ValueError("the first steps are not the batches deduplicated ahead by the last call "
                                  "(call discard() to drop them)")
-            primed = 1
+            primed = len(self._primed) // self.K
         cbs = [b.c() for b, _, _ in steps]
         if ahead:
             cbs += [b.c() for b in ahead]
@@ -669,7 +674,7 @@ class Pipeline:
         _check("emb_pipeline_steps", lib().emb_pipeline_steps(
             self._ct, self._pool, ctypes.byref(self._updc), n, batches, outs, grads, self.K, self._sets_c,
             _stream(stream), self.S, self._sides_c, self._events_c, _ptr(gws),
-            gws.numel() if gws is not None else 0, self._group_base % 2, primed, 1 if ahead else 0))
+            gws.numel() if gws is not None else 0, self._group_base % self.depth, primed, n_ahead, self.depth))
         self.steps_done += n
         self._group_base += (n + self.K - 1) // self.K
         self._primed = ahead

@@ -17,22 +17,23 @@
 //     enqueued; the main stream's waits for group g are enqueued only once
 //     every side_done[s] > g.
 //   main_done: groups whose main-stream record is enqueued; the dedups of
-//     group g >= 2 (which reuse the buffer sets of group g - 2) are enqueued
-//     only once main_done >= g - 1, after their wait for that record.
+//     group g >= P (which reuse the buffer sets of group g - P; P = depth,
+//     the number of buffer set parities) are enqueued only once
+//     main_done >= g - P + 1, after their wait for that record.
 // The side thread re-records the events of a parity only after the main
-// thread has enqueued its wait on the previous record (main_done >= g - 1
-// implies the main stream's wait for group g - 2 is enqueued), so no wait
+// thread has enqueued its wait on the previous record (main_done >= g - P + 1
+// implies the main stream's wait for group g - P is enqueued), so no wait
 // ever attaches to a later record, which could make the two streams wait
 // for each other.
 //
 // Calls can be chained (a training loop's look-ahead): a call may end with
-// the dedups of the group of batches after its steps (ahead), into the
-// buffer sets the next call's first group reads, and the next call then
+// the dedups of the A < P groups of batches after its steps (ahead), into
+// the buffer sets the next call's first groups read, and the next call then
 // starts with those dedups already enqueued (primed).  Groups are numbered
-// across calls (group_base) so that buffer parities alternate across the
+// across calls (group_base) so that buffer parities rotate across the
 // boundary; the look-ahead dedups wait like any others for the main stream's
-// group of the same parity, and the next call's first group waits for them
-// through the same event.  Every side stream of a call still starts after
+// group of the same parity, and the next call's first groups wait for them
+// through the same events.  Every side stream of a call still starts after
 // the work already on the main stream, so the batches it reads may be
 // written there until the call that dedups them.
 #include <atomic>
@@ -45,6 +46,7 @@
 namespace {
 
 constexpr int kMaxSideStreams = 16;  // one host thread each
+constexpr int kMaxDepth = 8;         // buffer set parities
 
 struct Schedule {
   const emb_tables* tables;
@@ -57,22 +59,24 @@ struct Schedule {
   const emb_dedup_set* sets;
   hipStream_t main;
   void* const* sides;
-  hipEvent_t ev_start, ev_main[2];
-  void* const* events;
+  hipEvent_t ev_start;
+  void* const* events;  // [1 + depth + depth * n_side]: start, main per parity, side per parity and stream
   void* group_ws;  // non-null: each group's dedups as one emb_unique_ids_batched call
   size_t group_ws_bytes;
+  int32_t depth;       // buffer set parities (groups whose sets are in use at once)
   int32_t group_base;  // this call's first group in the numbering across calls (buffer parity)
-  int32_t primed;      // 1: the first group's dedups were enqueued by the previous call
-  int32_t ahead;       // 1: also dedup the group of K batches after the steps (batches[n_steps...])
+  int32_t primed;      // the first groups whose dedups were enqueued by the previous call
+  int32_t ahead;       // groups of K batches after the steps (batches[n_steps...]) also deduped
 
-  hipEvent_t ev_side(int parity, int s) const { return (hipEvent_t)events[3 + parity * n_side + s]; }
+  hipEvent_t ev_main(int parity) const { return (hipEvent_t)events[1 + parity]; }
+  hipEvent_t ev_side(int parity, int s) const { return (hipEvent_t)events[1 + depth + parity * n_side + s]; }
   hipStream_t side(int s) const { return (hipStream_t)sides[s]; }
-  int parity(int g) const { return (group_base + g) & 1; }
-  // group g < ngroups: steps [g K, min(g K + K, n_steps)); group ngroups
-  // (with ahead): the K look-ahead batches
-  int start(int g) const { return g < ngroups ? g * K : n_steps; }
+  int parity(int g) const { return (group_base + g) % depth; }
+  // group g < ngroups: steps [g K, min(g K + K, n_steps)); group ngroups + j
+  // (j < ahead): the j-th K look-ahead batches
+  int start(int g) const { return g < ngroups ? g * K : n_steps + (g - ngroups) * K; }
   int count(int g) const { return g < ngroups ? (n_steps - g * K < K ? n_steps - g * K : K) : K; }
-  int side_first() const { return primed ? 1 : 0; }
+  int side_first() const { return primed; }
   int side_end() const { return ngroups + ahead; }
 };
 
@@ -87,13 +91,14 @@ emb_status dedup_one(const Schedule& c, int k, const emb_dedup_set& d, void* str
             d.ws_bytes, stream);
 }
 
-// side stream s's part of group g: (for g >= 2) its wait for the main
-// stream's group g - 2, the dedups of the group dealt to it (i % n_side == s)
-// into the buffer sets of the group's parity, and its record (groups 0 and 1
-// follow the call's start, and so every earlier group of the main stream)
+// side stream s's part of group g: (for g >= depth) its wait for the main
+// stream's group g - depth, the dedups of the group dealt to it
+// (i % n_side == s) into the buffer sets of the group's parity, and its
+// record (groups below depth follow the call's start, and so every earlier
+// group of the main stream)
 emb_status side_group(const Schedule& c, int g, int s) {
   const int par = c.parity(g);
-  if (g >= 2 && hipStreamWaitEvent(c.side(s), c.ev_main[par], 0) != hipSuccess) return EMB_EHIP;
+  if (g >= c.depth && hipStreamWaitEvent(c.side(s), c.ev_main(par), 0) != hipSuccess) return EMB_EHIP;
   if (c.group_ws != nullptr) {
     // a group of one batch: its own dedup (one dedup in flight on this
     // stream, beside kernels that never wait)
@@ -146,7 +151,7 @@ emb_status main_group_rest(const Schedule& c, int g) {
                            d.num_unique, nullptr, &u, d.ws, d.ws_bytes, c.main);
     if (st != EMB_OK) return st;
   }
-  return hip_ok(hipEventRecord(c.ev_main[par], c.main));
+  return hip_ok(hipEventRecord(c.ev_main(par), c.main));
 }
 
 emb_status main_group(const Schedule& c, int g) {
@@ -154,25 +159,27 @@ emb_status main_group(const Schedule& c, int g) {
   return st == EMB_OK ? main_group_rest(c, g) : st;
 }
 
-// the main stream's last wait of a call with look-ahead dedups: for them, so
+// the main stream's last waits of a call with look-ahead dedups: for them, so
 // that the end of the main stream's work is the end of all the call's work
 emb_status main_join_ahead(const Schedule& c) {
-  if (!c.ahead) return EMB_OK;
-  for (int s = 0; s < c.n_side; ++s)
-    if (hipStreamWaitEvent(c.main, c.ev_side(c.parity(c.ngroups), s), 0) != hipSuccess) return EMB_EHIP;
+  for (int j = 0; j < c.ahead; ++j)
+    for (int s = 0; s < c.n_side; ++s)
+      if (hipStreamWaitEvent(c.main, c.ev_side(c.parity(c.ngroups + j), s), 0) != hipSuccess) return EMB_EHIP;
   return EMB_OK;
 }
 
-// single thread: the side streams' part of group g + 1 is enqueued before the
-// main stream's part of group g
-// from group g_first on, the side streams' part of group g_first already
-// enqueued: each next group's side part, then this group's main part
-emb_status run_single_from(const Schedule& c, int g_first) {
+// single thread, from the main stream's group g_first on, with the side
+// streams' part of every group below next_side enqueued (or primed): the side
+// part of each group up to g + 1 before the main stream's part of group g,
+// then the side part of the remaining look-ahead groups
+emb_status run_single_from(const Schedule& c, int g_first, int next_side) {
   emb_status st = EMB_OK;
   for (int g = g_first; g < c.ngroups && st == EMB_OK; ++g) {
-    if (g + 1 < c.side_end() && (st = side_group_all(c, g + 1)) != EMB_OK) break;
-    st = main_group(c, g);
+    for (; next_side <= g + 1 && next_side < c.side_end() && st == EMB_OK; ++next_side)
+      st = side_group_all(c, next_side);
+    if (st == EMB_OK) st = main_group(c, g);
   }
+  for (; next_side < c.side_end() && st == EMB_OK; ++next_side) st = side_group_all(c, next_side);
   return st == EMB_OK ? main_join_ahead(c) : st;
 }
 
@@ -187,7 +194,7 @@ emb_status run_single(const Schedule& c) {
   for (int s = 0; s < c.n_side; ++s)
     if (side_wait_start(c, s) != EMB_OK) return EMB_EHIP;
   const emb_status st = c.side_first() == 0 ? side_group_all(c, 0) : EMB_OK;
-  return st == EMB_OK ? run_single_from(c, 0) : st;
+  return st == EMB_OK ? run_single_from(c, 0, c.side_first() > 1 ? c.side_first() : 1) : st;
 }
 
 bool await_count(const std::atomic<int>& n, int v, const std::atomic<int>& failed) {
@@ -216,7 +223,7 @@ emb_status run_threaded(const Schedule& c) {
     }
     for (int g = c.side_first(); g < c.side_end(); ++g) {
       if (failed.load(std::memory_order_acquire)) return;
-      if (g >= 2 && !await_count(main_done, g - 1, failed)) return;
+      if (g >= c.depth && !await_count(main_done, g - c.depth + 1, failed)) return;
       side_st[s] = side_group(c, g, s);
       if (side_st[s] != EMB_OK) {
         failed.store(1, std::memory_order_release);
@@ -228,8 +235,8 @@ emb_status run_threaded(const Schedule& c) {
   // With the first group's dedups enqueued by the previous call, its main
   // stream work goes first, before any helper thread starts: the device then
   // has work at once instead of after the helpers' first launches (launches
-  // from several threads take turns).  The helpers' first group (1) waits for
-  // nothing of the main stream's.
+  // from several threads take turns).  The helpers' first group (primed)
+  // waits for nothing of the main stream's (primed < depth).
   emb_status st = EMB_OK;
   int g_first = 0;
   if (c.primed) {
@@ -252,10 +259,10 @@ emb_status run_threaded(const Schedule& c) {
     if (g_first == 0) return run_single(c);
     for (int s = 0; s < c.n_side; ++s)
       if (side_wait_start(c, s) != EMB_OK) return EMB_EHIP;
-    // the primed first group's main stream work is enqueued: the side
-    // streams' group 1, then the rest in the single-thread order
-    st = 1 < c.side_end() ? side_group_all(c, 1) : EMB_OK;
-    return st == EMB_OK ? run_single_from(c, 1) : st;
+    // the primed first group's main stream work is enqueued: the rest in
+    // the single-thread order, the side streams' from the first group not
+    // primed
+    return run_single_from(c, 1, c.side_first());
   }
   for (int g = g_first; g < c.ngroups && st == EMB_OK; ++g) {
     if ((st = main_first_forward(c, g)) != EMB_OK) {
@@ -273,7 +280,7 @@ emb_status run_threaded(const Schedule& c) {
   }
   if (st == EMB_OK && c.ahead) {
     for (int s = 0; s < c.n_side; ++s)
-      if (!await_count(side_done[s], c.ngroups + 1, failed)) st = EMB_EHIP;
+      if (!await_count(side_done[s], c.side_end(), failed)) st = EMB_EHIP;
     if (st == EMB_OK) st = main_join_ahead(c);
   }
   for (int s = 0; s < c.n_side; ++s) helpers[s].join();
@@ -290,18 +297,21 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
                               const emb_batch* batches, float* const* outs, const float* const* grads,
                               int32_t group, const emb_dedup_set* sets, void* main_stream, int32_t n_side,
                               void* const* side_streams, void* const* events, void* group_ws,
-                              size_t group_ws_bytes, int32_t group_base, int32_t primed, int32_t ahead) {
+                              size_t group_ws_bytes, int32_t group_base, int32_t primed, int32_t ahead,
+                              int32_t depth) {
   if (tables == nullptr || update == nullptr || n_steps < 0 || group < 1 || n_side < 1 || n_side > group ||
-      group_base < 0 || (primed != 0 && primed != 1) || (ahead != 0 && ahead != 1))
+      depth < 2 || group_base < 0 || primed < 0 || primed >= depth || ahead < 0 || ahead >= depth)
     return EMB_EINVAL;
-  if (n_side > kMaxSideStreams) return EMB_EUNSUPPORTED;
+  if (n_side > kMaxSideStreams || depth > kMaxDepth) return EMB_EUNSUPPORTED;
   if (group_ws != nullptr && n_side != 1) return EMB_EINVAL;  // a group's one dedup runs on one stream
   if (group_ws != nullptr && group > emb::kMaxGroup) return EMB_EUNSUPPORTED;
   if (n_steps == 0) return ahead ? EMB_EINVAL : EMB_OK;
+  // the primed groups are whole groups of this call's first steps
+  if ((int64_t)primed * group > n_steps) return EMB_EINVAL;
   if (batches == nullptr || outs == nullptr || grads == nullptr || sets == nullptr || side_streams == nullptr ||
       events == nullptr)
     return EMB_EINVAL;
-  for (int i = 0; i < 3 + 2 * n_side; ++i)
+  for (int i = 0; i < 1 + depth + depth * n_side; ++i)
     if (events[i] == nullptr) return EMB_EINVAL;
   for (int s = 0; s < n_side; ++s)
     if (side_streams[s] == nullptr || side_streams[s] == main_stream) return EMB_EINVAL;
@@ -320,9 +330,8 @@ emb_status emb_pipeline_steps(const emb_tables* tables, int32_t pool, const emb_
   c.main = (hipStream_t)main_stream;
   c.sides = side_streams;
   c.ev_start = (hipEvent_t)events[0];
-  c.ev_main[0] = (hipEvent_t)events[1];
-  c.ev_main[1] = (hipEvent_t)events[2];
   c.events = events;
+  c.depth = depth;
   c.group_ws = group_ws;
   c.group_ws_bytes = group_ws_bytes;
   c.group_base = group_base;

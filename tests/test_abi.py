@@ -205,8 +205,8 @@ def test_pipeline_steps_argument_checks():
     sides = (ctypes.c_void_p * 2)(0x10, 0x20)
     events = (ctypes.c_void_p * 7)(*([0x40] * 7))
     no_events = (ctypes.c_void_p * 7)(*([0x40] * 6 + [0]))
-    def f(*a, group_ws=None, group_ws_bytes=0, group_base=0, primed=0, ahead=0):
-        return L.emb_pipeline_steps(*a, group_ws, group_ws_bytes, group_base, primed, ahead)
+    def f(*a, group_ws=None, group_ws_bytes=0, group_base=0, primed=0, ahead=0, depth=2):
+        return L.emb_pipeline_steps(*a, group_ws, group_ws_bytes, group_base, primed, ahead, depth)
 
     tb, ub = ctypes.byref(t), ctypes.byref(upd)
     assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events) == emb.EMB_OK   # nothing to do
@@ -268,6 +268,15 @@ def test_pipeline_steps_argument_checks():
     assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, ahead=2) == emb.EMB_EINVAL
     assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events, ahead=1) == emb.EMB_EINVAL
     assert f(tb, 0, ub, 0, b, ptrs, ptrs, 1, sets, None, 1, sides, events, primed=1) == emb.EMB_OK
+    # buffer set parities: 2..8; primed and ahead below the depth; primed
+    # groups whole groups of the call's steps
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, depth=1) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, depth=9) == emb.EMB_EUNSUPPORTED
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, depth=3, ahead=3) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, depth=3, primed=2) == emb.EMB_EINVAL
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, events, primed=-1) == emb.EMB_EINVAL
+    ev_d3 = (ctypes.c_void_p * 7)(*([0x40] * 6 + [0]))   # 1 + 3 + 3 events for depth 3 and one side stream
+    assert f(tb, 0, ub, 1, b, ptrs, ptrs, 1, sets, None, 1, sides, ev_d3, depth=3) == emb.EMB_EINVAL
     assert f(tb, 0, ub, 2, bad_b, outs4, grads4, 2, sets4, None, 1, sides, events, ahead=1) == emb.EMB_EINVAL
     assert f(tb, 0, ub, 2, b4, outs4, grads4, 2, small, None, 1, sides, events, ahead=1) == emb.EMB_EWORKSPACE
     # with group base 1 the steps take the last two sets and the look-ahead

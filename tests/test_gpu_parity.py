@@ -647,16 +647,18 @@ def test_stale_schedule_matches_oracle_replay(name, concurrent):
     parity.check_rows(dl, store, touched, w.opt)
 
 
-@pytest.mark.parametrize("group,sides,nsteps,gd", [(1, 1, 5, False), (2, 1, 7, False), (4, 1, 10, False),
-                                                   (2, 2, 7, False), (6, 3, 13, False), (1, 1, 5, True),
-                                                   (2, 1, 7, True), (6, 1, 13, True), (16, 1, 20, True)])
-def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd):
+@pytest.mark.parametrize("group,sides,nsteps,gd,depth", [
+    (1, 1, 5, False, 2), (2, 1, 7, False, 2), (4, 1, 10, False, 2), (2, 2, 7, False, 2), (6, 3, 13, False, 2),
+    (1, 1, 5, True, 2), (2, 1, 7, True, 2), (6, 1, 13, True, 2), (16, 1, 20, True, 2),
+    (1, 1, 9, True, 3), (2, 2, 11, False, 3), (2, 1, 15, True, 5)])
+def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd, depth):
     """The dedups of the next group of batches on a side stream while the main
     stream runs the forward and update of the current group change nothing:
     tables, state and pooled outputs equal those of serial steps bit for bit
     (step counts that leave a partial last group included; gd: each group's
-    dedups as one emb_unique_ids_batched call)."""
-    _say(f"case pipelined vs serial group={group} side streams={sides} steps={nsteps} group dedup={gd}")
+    dedups as one emb_unique_ids_batched call; depth: buffer set parities)."""
+    _say(f"case pipelined vs serial group={group} side streams={sides} steps={nsteps} group dedup={gd} "
+         f"depth={depth}")
     import torch
     import paper_2112_02752_amd as emb
     w = synth.scaled(synth.workload("c3"), rows_div=500, bags_div=8, name="c3-small")
@@ -674,7 +676,7 @@ def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd):
                 layer.step(b, out, g)
         else:
             pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
-                                max_bags=w.num_bags, group=group, side_streams=sides, group_dedup=gd)
+                                max_bags=w.num_bags, group=group, side_streams=sides, group_dedup=gd, depth=depth)
             # two runs: the second starts after everything the first enqueued
             half = nsteps // 2
             pipe.run([(b, o, g) for (b, g), o in zip(dev_b[:half], outs[:half])])
@@ -690,17 +692,22 @@ def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd):
         np.testing.assert_array_equal(a, b)
 
 
-@pytest.mark.parametrize("group,sides,gd,chunks", [(2, 1, True, (3, 4, 2)), (4, 1, True, (5, 8, 4)),
-                                                   (1, 1, False, (2, 3, 1)), (2, 2, False, (4, 3, 2)),
-                                                   (6, 3, False, (7, 6, 6)), (4, 1, True, (4, "discard", 5))])
-def test_pipelined_chained_calls_equal_serial(group, sides, gd, chunks):
+@pytest.mark.parametrize("group,sides,gd,chunks,depth,look", [
+    (2, 1, True, (3, 4, 2), 2, 1), (4, 1, True, (5, 8, 4), 2, 1), (1, 1, False, (2, 3, 1), 2, 1),
+    (2, 2, False, (4, 3, 2), 2, 1), (6, 3, False, (7, 6, 6), 2, 1), (4, 1, True, (4, "discard", 5), 2, 1),
+    # look-ahead of several groups, with as many more buffer set parities
+    (2, 1, True, (3, 5, 4), 3, 2), (4, 1, True, (6, 9, 8), 3, 2), (1, 1, False, (2, 3, 2), 3, 2),
+    (2, 2, False, (5, 7, 6), 4, 3), (2, 1, True, (3, 4, 2), 3, 1), (2, 1, True, (4, "discard", 5), 3, 2)])
+def test_pipelined_chained_calls_equal_serial(group, sides, gd, chunks, depth, look):
     """Chained calls: each call but the last also dedups the next call's
-    first group of batches, and the next call starts with those dedups done
-    (a training loop's look-ahead).  Tables, state and pooled outputs equal
-    those of serial steps bit for bit; a call that starts with other batches
-    than the ones deduplicated ahead is refused; after discard() the next
-    call dedups its own first group."""
-    _say(f"case pipelined chained group={group} side streams={sides} group dedup={gd} chunks={chunks}")
+    first `look` groups of batches, and the next call starts with those
+    dedups done (a training loop's look-ahead; `depth` buffer set parities).
+    Tables, state and pooled outputs equal those of serial steps bit for
+    bit; a call that starts with other batches than the ones deduplicated
+    ahead is refused; after discard() the next call dedups its own first
+    groups."""
+    _say(f"case pipelined chained group={group} side streams={sides} group dedup={gd} chunks={chunks} "
+         f"depth={depth} look-ahead groups={look}")
     import torch
     import paper_2112_02752_amd as emb
     sizes = [c for c in chunks if c != "discard"]
@@ -720,7 +727,7 @@ def test_pipelined_chained_calls_equal_serial(group, sides, gd, chunks):
                 layer.step(b, out, g)
         else:
             pipe = emb.Pipeline(dl.tables, w.pool, w.opt, w.lr, w.eps, dl.state, max_indices=nmax,
-                                max_bags=w.num_bags, group=group, side_streams=sides, group_dedup=gd)
+                                max_bags=w.num_bags, group=group, side_streams=sides, group_dedup=gd, depth=depth)
             k = 0
             for i, c in enumerate(chunks):
                 if c == "discard":
@@ -729,10 +736,10 @@ def test_pipelined_chained_calls_equal_serial(group, sides, gd, chunks):
                 nxt = chunks[i + 1] if i + 1 < len(chunks) else None
                 ahead = None
                 if isinstance(nxt, int):
-                    ahead = [b for b, _ in dev_b[k + c:k + c + group]]
+                    ahead = [b for b, _ in dev_b[k + c:k + c + look * group]]
                 elif nxt == "discard":
                     # dedups ahead of batches that the next call will not start with
-                    ahead = [b for b, _ in dev_b[k + c + 1:k + c + 1 + group]]
+                    ahead = [b for b, _ in dev_b[k + c + 1:k + c + 1 + look * group]]
                 steps = [(b, o, g) for (b, g), o in zip(dev_b[k:k + c], outs[k:k + c])]
                 if k > 0 and pipe._primed is not None:
                     with pytest.raises(ValueError):

@@ -64,7 +64,9 @@ def parse():
                          "least a million lookups, else serial; stale: the asynchronous schedule with "
                          "staleness one (the forward of batch k+1 on a side stream, reading the table before "
                          "the update of batch k, alongside the dedup of batch k)")
-    ap.add_argument("--group", type=int, default=4, help="batches per group of the pipelined schedule")
+    ap.add_argument("--group", type=int, default=None,
+                    help="batches per group of the pipelined schedule (default: the binding's choice for the "
+                         "batch size, emb.pipeline_group)")
     ap.add_argument("--depth", type=int, default=2,
                     help="pipelined: buffer set parities; chained calls look ahead depth - 1 groups")
     ap.add_argument("--no-chain", action="store_true",
@@ -276,14 +278,16 @@ def main():
     # holds exactly `steps` dedups and `steps` forwards, backwards and
     # updates.  The pipelined schedule also runs one call on its own over
     # `steps` batches of their own (isolated_call).
-    look = min(args.depth - 1, args.steps // args.group) if args.schedule == "pipelined" else 0
-    chain = args.schedule == "pipelined" and not args.no_chain and look > 0
-    n_ahead = look * args.group if chain else 0
-    n_iso = args.steps if args.schedule == "pipelined" else 0
-    n_batches = total + (1 if args.schedule == "stale" else 0) + n_ahead + n_iso
     print(f"[bench] {w.name}: {w.description}", file=sys.stderr, flush=True)
     t0 = time.time()
-    batches = [synth.make_batch(w, s) for s in range(n_batches)]
+    first = synth.make_batch(w, 0)
+    group = args.group if args.group else emb.pipeline_group(len(first.indices))
+    look = min(args.depth - 1, args.steps // group) if args.schedule == "pipelined" else 0
+    chain = args.schedule == "pipelined" and not args.no_chain and look > 0
+    n_ahead = look * group if chain else 0
+    n_iso = args.steps if args.schedule == "pipelined" else 0
+    n_batches = total + (1 if args.schedule == "stale" else 0) + n_ahead + n_iso
+    batches = [first] + [synth.make_batch(w, s) for s in range(1, n_batches)]
     print(f"[bench] generated {n_batches} batches in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
     W = torch.empty((w.total_rows, w.dim), dtype=torch.float32 if w.dtype == "fp32" else torch.bfloat16,
                     device=dev)
@@ -333,7 +337,7 @@ def main():
                 clayer.step(dev_batches[i][0], out, dev_batches[i][1], sp)
     elif args.schedule == "pipelined":
         pipe = emb.Pipeline(tables, w.pool, w.opt, w.lr, w.eps, state, max_indices=nmax, max_bags=w.num_bags,
-                            group=args.group, side_streams=args.side_streams, group_dedup=args.dedup == "group",
+                            group=group, side_streams=args.side_streams, group_dedup=args.dedup == "group",
                             depth=args.depth)
 
         def run_steps(idx, ahead=None):
@@ -614,7 +618,7 @@ def main():
                    "bags": w.num_bags, "lookups_per_step": N_avg, "unique_rows_per_step": U_avg,
                    "table_bytes": w.weight_bytes, "schedule": args.schedule,
                    "staleness": 1 if args.schedule == "stale" else 0,
-                   "group": args.group if args.schedule == "pipelined" else None,
+                   "group": group if args.schedule == "pipelined" else None,
                    "chained": chain,
                    "depth": args.depth if args.schedule == "pipelined" else None,
                    "look_ahead_groups": look if chain else 0,

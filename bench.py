@@ -67,8 +67,11 @@ def parse():
     ap.add_argument("--group", type=int, default=None,
                     help="batches per group of the pipelined schedule (default: the binding's choice for the "
                          "batch size, emb.pipeline_group)")
-    ap.add_argument("--depth", type=int, default=2,
-                    help="pipelined: buffer set parities; chained calls look ahead depth - 1 groups")
+    ap.add_argument("--depth", type=int, default=3,
+                    help="pipelined: buffer set parities (groups whose dedup buffers are in use at once; with 3 "
+                         "a chained call's look-ahead dedups need not wait for its last-but-one group)")
+    ap.add_argument("--look", type=int, default=1,
+                    help="pipelined, chained: groups each call dedups ahead for the next (1..depth-1)")
     ap.add_argument("--no-chain", action="store_true",
                     help="pipelined: time one call on its own (its first group's dedups and its last group's "
                          "forward and update not overlapped) instead of a call in a chain of calls")
@@ -273,7 +276,7 @@ def main():
     total = n_warm + args.steps
     # the stale schedule's last timed step runs the forward of one more batch;
     # the chained pipelined schedule's timed call dedups the groups after its
-    # steps (depth - 1 of them, as many as its steps hold), and its own first
+    # steps (`look` of them, below depth and as many as its steps hold), and its own first
     # groups are deduplicated at the end of the warm-up: the timed region
     # holds exactly `steps` dedups and `steps` forwards, backwards and
     # updates.  The pipelined schedule also runs one call on its own over
@@ -282,7 +285,7 @@ def main():
     t0 = time.time()
     first = synth.make_batch(w, 0)
     group = args.group if args.group else emb.pipeline_group(len(first.indices))
-    look = min(args.depth - 1, args.steps // group) if args.schedule == "pipelined" else 0
+    look = min(args.look, args.depth - 1, args.steps // group) if args.schedule == "pipelined" else 0
     chain = args.schedule == "pipelined" and not args.no_chain and look > 0
     n_ahead = look * group if chain else 0
     n_iso = args.steps if args.schedule == "pipelined" else 0

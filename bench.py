@@ -67,7 +67,7 @@ def parse():
     ap.add_argument("--group", type=int, default=None,
                     help="batches per group of the pipelined schedule (default: the binding's choice for the "
                          "batch size, emb.pipeline_group)")
-    ap.add_argument("--depth", type=int, default=3,
+    ap.add_argument("--depth", type=int, default=2,
                     help="pipelined: buffer set parities (groups whose dedup buffers are in use at once; with 3 "
                          "a chained call's look-ahead dedups need not wait for its last-but-one group)")
     ap.add_argument("--look", type=int, default=1,
@@ -446,9 +446,10 @@ def main():
             grp = idx[g0:g0 + pipe.K]
             # the device spins while the host enqueues the group (a batched
             # dedup and two calls per batch take the host longer than the
-            # device), so that the events time the kernels and not the host
+            # device), so that the events time the kernels and not the host:
+            # about 0.2 ms of spin per batch, several times the host's time
             if hasattr(torch.cuda, "_sleep"):
-                torch.cuda._sleep(1 << 20)
+                torch.cuda._sleep((1 << 19) * len(grp))
             eg = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
             eg[0].record(stream)
             emb.unique_ids_batched(tables, [dev_batches[i][0] for i in grp], pipe.sets[:len(grp)], pipe.group_ws,

@@ -198,6 +198,12 @@ class Batch:
         # the C descriptor is built with the batch, not on its first use
         self.c()
 
+    def __setattr__(self, name, value):
+        # assigning a field drops the cached descriptor
+        if name in ("offsets", "indices", "bags_per_table"):
+            self.__dict__["_ckey"] = None
+        object.__setattr__(self, name, value)
+
     def c(self) -> CBatch:
         """The C descriptor; rebuilt if a tensor was replaced or reallocated."""
         idx = self.indices
@@ -205,8 +211,19 @@ class Batch:
         if getattr(self, "_ckey", None) != key:
             n = key[2]
             self._c = CBatch(self.bags_per_table, key[0], key[1] if n else None, n, key[4])
+            self._cb = bytes(self._c)
             self._ckey = key
         return self._c
+
+    def _c_bytes(self) -> bytes:
+        """The descriptor's bytes, for arrays of descriptors: with the fields
+        unassigned since it was built, only a reallocation of a tensor (its
+        address or length) is checked for."""
+        k = self.__dict__.get("_ckey")
+        idx = self.indices
+        if k is None or k[0] != self.offsets.data_ptr() or k[1] != idx.data_ptr() or k[2] != idx.numel():
+            self.c()
+        return self._cb
 
 
 def workspace_size(num_indices: int, num_bags: int, dim: int) -> int:
@@ -665,12 +682,12 @@ class Pipeline:
                 raise ValueError("the first steps are not the batches deduplicated ahead by the last call "
                                  "(call discard() to drop them)")
             primed = len(self._primed) // self.K
-        cbs = [b.c() for b, _, _ in steps]
-        if ahead:
-            cbs += [b.c() for b in ahead]
-        if max(c.num_indices for c in cbs) > self.max_indices:
+        # the descriptors' bytes joined into one array (one copy)
+        bl = [b for b, _, _ in steps] + (ahead if ahead else [])
+        cbs = [b._c_bytes() for b in bl]
+        if max(b._ckey[2] for b in bl) > self.max_indices:
             raise ValueError("batch larger than the pipeline's buffers")
-        batches = (CBatch * len(cbs))(*cbs)
+        batches = (CBatch * len(cbs)).from_buffer_copy(b"".join(cbs))
         ptrs = {}  # outputs are often one tensor for every step
 
         def ptr(t):

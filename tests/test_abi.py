@@ -322,3 +322,37 @@ def test_unique_ids_batched_argument_checks():
     # 2^31 + 1 rows need 32 key bits: no room for a batch index
     wide = _tables(row_offset=(0, (1 << 31) + 1))
     assert f(ctypes.byref(wide), 2, b, sets, 0x800000, gneed, None) == emb.EMB_EUNSUPPORTED
+
+
+def test_pipeline_group_by_batch_size():
+    """Groups of 8 batches, 4 once 8 batches would exceed 2^25 ids."""
+    assert emb.pipeline_group(0) == 8
+    assert emb.pipeline_group(491_724) == 8          # the 50M-row workload
+    assert emb.pipeline_group(1 << 22) == 8          # exactly 2^25 ids in 8 batches
+    assert emb.pipeline_group((1 << 22) + 1) == 4
+    assert emb.pipeline_group(5_484_949) == 4        # the 26-table workload
+
+
+def test_batch_descriptor_follows_its_tensors():
+    """The cached C descriptor of a Batch (and its bytes, which pipelined
+    calls join into one array) follows field assignments, an in-place
+    shrink of the index tensor and a change of index width."""
+    import torch
+    b = emb.Batch(torch.zeros(17, dtype=torch.int32), torch.arange(100, dtype=torch.int32), 16)
+    assert bytes(b.c()) == b._c_bytes()
+    d = emb.CBatch.from_buffer_copy(b._c_bytes())
+    assert (d.num_indices, d.bags_per_table, d.index_bytes) == (100, 16, 4)
+    b.indices = torch.arange(50, dtype=torch.int32)
+    assert emb.CBatch.from_buffer_copy(b._c_bytes()).num_indices == 50
+    b.indices.resize_(40)
+    assert emb.CBatch.from_buffer_copy(b._c_bytes()).num_indices == 40
+    b.bags_per_table = 8
+    assert emb.CBatch.from_buffer_copy(b._c_bytes()).bags_per_table == 8
+    b.indices = torch.arange(30, dtype=torch.int64)
+    d = emb.CBatch.from_buffer_copy(b._c_bytes())
+    assert (d.num_indices, d.index_bytes, d.indices) == (30, 8, b.indices.data_ptr())
+    b.offsets = torch.zeros(9, dtype=torch.int32)
+    assert emb.CBatch.from_buffer_copy(b._c_bytes()).offsets == b.offsets.data_ptr()
+    # an empty batch carries no index pointer
+    e = emb.Batch(torch.zeros(17, dtype=torch.int32), torch.zeros(0, dtype=torch.int32), 16)
+    assert emb.CBatch.from_buffer_copy(e._c_bytes()).indices is None

@@ -694,6 +694,7 @@ def test_pipelined_schedule_equals_serial(group, sides, nsteps, gd, depth):
 
 @pytest.mark.parametrize("group,sides,gd,chunks,depth,look", [
     (2, 1, True, (3, 4, 2), 2, 1), (4, 1, True, (5, 8, 4), 2, 1), (1, 1, False, (2, 3, 1), 2, 1),
+    (8, 1, True, (5, 20, 8), 2, 1),
     (2, 2, False, (4, 3, 2), 2, 1), (6, 3, False, (7, 6, 6), 2, 1), (4, 1, True, (4, "discard", 5), 2, 1),
     # look-ahead of several groups, with as many more buffer set parities
     (2, 1, True, (3, 5, 4), 3, 2), (4, 1, True, (6, 9, 8), 3, 2), (1, 1, False, (2, 3, 2), 3, 2),
@@ -802,7 +803,8 @@ def test_pipelined_chained_bf16_tables_stochastic_rounding():
 
 @pytest.mark.parametrize("name,nsteps,group,sides,gd", [("c3", 6, 4, 1, False), ("c3", 13, 6, 3, False),
                                                         ("c2", 3, 2, 1, False), ("c2", 5, 4, 2, False),
-                                                        ("c3", 13, 6, 1, True), ("c2", 5, 4, 1, True)])
+                                                        ("c3", 13, 6, 1, True), ("c2", 5, 4, 1, True),
+                                                        ("c3", 17, 8, 1, True)])
 def test_pipelined_schedule_full_size(name, nsteps, group, sides, gd):
     """Full-size pipelined steps against the oracle replaying the same steps on
     the rows they touch: every pooled output, the final rows and state, rows

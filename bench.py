@@ -594,7 +594,8 @@ def main():
     dedup_kind = f"emb_unique_ids_batched, groups of {pipe.K}" if group_phases else "emb_unique_ids"
     traffic = counter_traffic(f"{w.name}: {w.description}", dedup_kind)
     dedup_kernels = ("per group of batches: k_prepare_group, then per pass k_tile_counts + k_column_scan + "
-                     "k_sort_pass, then k_split_group, k_uniq_counts_group, k_uniq_scan_group, k_unique_group "
+                     "k_sort_pass (the last writing each batch's share into its own buffers), then "
+                     "k_uniq_counts_group, k_uniq_scan_group, k_unique_group "
                      f"(emb_unique_ids_batched over groups of {pipe.K}; per batch: the group's time over its "
                      "size)") if group_phases else "k_sort_pass x passes + k_unique (emb_unique_ids)"
     phases = {}

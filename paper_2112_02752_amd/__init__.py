@@ -11,6 +11,7 @@ part of a recommendation model, turning sparse ids into dense features
 """
 from __future__ import annotations
 
+import array
 import ctypes
 import os
 from dataclasses import dataclass
@@ -688,15 +689,17 @@ class Pipeline:
         if max(b._ckey[2] for b in bl) > self.max_indices:
             raise ValueError("batch larger than the pipeline's buffers")
         batches = (CBatch * len(cbs)).from_buffer_copy(b"".join(cbs))
-        ptrs = {}  # outputs are often one tensor for every step
-
-        def ptr(t):
-            v = ptrs.get(id(t))
-            if v is None and t is not None:
-                v = ptrs[id(t)] = t.data_ptr()
-            return v
-        outs = (ctypes.c_void_p * n)(*[ptr(o) for _, o, _ in steps])
-        grads = (ctypes.c_void_p * n)(*[ptr(g) for _, _, g in steps])
+        # pointer arrays built as 64-bit integers (0 for an absent tensor), the
+        # output's address taken once while consecutive steps share it
+        ol, gl = [], []
+        last_o, last_p = None, 0
+        for _, o, g in steps:
+            if o is not last_o:
+                last_o, last_p = o, (o.data_ptr() if o is not None else 0)
+            ol.append(last_p)
+            gl.append(g.data_ptr() if g is not None else 0)
+        outs = (ctypes.c_void_p * n).from_buffer(array.array("Q", ol))
+        grads = (ctypes.c_void_p * n).from_buffer(array.array("Q", gl))
         self._updc.seed = self.seed + self.steps_done
         gws = self.group_ws
         _check("emb_pipeline_steps", lib().emb_pipeline_steps(

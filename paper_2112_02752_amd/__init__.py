@@ -633,7 +633,7 @@ class Pipeline:
         self._sets_c = (CDedupSet * len(self.sets))(*[
             CDedupSet(_ptr(b.unique_keys), _ptr(b.counts), _ptr(b.seg_offsets), _ptr(b.sort_perm),
                       _ptr(b.num_unique), _ptr(b.ws), b.ws.numel() * b.ws.element_size()) for b in self.sets])
-        self._status = torch.zeros(4, dtype=torch.int32, device=dev)
+        self._status = torch.zeros((len(self.sets), 4), dtype=torch.int32, device=dev)
         self._ct = ctypes.byref(tables.c())
         self.rounding, self.seed, self.steps_done = rounding, seed, 0
         self._updc = _update(opt, lr, eps, state, rounding, seed)
@@ -717,12 +717,13 @@ class Pipeline:
 
     def status(self, stream=None):
         """Per buffer set, the status of its last step (emb_workspace_status);
-        synchronises."""
-        out = []
-        for b in self.sets:
-            workspace_status(b.ws, self._status, stream)
-            out.append(tuple(int(x) for x in self._status.cpu()))
-        return out
+        synchronises once: every set's status is written on the device, then
+        copied back together."""
+        import torch
+        for i, b in enumerate(self.sets):
+            workspace_status(b.ws, self._status[i], stream)
+        torch.cuda.synchronize(self._status.device)
+        return [tuple(int(x) for x in row) for row in self._status.cpu().tolist()]
 
     def check(self, stream=None) -> None:
         """Raise StepFailed if the last step of any buffer set failed on the
